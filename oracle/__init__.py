@@ -1,0 +1,10 @@
+"""fp64 CPU oracle for verifier-side window scoring.
+
+Test infrastructure only: the test suite, the smoke check and the benchmark's
+CPU-baseline leg are its only users.  It shares no code with the HIP library.
+"""
+from .ipdv_oracle import (  # noqa: F401
+    DRIVER_S, DRIVER_T, SRC_S, SRC_T, SRC_DISCARDED, REPLACEMENT,
+    append_window, gather_sequence, attention_rows, verify_attention,
+    verify_attn_paged, logits_fp64, lmhead_logsoftmax, accept_scan, eq9_stepper,
+)

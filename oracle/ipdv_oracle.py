@@ -1,0 +1,319 @@
+"""fp64 CPU oracle for verifier-side window scoring (Interactive-Policy Distillation).
+
+TEST INFRASTRUCTURE ONLY.  Only the test suite, the smoke check and the
+benchmark's CPU-baseline leg may import or call this module.  It shares no
+code with the HIP library or its Python binding and imports neither.
+
+What it computes, each part written from the paper's definitions:
+
+* ``verify_attn_paged`` -- the verification stage of one fused-engine step
+  (Section 3.2.3, "Fused Inference Engine"): the verifier appends the window's
+  keys/values to its own paged cache and scores every window row in one
+  prefill pass over the resident prefix.  Plain causal softmax attention,
+  evaluated per row and head in fp64.
+* ``lmhead_logsoftmax`` -- the verifier's next-token distribution at each
+  window row: logits, their log-softmax (temperature 1, Appendix A), the
+  proposed token's log-prob (the log q / log pi term of Eq. (4)), the top-K
+  support of Eq. (5) and the entropy.  Top-K is a full stable sort by
+  (logit descending, index ascending).
+* ``accept_scan`` -- the verdict stage (Section 3.2.3) applying the top-K
+  coverage transition of Eq. (9) over a window with the EOS and maximum
+  length rules; ``eq9_stepper`` is a second, token-by-token writing of
+  Eq. (9) used to cross-check it.
+
+Readings where the paper is silent (tie-break, window/row alignment, cache
+rollback lengths, EOS inside a window, length cap) are listed in the
+repository's design notes; each is restated at the function that uses it.
+
+Cache layouts (the library's documented layouts):
+``k_cache[num_pages, Hkv, page_size, D]`` and
+``v_cache[num_pages, Hkv, D, page_size]``.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+DRIVER_S = 0          # the student drives; the teacher verifies
+DRIVER_T = 1          # the teacher drives; the student verifies
+SRC_S = 0             # token emitted from the student's proposal
+SRC_T = 1             # token emitted from the teacher's proposal
+SRC_DISCARDED = 255   # draft not emitted
+
+
+def _f64(x):
+    """Exact upcast of an input array (fp32 / bf16-valued) to fp64."""
+    return np.asarray(x, dtype=np.float64)
+
+
+def _seq_list(n_seq, seq_ids):
+    return list(range(n_seq)) if seq_ids is None else [int(s) for s in seq_ids]
+
+
+# ---------------------------------------------------------------------------
+# Verification stage: append + causal attention over the paged cache
+# ---------------------------------------------------------------------------
+
+def append_window(k_cache, v_cache, k_new, v_new, page_table, ctx_lens, cu_q,
+                  seq_ids=None, n_seq=None):
+    """Write each window row's key/value into the verifier's pages (in place).
+
+    Row i of sequence b is the token at absolute position L_b + i; it goes to
+    page ``page_table[b][(L_b+i) // ps]``, slot ``(L_b+i) % ps`` -- appending
+    externally proposed tokens to a live request's cache (Section 3.2.3).
+    """
+    ps = k_cache.shape[2]
+    n_seq = len(ctx_lens) if n_seq is None else n_seq
+    for b in _seq_list(n_seq, seq_ids):
+        L = int(ctx_lens[b])
+        for i in range(int(cu_q[b + 1]) - int(cu_q[b])):
+            row = int(cu_q[b]) + i
+            pos = L + i
+            page = int(page_table[b][pos // ps])
+            k_cache[page, :, pos % ps, :] = k_new[row]
+            v_cache[page, :, :, pos % ps] = v_new[row]
+
+
+def gather_sequence(k_cache, v_cache, page_table, b, n_tokens):
+    """Keys and values of positions [0, n_tokens) of sequence b, as fp64
+    arrays [n_tokens, Hkv, D]."""
+    ps = k_cache.shape[2]
+    pos = np.arange(n_tokens)
+    pages = np.asarray(page_table[b])[pos // ps].astype(np.int64)
+    slots = pos % ps
+    K = _f64(k_cache[pages, :, slots, :])          # [n, Hkv, D]
+    V = _f64(v_cache[pages, :, :, slots])          # [n, Hkv, D]
+    return K, V
+
+
+def attention_rows(q, K, V, L, scale, Hkv):
+    """Causal attention of k window rows q[k, Hq, D] whose keys are K/V[L+k, Hkv, D].
+
+    Row i sees keys 0 .. L+i inclusive.  Query head h reads KV head
+    h // (Hq/Hkv) (contiguous grouped-query groups).  Softmax is
+    exp(s - max s) / sum, evaluated in fp64.
+    """
+    q = _f64(q)
+    k_rows, Hq, D = q.shape
+    group = Hq // Hkv
+    out = np.zeros((k_rows, Hq, D), np.float64)
+    for i in range(k_rows):
+        n_vis = L + i + 1
+        for h in range(Hq):
+            g = h // group
+            s = (K[:n_vis, g, :] @ q[i, h, :]) * scale
+            p = np.exp(s - s.max())
+            p /= p.sum()
+            out[i, h, :] = p @ V[:n_vis, g, :]
+    return out
+
+
+def verify_attention(q, k_cache, v_cache, page_table, ctx_lens, cu_q, scale,
+                     seq_ids=None, n_seq=None, out=None):
+    """Attention of every window row over its sequence's cache, which must
+    already hold the window (see ``append_window``).  Returns fp64 [T, Hq, D];
+    rows of sequences not in ``seq_ids`` are left as in ``out`` (zeros)."""
+    T, Hq, D = q.shape
+    Hkv = k_cache.shape[1]
+    n_seq = len(ctx_lens) if n_seq is None else n_seq
+    if out is None:
+        out = np.zeros((T, Hq, D), np.float64)
+    for b in _seq_list(n_seq, seq_ids):
+        L = int(ctx_lens[b])
+        r0, r1 = int(cu_q[b]), int(cu_q[b + 1])
+        if r1 == r0:
+            continue
+        K, V = gather_sequence(k_cache, v_cache, page_table, b, L + (r1 - r0))
+        out[r0:r1] = attention_rows(q[r0:r1], K, V, L, scale, Hkv)
+    return out
+
+
+def verify_attn_paged(q, k_new, v_new, k_cache, v_cache, page_table, ctx_lens, cu_q,
+                      scale, seq_ids=None, n_seq=None):
+    """The whole verification-stage attention: append the window to copies of
+    the caches, then attend.  Returns (out fp64 [T,Hq,D], k_cache', v_cache')."""
+    kc = np.array(k_cache, copy=True)
+    vc = np.array(v_cache, copy=True)
+    append_window(kc, vc, k_new, v_new, page_table, ctx_lens, cu_q, seq_ids, n_seq)
+    out = verify_attention(q, kc, vc, page_table, ctx_lens, cu_q, scale, seq_ids, n_seq)
+    return out, kc, vc
+
+
+# ---------------------------------------------------------------------------
+# LM head + vocabulary log-softmax + top-K support
+# ---------------------------------------------------------------------------
+
+def logits_fp64(hidden, W, chunk=16384):
+    """l = h W^T in fp64, [M, V] (W is [V, Hd], the nn.Linear layout)."""
+    h = _f64(hidden)
+    V = W.shape[0]
+    out = np.empty((h.shape[0], V), np.float64)
+    for v0 in range(0, V, chunk):
+        out[:, v0:v0 + chunk] = h @ _f64(W[v0:v0 + chunk]).T
+    return out
+
+
+def lmhead_logsoftmax(hidden, W, prop_tok, K, logits=None):
+    """Verifier outputs for each row: log-softmax, proposal log-prob, top-K.
+
+    Top-K (Eq. (5)) is the first K entries of a stable sort of the row by
+    logit descending, so equal logits keep ascending index order (the paper
+    does not fix the tie-break; lower index wins here).  Argmax is the first
+    entry of that order.  Entropy is -sum_v p_v log p_v.
+
+    Also returns the decision margins used by parity checks:
+    ``argmax_margin`` = l_(1) - l_(2); ``set_margin`` = l_(K) - l_(K+1);
+    ``cover_margin`` = l_prop - l_(K+1) if the proposal is in the top-K,
+    else l_(K) - l_prop (inf where undefined).
+    """
+    l = logits_fp64(hidden, W) if logits is None else _f64(logits)
+    M, V = l.shape
+    Kc = min(int(K), V)
+    mx = l.max(axis=1)
+    lse = mx + np.log(np.exp(l - mx[:, None]).sum(axis=1))
+    logp = l - lse[:, None]
+    prop = np.asarray(prop_tok, np.int64)
+    res = {
+        "lse": lse,
+        "logp_prop": logp[np.arange(M), prop],
+        "argmax": np.zeros(M, np.int64),
+        "topk_idx": np.zeros((M, Kc), np.int64),
+        "topk_logp": np.zeros((M, Kc), np.float64),
+        "entropy": -(np.exp(logp) * logp).sum(axis=1),
+        "argmax_margin": np.full(M, np.inf),
+        "set_margin": np.full(M, np.inf),
+        "cover_margin": np.full(M, np.inf),
+        "covered": np.zeros(M, bool),
+    }
+    for m in range(M):
+        order = np.argsort(-l[m], kind="stable")
+        res["argmax"][m] = order[0]
+        res["topk_idx"][m] = order[:Kc]
+        res["topk_logp"][m] = logp[m, order[:Kc]]
+        if V > 1:
+            res["argmax_margin"][m] = l[m, order[0]] - l[m, order[1]]
+        rank = int(np.nonzero(order == prop[m])[0][0])
+        res["covered"][m] = rank < Kc
+        if 0 < Kc < V:
+            res["set_margin"][m] = l[m, order[Kc - 1]] - l[m, order[Kc]]
+            if rank < Kc:
+                res["cover_margin"][m] = l[m, prop[m]] - l[m, order[Kc]]
+            else:
+                res["cover_margin"][m] = l[m, order[Kc - 1]] - l[m, prop[m]]
+    return res
+
+
+# ---------------------------------------------------------------------------
+# Verdict stage: top-K coverage rule of Eq. (9) over a window
+# ---------------------------------------------------------------------------
+
+def accept_scan(cu_q, prop_tok, topk_idx, K, driver, ctx_lens, seq_lens, eos_id, max_len):
+    """Verdict for every sequence's window (Eq. (9), Section 3.2.3).
+
+    Row i of sequence b scores draft i (``prop_tok[cu_q[b]+i]``), proposed by
+    the driver; covered_i = draft in the verifier's top-K at that row.
+
+    * Driver S (teacher verifies): drafts are accepted (source S) while
+      covered.  The first uncovered draft is a takeover: it is rejected, the
+      teacher will emit a replacement there (sampled later), and the next
+      driver is T.
+    * Driver T (student verifies): drafts are accepted (source T).  The first
+      covered draft is a handback: it is kept, later drafts are discarded and
+      the next driver is S.
+    * EOS: a student EOS ends the request only if covered (else takeover); a
+      teacher EOS is accepted and ends it.  Drafts after it are discarded.
+    * Length cap: draft i needs seq_len + i < max_len; a request whose
+      accepted drafts reach max_len ends (a takeover's replacement is checked
+      by the caller when it is sampled).
+
+    Returns arrays: n_acc, event_row (-1: no transition), next_driver,
+    finished, new_cache_len, and src[T] (0 S, 1 T, 255 discarded).
+    new_cache_len = L_b + n_acc, plus one after a takeover (the rejected
+    row's input token stays cached; the replacement becomes the last token).
+    """
+    cu_q = np.asarray(cu_q, np.int64)
+    B = len(cu_q) - 1
+    T = int(cu_q[-1])
+    n_acc = np.zeros(B, np.int64)
+    event_row = np.full(B, -1, np.int64)
+    next_driver = np.asarray(driver, np.int64).copy()
+    finished = np.zeros(B, np.int64)
+    new_cache_len = np.zeros(B, np.int64)
+    src = np.full(T, SRC_DISCARDED, np.int64)
+    for b in range(B):
+        r0, r1 = int(cu_q[b]), int(cu_q[b + 1])
+        drv = int(driver[b])
+        takeover = False
+        for i in range(r1 - r0):
+            row = r0 + i
+            if int(seq_lens[b]) + i >= int(max_len):
+                finished[b] = 1
+                break
+            tok = int(prop_tok[row])
+            covered = K > 0 and tok in [int(t) for t in topk_idx[row][:K]]
+            if drv == DRIVER_S:
+                if not covered:
+                    event_row[b] = i
+                    next_driver[b] = DRIVER_T
+                    takeover = True
+                    break
+                src[row] = SRC_S
+                n_acc[b] = i + 1
+                stop = tok == eos_id
+            else:
+                src[row] = SRC_T
+                n_acc[b] = i + 1
+                if covered:
+                    event_row[b] = i
+                    next_driver[b] = DRIVER_S
+                stop = covered or tok == eos_id
+            if tok == eos_id or int(seq_lens[b]) + n_acc[b] >= int(max_len):
+                finished[b] = 1
+                stop = True
+            if stop:
+                break
+        new_cache_len[b] = int(ctx_lens[b]) + n_acc[b] + (1 if takeover else 0)
+    return {"n_acc": n_acc, "event_row": event_row, "next_driver": next_driver,
+            "finished": finished, "new_cache_len": new_cache_len, "src": src}
+
+
+REPLACEMENT = -1   # placeholder for the teacher's replacement token
+
+
+def eq9_stepper(drafts, verifier_topk, K, m1, eos_id, room):
+    """Token-by-token iteration of Eq. (9) over one window (second writing).
+
+    ``drafts[t]`` is the driver's proposal at step t and ``verifier_topk[t]``
+    the verifier's support S_t.  Each step emits (x_t, z_t) and sets m_{t+1}
+    by the four cases of Eq. (9).  The remaining drafts were proposed by the
+    old driver, so the walk stops as soon as the driver changes, at an
+    emitted EOS, or when ``room`` tokens have been emitted.  A takeover emits
+    the placeholder REPLACEMENT (the teacher samples it later).
+
+    Returns (emitted tokens, their sources, final driver, finished flag).
+    """
+    m = m1
+    xs, zs = [], []
+    finished = False
+    for t, x_tilde in enumerate(drafts):
+        if len(xs) >= room:
+            finished = True
+            break
+        in_support = x_tilde in list(verifier_topk[t])[:K] if K > 0 else False
+        if m == DRIVER_S and in_support:           # case 1
+            x, z, m_next = x_tilde, SRC_S, DRIVER_S
+        elif m == DRIVER_S:                        # case 2: takeover
+            x, z, m_next = REPLACEMENT, SRC_T, DRIVER_T
+        elif in_support:                           # case 3: handback
+            x, z, m_next = x_tilde, SRC_T, DRIVER_S
+        else:                                      # case 4
+            x, z, m_next = x_tilde, SRC_T, DRIVER_T
+        xs.append(x)
+        zs.append(z)
+        changed = m_next != m
+        m = m_next
+        if x == eos_id or (x != REPLACEMENT and len(xs) >= room):
+            finished = True
+            break
+        if changed:
+            break
+    return xs, zs, m, finished
