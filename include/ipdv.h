@@ -1,0 +1,228 @@
+/*
+ * ipdv.h -- C ABI of the verifier-side window scoring library (libipdv.so)
+ * for AMD Instinct MI355X (gfx950).
+ *
+ * The three entry points are the verifier's calls in one propose-and-verify
+ * step of Interactive-Policy Distillation (Section 3.2.3, "Fused Inference
+ * Engine", and Eq. (9)):
+ *
+ *   verify_attn_paged        -- the verification stage's attention: append the
+ *                               proposer's window to the verifier's own paged
+ *                               KV cache and score every window row in one
+ *                               prefill pass over the resident prefix;
+ *   lmhead_logsoftmax_verify -- the verifier's next-token distribution at each
+ *                               window row (LM head + log-softmax at
+ *                               temperature 1): proposal log-prob, LSE, argmax,
+ *                               top-K support (Eq. (5)) and entropy;
+ *   accept_scan              -- the verdict stage: the top-K coverage rule of
+ *                               Eq. (9) applied as a first-event scan over each
+ *                               window, with the EOS and length rules and the
+ *                               rollback length shared by both caches.
+ *
+ * Conventions common to every entry point:
+ *   - All array arguments are DEVICE pointers owned by the caller (except the
+ *     host-side shape arguments of the *_workspace_size queries).  The library
+ *     allocates no device memory and keeps no state besides a thread-local
+ *     error message.
+ *   - Every call only enqueues work on `hip_stream` (a hipStream_t; NULL = the
+ *     default stream) and returns; it never synchronises.
+ *   - Arrays are dense, row-major, with the shapes given below.  Floating
+ *     inputs are IPDV_F32 (float) or IPDV_BF16 (bfloat16) as `dtype` says;
+ *     arithmetic accumulates in fp32.
+ *   - Return value: IPDV_OK, or a negative ipdv_status when host-side
+ *     validation fails (nothing is launched) or a HIP launch fails.
+ *     ipdv_last_error() then describes the failure.  Nothing is printed and
+ *     nothing aborts.
+ *   - Device data that break the documented contract (page ids, lengths that
+ *     do not fit the page table) give unspecified outputs; the kernels clamp
+ *     every index they read so that no access leaves the caller's buffers.
+ *
+ * Window convention.  Sequence b has L_b = ctx_lens[b] tokens in this
+ * verifier's cache and k_b = cu_q[b+1] - cu_q[b] window rows.  Row i
+ * (0 <= i < k_b, batch row cu_q[b] + i) is the token at absolute position
+ * L_b + i; its output distribution predicts position L_b + i + 1 and scores
+ * proposed token prop_tok[cu_q[b] + i].
+ */
+#ifndef IPDV_H
+#define IPDV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  IPDV_OK = 0,
+  IPDV_EINVAL = -1,        /* null required pointer or out-of-range argument  */
+  IPDV_EUNSUPPORTED = -2,  /* a shape / dtype combination not implemented      */
+  IPDV_EWORKSPACE = -3,    /* workspace null or smaller than the size query    */
+  IPDV_EHIP = -4           /* a HIP launch or runtime call failed              */
+} ipdv_status;
+
+typedef enum { IPDV_F32 = 0, IPDV_BF16 = 1 } ipdv_dtype;
+
+/* Driver codes (accept_scan): who proposed the window. */
+#define IPDV_DRIVER_S 0   /* the student drives; the teacher verifies */
+#define IPDV_DRIVER_T 1   /* the teacher drives; the student verifies */
+
+/* Source labels (accept_scan `src`). */
+#define IPDV_SRC_S 0
+#define IPDV_SRC_T 1
+#define IPDV_SRC_DISCARDED 255
+
+/* Largest supported top-K (the paper sweeps K in {4, 8, 16, 32}). */
+#define IPDV_MAX_K 32
+
+/*
+ * Workspace bytes verify_attn_paged needs for these host-side shape values
+ * (0 if the arguments are invalid).  max_q is an upper bound of k_b over the
+ * sequences of the call; max_pages_per_seq and page_size as passed to
+ * verify_attn_paged.
+ */
+size_t ipdv_attn_workspace_size(int n_seq, int Hq, int Hkv, int D, int max_q,
+                                int max_pages_per_seq, int page_size);
+
+/*
+ * verify_attn_paged -- verification-stage attention over the paged cache
+ * (Section 3.2.3: the verifier evaluates all unverified drafts of its
+ * sub-batch in one prefill pass, computing only the newly appended tokens
+ * while the prefix cache stays resident; the proposer's tokens are appended
+ * to the verifier's live cache).
+ *
+ * For every handled sequence b and window row i, in place:
+ *   1. append: k_cache/v_cache at position L_b + i  <-  k_new/v_new[cu_q[b]+i];
+ *   2. attend: for query head h and KV head g = h / (Hq/Hkv),
+ *        out[cu_q[b]+i, h, :] = softmax_j( scale * q[cu_q[b]+i, h, :] . K_j )
+ *                               . V_j   over keys j = 0 .. L_b + i (inclusive).
+ * Q and K are taken as already position-encoded; no other mask or softcap.
+ *
+ * q       [T, Hq, D]    window queries (dtype)
+ * k_new   [T, Hkv, D]   window keys    (dtype)
+ * v_new   [T, Hkv, D]   window values  (dtype)
+ * k_cache [num_pages, Hkv, page_size, D]   key pages: per KV head, one key
+ *                                          vector per slot (dtype, in/out)
+ * v_cache [num_pages, Hkv, D, page_size]   value pages, channel-major: per
+ *                                          KV head and channel, one value per
+ *                                          slot (dtype, in/out)
+ * page_table [B, max_pages_per_seq] int32  pages of sequence b in order;
+ *                                          position p lives in page
+ *                                          page_table[b][p / page_size], slot
+ *                                          p % page_size.  Entries up to
+ *                                          (L_b + k_b - 1) / page_size must be
+ *                                          valid page ids < num_pages.
+ * ctx_lens [B] int32    L_b (>= 0)
+ * cu_q    [B+1] int32   window row offsets (non-decreasing, cu_q[0] = 0 for the
+ *                       batch; T = cu_q[B])
+ * seq_ids [n_seq] int32 the sequences this call handles (the verifier's
+ *                       sub-batch, Section 3.2.3 groups requests by verifier);
+ *                       NULL = sequences 0 .. n_seq-1.  Rows of other
+ *                       sequences are neither read nor written.
+ * max_q                 >= k_b for every handled sequence (host-side bound)
+ * out     [T, Hq, D]    attention output (dtype)
+ * Hq, Hkv, D            Hq % Hkv == 0; D in {64, 128}
+ * page_size             16, 32 or 64
+ * scale                 softmax scale (normally 1/sqrt(D))
+ * workspace             device buffer of >= ipdv_attn_workspace_size(...)
+ *                       bytes (split-KV partial results); contents on entry
+ *                       are ignored.
+ *
+ * Errors: IPDV_EINVAL (null pointer, n_seq < 0, max_q < 1, bad head counts,
+ * scale not finite), IPDV_EUNSUPPORTED (D, page_size, dtype),
+ * IPDV_EWORKSPACE, IPDV_EHIP.
+ */
+int verify_attn_paged(const void* q, const void* k_new, const void* v_new,
+                      void* k_cache, void* v_cache,
+                      const int32_t* page_table, int max_pages_per_seq,
+                      const int32_t* ctx_lens, const int32_t* cu_q,
+                      const int32_t* seq_ids, int n_seq, int max_q,
+                      void* out,
+                      int Hq, int Hkv, int D, int page_size, int num_pages, float scale,
+                      int dtype, void* workspace, size_t workspace_bytes,
+                      void* hip_stream);
+
+/* Workspace bytes lmhead_logsoftmax_verify needs (0 if invalid). */
+size_t ipdv_lmhead_workspace_size(int M, int Hd, int V, int K);
+
+/*
+ * lmhead_logsoftmax_verify -- the verifier's next-token distribution at each
+ * window row (temperature 1, as in the paper's rollouts, Appendix A), without
+ * writing the logits to memory.
+ *
+ * For row m: logits l = hidden[m] . W^T (W is the [V, Hd] nn.Linear /
+ * tied-embedding layout), LSE = log sum_v exp(l_v), and
+ *   lse[m]        = LSE                                   (fp32)
+ *   logp_prop[m]  = l[prop_tok[m]] - LSE  (the log q or log pi term of Eq. (4))
+ *   argmax[m]     = the first index of the top-K order
+ *   topk_idx[m,:] = Top_K of Eq. (5): the K largest logits, sorted by logit
+ *                   descending, lower index first on equal logits
+ *   topk_logp[m,:]= l[topk_idx] - LSE
+ *   entropy[m]    = -sum_v p_v log p_v  (optional; NULL skips it)
+ * Row m's outputs go to row out_rows[m] of each output array when out_rows is
+ * non-NULL (scatter into batch-wide arrays), else to row m.
+ *
+ * hidden  [M, Hd]   (dtype);   W [V, Hd] (dtype);   prop_tok [M] int32 in [0, V)
+ * out_rows [M] int32 or NULL
+ * lse, logp_prop, entropy: float [rows];  argmax int32 [rows];
+ * topk_idx int32 [rows, K];  topk_logp float [rows, K]
+ * Requirements: M >= 0, Hd % 64 == 0, 1 <= K <= min(IPDV_MAX_K, V).
+ *
+ * Errors: IPDV_EINVAL, IPDV_EUNSUPPORTED (dtype, Hd), IPDV_EWORKSPACE, IPDV_EHIP.
+ */
+int lmhead_logsoftmax_verify(const void* hidden, const void* W,
+                             const int32_t* prop_tok, const int32_t* out_rows,
+                             int M, int Hd, int V, int K,
+                             float* lse, float* logp_prop, int32_t* argmax,
+                             int32_t* topk_idx, float* topk_logp, float* entropy,
+                             int dtype, void* workspace, size_t workspace_bytes,
+                             void* hip_stream);
+
+/*
+ * accept_scan -- the verdict stage (Section 3.2.3) with the top-K coverage
+ * rule of Eq. (9), one window per sequence.
+ *
+ * Row i of sequence b scores draft i = prop_tok[cu_q[b]+i], proposed by the
+ * driver; covered_i = the draft appears in topk_idx[cu_q[b]+i, 0..K-1] (the
+ * verifier's support).
+ *   driver S: drafts are accepted (src S) while covered; the first uncovered
+ *     draft is a takeover (rejected; the teacher emits the replacement later;
+ *     next driver T).
+ *   driver T: drafts are accepted (src T); the first covered draft is a
+ *     handback (kept; later drafts discarded; next driver S).
+ *   EOS: a student EOS ends the request only if covered (else takeover); a
+ *     teacher EOS is accepted and ends it.
+ *   length: draft i needs seq_lens[b] + i < max_len; a request whose accepted
+ *     drafts reach max_len is finished.
+ * Outputs per sequence: n_acc (accepted drafts), event_row (row of the
+ * takeover / handback, -1 if none), next_driver, finished (0/1),
+ * new_cache_len = L_b + n_acc (+1 after a takeover: the rejected row's input
+ * stays cached and the replacement becomes the last token) -- the common
+ * boundary both models' caches roll back to; per row: src (IPDV_SRC_*).
+ *
+ * cu_q [B+1] int32, prop_tok [T] int32, topk_idx [T, K] int32 (K = 0 allowed:
+ * nothing is covered), driver [B] uint8, ctx_lens [B] int32, seq_lens [B]
+ * int32.  Outputs: n_acc, event_row, new_cache_len int32 [B]; next_driver,
+ * finished uint8 [B]; src uint8 [T].
+ *
+ * Errors: IPDV_EINVAL (null pointer, B < 0, K < 0 or K > IPDV_MAX_K), IPDV_EHIP.
+ */
+int accept_scan(const int32_t* cu_q, const int32_t* prop_tok,
+                const int32_t* topk_idx, int K,
+                const uint8_t* driver, const int32_t* ctx_lens, const int32_t* seq_lens,
+                int32_t eos_id, int32_t max_len, int B,
+                int32_t* n_acc, int32_t* event_row, uint8_t* next_driver,
+                uint8_t* finished, int32_t* new_cache_len, uint8_t* src,
+                void* hip_stream);
+
+/* Thread-local description of the last non-OK status ("" if none). */
+const char* ipdv_last_error(void);
+
+/* Library version string. */
+const char* ipdv_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* IPDV_H */

@@ -1,0 +1,164 @@
+// C ABI of libipdv: argument validation, workspace sizing, error reporting and
+// dispatch to the gfx950 kernels.  Declarations and the full contract are in
+// include/ipdv.h.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+
+#include "../../include/ipdv.h"
+#include "kernels.h"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+int fail(int status, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return status;
+}
+
+int ok() {
+  g_err[0] = '\0';
+  return IPDV_OK;
+}
+
+int hip_fail(const char* what, hipError_t e) {
+  return fail(IPDV_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool is_pow2(int x) { return x > 0 && (x & (x - 1)) == 0; }
+
+}  // namespace
+
+namespace ipdv {
+
+// Keys streamed by one wave per split (a multiple of 32).  IPDV_ATTN_SUB
+// overrides the default for tuning sweeps.
+int attn_sub_tokens() {
+  static int v = [] {
+    const char* s = getenv("IPDV_ATTN_SUB");
+    int x = s ? atoi(s) : 0;
+    if (x < 32 || x > 1024 || x % 32 != 0) x = 256;
+    return x;
+  }();
+  return v;
+}
+
+}  // namespace ipdv
+
+extern "C" {
+
+const char* ipdv_last_error(void) { return g_err; }
+
+const char* ipdv_version(void) { return "ipdv 0.1 gfx950"; }
+
+static int attn_shape_check(int n_seq, int Hq, int Hkv, int D, int max_q, int max_pages,
+                            int page_size) {
+  if (n_seq < 0) return fail(IPDV_EINVAL, "n_seq must be >= 0 (got %d)", n_seq);
+  if (Hq <= 0 || Hkv <= 0 || Hq % Hkv != 0)
+    return fail(IPDV_EINVAL, "Hq (%d) must be a positive multiple of Hkv (%d)", Hq, Hkv);
+  if (max_q < 1) return fail(IPDV_EINVAL, "max_q must be >= 1 (got %d)", max_q);
+  if (max_pages < 1) return fail(IPDV_EINVAL, "max_pages_per_seq must be >= 1 (got %d)", max_pages);
+  if (D != 64 && D != 128) return fail(IPDV_EUNSUPPORTED, "head dim D=%d not in {64, 128}", D);
+  if (!is_pow2(page_size) || page_size < 16 || page_size > 64)
+    return fail(IPDV_EUNSUPPORTED, "page_size=%d not in {16, 32, 64}", page_size);
+  if ((long)n_seq * Hkv > 65535) return fail(IPDV_EUNSUPPORTED, "n_seq * Hkv exceeds 65535");
+  if ((long)max_q * (Hq / Hkv) > 64L * 65535) return fail(IPDV_EUNSUPPORTED, "max_q * Hq/Hkv too large");
+  return IPDV_OK;
+}
+
+size_t ipdv_attn_workspace_size(int n_seq, int Hq, int Hkv, int D, int max_q,
+                                int max_pages_per_seq, int page_size) {
+  if (attn_shape_check(n_seq, Hq, Hkv, D, max_q, max_pages_per_seq, page_size) != IPDV_OK) return 0;
+  return ipdv::attn_plan(n_seq, Hq, Hkv, D, max_q, max_pages_per_seq, page_size).workspace_bytes;
+}
+
+int verify_attn_paged(const void* q, const void* k_new, const void* v_new, void* k_cache,
+                      void* v_cache, const int32_t* page_table, int max_pages_per_seq,
+                      const int32_t* ctx_lens, const int32_t* cu_q, const int32_t* seq_ids,
+                      int n_seq, int max_q, void* out, int Hq, int Hkv, int D, int page_size,
+                      int num_pages, float scale, int dtype, void* workspace,
+                      size_t workspace_bytes, void* hip_stream) {
+  int st = attn_shape_check(n_seq, Hq, Hkv, D, max_q, max_pages_per_seq, page_size);
+  if (st != IPDV_OK) return st;
+  if (dtype != IPDV_F32 && dtype != IPDV_BF16) return fail(IPDV_EUNSUPPORTED, "dtype %d", dtype);
+  if (num_pages < 1) return fail(IPDV_EINVAL, "num_pages must be >= 1 (got %d)", num_pages);
+  if (!std::isfinite(scale)) return fail(IPDV_EINVAL, "scale must be finite");
+  if (n_seq == 0) return ok();
+  if (!q || !k_new || !v_new || !k_cache || !v_cache || !page_table || !ctx_lens || !cu_q || !out)
+    return fail(IPDV_EINVAL, "null required pointer");
+  const ipdv::AttnPlan pl = ipdv::attn_plan(n_seq, Hq, Hkv, D, max_q, max_pages_per_seq, page_size);
+  if (!workspace || workspace_bytes < pl.workspace_bytes)
+    return fail(IPDV_EWORKSPACE, "workspace of %zu bytes needed (got %zu)", pl.workspace_bytes,
+                workspace ? workspace_bytes : (size_t)0);
+  ipdv::AttnLaunch L{q, k_new, v_new, k_cache, v_cache, page_table, max_pages_per_seq,
+                     ctx_lens, cu_q, seq_ids, n_seq, out, Hq, Hkv, D, page_size, num_pages,
+                     scale, dtype == IPDV_BF16, workspace};
+  hipError_t e = ipdv::launch_verify_attn(L, pl, reinterpret_cast<hipStream_t>(hip_stream));
+  if (e != hipSuccess) return hip_fail("verify_attn_paged launch", e);
+  return ok();
+}
+
+static int lm_shape_check(int M, int Hd, int V, int K) {
+  if (M < 0) return fail(IPDV_EINVAL, "M must be >= 0 (got %d)", M);
+  if (V < 1) return fail(IPDV_EINVAL, "V must be >= 1 (got %d)", V);
+  if (K < 1 || K > IPDV_MAX_K || K > V)
+    return fail(IPDV_EINVAL, "K=%d must satisfy 1 <= K <= min(%d, V=%d)", K, IPDV_MAX_K, V);
+  if (Hd < 64 || Hd % 64 != 0) return fail(IPDV_EUNSUPPORTED, "Hd=%d must be a positive multiple of 64", Hd);
+  if (M > 2147483647 / 2) return fail(IPDV_EUNSUPPORTED, "M too large");
+  return IPDV_OK;
+}
+
+size_t ipdv_lmhead_workspace_size(int M, int Hd, int V, int K) {
+  if (lm_shape_check(M, Hd, V, K) != IPDV_OK) return 0;
+  return ipdv::lm_plan(M, Hd, V, K, true).workspace_bytes;
+}
+
+int lmhead_logsoftmax_verify(const void* hidden, const void* W, const int32_t* prop_tok,
+                             const int32_t* out_rows, int M, int Hd, int V, int K, float* lse,
+                             float* logp_prop, int32_t* argmax, int32_t* topk_idx,
+                             float* topk_logp, float* entropy, int dtype, void* workspace,
+                             size_t workspace_bytes, void* hip_stream) {
+  int st = lm_shape_check(M, Hd, V, K);
+  if (st != IPDV_OK) return st;
+  if (dtype != IPDV_F32 && dtype != IPDV_BF16) return fail(IPDV_EUNSUPPORTED, "dtype %d", dtype);
+  if (M == 0) return ok();
+  if (!hidden || !W || !prop_tok || !lse || !logp_prop || !argmax || !topk_idx || !topk_logp)
+    return fail(IPDV_EINVAL, "null required pointer");
+  const ipdv::LmPlan pl = ipdv::lm_plan(M, Hd, V, K, dtype == IPDV_BF16);
+  const size_t need = ipdv::lm_plan(M, Hd, V, K, true).workspace_bytes;
+  if (!workspace || workspace_bytes < need)
+    return fail(IPDV_EWORKSPACE, "workspace of %zu bytes needed (got %zu)", need,
+                workspace ? workspace_bytes : (size_t)0);
+  ipdv::LmLaunch L{hidden, W, prop_tok, out_rows, M, Hd, V, K, lse, logp_prop, argmax,
+                   topk_idx, topk_logp, entropy, dtype == IPDV_BF16, workspace};
+  hipError_t e = ipdv::launch_lmhead(L, pl, reinterpret_cast<hipStream_t>(hip_stream));
+  if (e != hipSuccess) return hip_fail("lmhead_logsoftmax_verify launch", e);
+  return ok();
+}
+
+int accept_scan(const int32_t* cu_q, const int32_t* prop_tok, const int32_t* topk_idx, int K,
+                const uint8_t* driver, const int32_t* ctx_lens, const int32_t* seq_lens,
+                int32_t eos_id, int32_t max_len, int B, int32_t* n_acc, int32_t* event_row,
+                uint8_t* next_driver, uint8_t* finished, int32_t* new_cache_len, uint8_t* src,
+                void* hip_stream) {
+  if (B < 0) return fail(IPDV_EINVAL, "B must be >= 0 (got %d)", B);
+  if (K < 0 || K > IPDV_MAX_K) return fail(IPDV_EINVAL, "K=%d must be in [0, %d]", K, IPDV_MAX_K);
+  if (B == 0) return ok();
+  if (!cu_q || !prop_tok || (K > 0 && !topk_idx) || !driver || !ctx_lens || !seq_lens || !n_acc ||
+      !event_row || !next_driver || !finished || !new_cache_len || !src)
+    return fail(IPDV_EINVAL, "null required pointer");
+  ipdv::ScanLaunch L{cu_q, prop_tok, topk_idx, K, driver, ctx_lens, seq_lens, eos_id, max_len,
+                     B, n_acc, event_row, next_driver, finished, new_cache_len, src};
+  hipError_t e = ipdv::launch_accept_scan(L, reinterpret_cast<hipStream_t>(hip_stream));
+  if (e != hipSuccess) return hip_fail("accept_scan launch", e);
+  return ok();
+}
+
+}  // extern "C"

@@ -1,0 +1,92 @@
+// Host-side launch interface between the C ABI (abi.cpp) and the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#define IPDV_MAX_K_DEV 32
+#define IPDV_DRIVER_S_DEV 0
+
+namespace ipdv {
+
+// ---- verification-stage attention ----
+struct AttnPlan {
+  int n_qg;            // 64-row query groups per (sequence, KV head)
+  int qt;              // 16-row MFMA tiles per group (1..4)
+  int sub;             // keys per wave
+  int chunk;           // keys per workgroup
+  int max_chunks;      // chunk slots per group (padded to a multiple of 8)
+  size_t part_o_bytes, part_lse_bytes, workspace_bytes;
+};
+
+struct AttnLaunch {
+  const void* q;
+  const void* k_new;
+  const void* v_new;
+  void* k_cache;
+  void* v_cache;
+  const int32_t* page_table;
+  int max_pages;
+  const int32_t* ctx_lens;
+  const int32_t* cu_q;
+  const int32_t* seq_ids;
+  int n_seq;
+  void* out;
+  int Hq, Hkv, D, page_size, num_pages;
+  float scale;
+  bool dtype_bf16;
+  void* workspace;
+};
+
+int attn_sub_tokens();
+AttnPlan attn_plan(int n_seq, int Hq, int Hkv, int D, int max_q, int max_pages, int page_size);
+hipError_t launch_verify_attn(const AttnLaunch& L, const AttnPlan& pl, hipStream_t st);
+
+// ---- LM head + log-softmax ----
+struct LmPlan {
+  int n_groups, n_vt, n_rt, rb;
+  size_t rec_bytes, workspace_bytes;
+};
+
+struct LmLaunch {
+  const void* hidden;
+  const void* W;
+  const int32_t* prop_tok;
+  const int32_t* out_rows;
+  int M, Hd, V, K;
+  float* lse;
+  float* logp_prop;
+  int32_t* argmax;
+  int32_t* topk_idx;
+  float* topk_logp;
+  float* entropy;
+  bool dtype_bf16;
+  void* workspace;
+};
+
+LmPlan lm_plan(int M, int Hd, int V, int K, bool bf16);
+hipError_t launch_lmhead(const LmLaunch& L, const LmPlan& pl, hipStream_t st);
+
+// ---- verdict scan ----
+struct ScanLaunch {
+  const int32_t* cu_q;
+  const int32_t* prop_tok;
+  const int32_t* topk_idx;
+  int K;
+  const uint8_t* driver;
+  const int32_t* ctx_lens;
+  const int32_t* seq_lens;
+  int32_t eos_id, max_len;
+  int B;
+  int32_t* n_acc;
+  int32_t* event_row;
+  uint8_t* next_driver;
+  uint8_t* finished;
+  int32_t* new_cache_len;
+  uint8_t* src;
+};
+
+hipError_t launch_accept_scan(const ScanLaunch& L, hipStream_t st);
+
+}  // namespace ipdv

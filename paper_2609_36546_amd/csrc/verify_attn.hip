@@ -1,0 +1,566 @@
+// Verification-stage attention for gfx950: fused window append + split-KV
+// multi-token causal grouped-query attention over a paged KV cache, and the
+// split combine.
+//
+// Operation (Section 3.2.3 of the paper: the verifier scores all drafts of
+// its sub-batch in one prefill pass over its resident cache, after the
+// proposer's tokens are appended to it): for sequence b with L cached tokens
+// and a k-row window, row i attends to keys 0 .. L+i of its KV head.
+//
+// The window's keys and values are first appended to the pages by a small
+// kernel, so the attention kernel streams every key the same way.
+//
+// Work decomposition.  The query rows of one (sequence, KV head) -- k window
+// positions x G = Hq/Hkv heads -- are packed position-major into groups of up
+// to 64 rows (four 16-row MFMA tiles), so every key byte streamed from HBM
+// feeds all G heads of all k positions at once.  A workgroup (4 waves) takes
+// one chunk of the key range; each wave streams its quarter in 32-key blocks
+// with the next block's loads in flight while the current one is computed:
+//
+//   S^T[32 keys x 16 rows] = K . Q^T     v_mfma_f32_16x16x32_bf16, A = key rows
+//   online softmax in exp2 units on S^T (a lane owns one query row, so the
+//   running max / sum and the output rescale need no lane exchange besides
+//   the two xor-shuffles of the block max)
+//   O^T[d x 16 rows] += V^T . P^T        A = the channel-major value page rows,
+//                                        B = P^T straight from the S^T layout
+//
+// The value pages are channel-major ([page][head][D][slot]), so the A operand
+// of the PV product -- 8 consecutive keys of one channel -- is one 16-byte
+// load, and P never leaves registers.  MFMA rows of the QK product are
+// permuted (row r <-> key 8(r/4) + 4s + r%4 in sub-tile s) so that each lane
+// ends up holding exactly the 8 consecutive keys its PV operand needs.
+//
+// The four waves of a workgroup merge their partial results through LDS;
+// chunks of one (sequence, head group) are merged by a combine kernel in
+// log-sum-exp form, unless the sequence fits in one chunk (then the
+// workgroup writes the output itself).
+#include "common.h"
+#include "kernels.h"
+
+namespace ipdv {
+namespace {
+
+constexpr int kWaves = 4;
+constexpr int kBlk = 32;      // keys per block
+constexpr int kRows = 64;     // packed query rows per workgroup
+constexpr float kRescaleSlack = 8.0f;  // log2 units a stale running max may lag
+constexpr int kQPad = 8;      // elements of padding per LDS query row (bank spread)
+
+struct AttnParams {
+  const void* q;
+  const void* k_new;
+  const void* v_new;
+  void* k_cache;
+  void* v_cache;
+  const int32_t* page_table;
+  const int32_t* ctx_lens;
+  const int32_t* cu_q;
+  const int32_t* seq_ids;
+  void* out;
+  float* part_o;      // [slots][kRows][D]
+  float* part_lse;    // [slots][kRows]
+  int max_pages;
+  int Hq, Hkv, G;
+  int page_size, log2ps, num_pages;
+  int chunk, sub;     // keys per workgroup chunk / per wave
+  int max_chunks, n_qg;
+  float scale_log2;   // softmax scale * log2(e)
+};
+
+template <typename DT, int D> struct Frags;
+
+template <int D> struct Frags<bf16, D> {
+  static constexpr int KS = D / 32;   // k-steps of the QK product
+  bf16x8 k[2][KS];                    // A operand: key rows of sub-tiles 0/1
+  bf16x8 v[D / 16];                   // A operand: channel rows, 8 keys each
+};
+
+template <int D> struct Frags<float, D> {
+  static constexpr int KS = D / 4;    // v_mfma_f32_16x16x4_f32: one value per lane
+  float k[2][KS];
+  floatx4 v[D / 16][2];
+};
+
+template <typename DT, int D> struct QFrag;
+template <int D> struct QFrag<bf16, D> { bf16x8 q[D / 32]; };
+template <int D> struct QFrag<float, D> { float q[D / 4]; };
+
+__device__ __forceinline__ int clampi(int x, int lo, int hi) { return x < lo ? lo : (x > hi ? hi : x); }
+
+// Loads one 32-key block from the pages (the window has been appended by the
+// time this kernel runs).  TAIL: the block reaches past the last visible key
+// n_keys; value lanes of those keys are zeroed so that masked probabilities
+// never meet stale or poisoned slots (their page-table entries are clamped
+// into the pool, so every load stays in bounds).
+template <typename DT, int D, bool TAIL>
+__device__ __forceinline__ void load_block(const AttnParams& a, Frags<DT, D>& f, int t0, int n_keys,
+                                           int g, int my_page, int pbase) {
+  const int lane = lane_id();
+  const int c16 = lane & 15, j = lane >> 4;
+  // K rows: the lane's key for sub-tile s is t0 + 8*(c16/4) + 4s + c16%4; both
+  // sub-tiles' keys share one 8-aligned group, hence one page.
+  const int kgrp = t0 + 8 * (c16 >> 2);
+  const int kpage = __shfl(my_page, clampi((kgrp >> a.log2ps) - pbase, 0, kWave - 1), kWave);
+  const DT* kbase = reinterpret_cast<const DT*>(a.k_cache) +
+                    (size_t)(kpage * a.Hkv + g) * a.page_size * D;
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    const int pos = kgrp + 4 * s + (c16 & 3);
+    const DT* row = kbase + (pos & (a.page_size - 1)) * D;
+    if constexpr (sizeof(DT) == 2) {
+#pragma unroll
+      for (int ks = 0; ks < D / 32; ++ks) f.k[s][ks] = ld16<bf16x8>(row + 8 * j + 32 * ks);
+    } else {
+#pragma unroll
+      for (int c = 0; c < D / 16; ++c) {
+        floatx4 v = ld16<floatx4>(row + j * (D / 4) + 4 * c);
+        f.k[s][4 * c + 0] = v[0];
+        f.k[s][4 * c + 1] = v[1];
+        f.k[s][4 * c + 2] = v[2];
+        f.k[s][4 * c + 3] = v[3];
+      }
+    }
+  }
+  // V^T rows: channel 16*dt + c16, keys t0 + 8j .. t0 + 8j + 7.
+  const int vpos = t0 + 8 * j;
+  const int vpage = __shfl(my_page, clampi((vpos >> a.log2ps) - pbase, 0, kWave - 1), kWave);
+  const DT* vc = reinterpret_cast<const DT*>(a.v_cache) +
+                 ((size_t)(vpage * a.Hkv + g) * D) * a.page_size + (vpos & (a.page_size - 1));
+#pragma unroll
+  for (int dt = 0; dt < D / 16; ++dt) {
+    const DT* p = vc + (size_t)(16 * dt + c16) * a.page_size;
+    if constexpr (sizeof(DT) == 2) {
+      f.v[dt] = ld16<bf16x8>(p);
+      if constexpr (TAIL) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if (vpos + e >= n_keys) f.v[dt][e] = static_cast<bf16>(0.f);
+      }
+    } else {
+      f.v[dt][0] = ld16<floatx4>(p);
+      f.v[dt][1] = ld16<floatx4>(p + 4);
+      if constexpr (TAIL) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if (vpos + e >= n_keys) f.v[dt][e >> 2][e & 3] = 0.f;
+      }
+    }
+  }
+}
+
+// One 32-key block for every query tile: S^T = K Q^T, online softmax in
+// exp2 units, O^T += V^T P^T.
+template <typename DT, int D, int QT, bool TAIL>
+__device__ __forceinline__ void attend_block(const AttnParams& a, const Frags<DT, D>& f,
+                                             const DT* s_q, const int (&qlimit)[QT],
+                                             int t0, floatx4 (&acc)[QT][D / 16],
+                                             float (&m_run)[QT], float (&l_run)[QT]) {
+  const int lane = lane_id();
+  const int j = lane >> 4, c16 = lane & 15;
+#pragma unroll
+  for (int t = 0; t < QT; ++t) {
+    // B operand (Q^T) of tile t from the LDS copy of the query rows.
+    const DT* qrow = s_q + (16 * t + c16) * (D + kQPad);
+    floatx4 s[2];
+#pragma unroll
+    for (int st = 0; st < 2; ++st) {
+      floatx4 z = {0.f, 0.f, 0.f, 0.f};
+      if constexpr (sizeof(DT) == 2) {
+#pragma unroll
+        for (int ks = 0; ks < D / 32; ++ks) {
+          const bf16x8 qv = *reinterpret_cast<const bf16x8*>(qrow + 8 * j + 32 * ks);
+          z = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f.k[st][ks], qv, z, 0, 0, 0);
+        }
+      } else {
+#pragma unroll
+        for (int ks = 0; ks < D / 4; ++ks)
+          z = __builtin_amdgcn_mfma_f32_16x16x4f32(f.k[st][ks], qrow[j * (D / 4) + ks], z, 0, 0, 0);
+      }
+      s[st] = z;
+    }
+    // s[st][e] is the score of key t0 + 8j + 4st + e for the lane's row.
+    float x[8];
+    float bm = -INFINITY;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      float v = s[e >> 2][e & 3] * a.scale_log2;
+      if (TAIL && (t0 + 8 * j + e) >= qlimit[t]) v = -INFINITY;
+      x[e] = v;
+      bm = fmaxf(bm, v);
+    }
+    bm = wave_max_xor(bm, 16);
+    bm = wave_max_xor(bm, 32);
+    const float m_old = m_run[t];
+    const float m_new = (bm > m_old + kRescaleSlack || m_old == -INFINITY) ? fmaxf(bm, m_old) : m_old;
+    const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
+    if (__any(m_new != m_old)) {
+      const float alpha = fast_exp2(m_old - m_use);
+      l_run[t] *= alpha;
+#pragma unroll
+      for (int dt = 0; dt < D / 16; ++dt) acc[t][dt] *= alpha;
+    }
+    m_run[t] = m_new;
+    float p[8];
+    float ps = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      p[e] = fast_exp2(x[e] - m_use);
+      ps += p[e];
+    }
+    l_run[t] += ps;
+    if constexpr (sizeof(DT) == 2) {
+      bf16x8 pf;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) pf[e] = static_cast<bf16>(p[e]);
+#pragma unroll
+      for (int dt = 0; dt < D / 16; ++dt)
+        acc[t][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f.v[dt], pf, acc[t][dt], 0, 0, 0);
+    } else {
+#pragma unroll
+      for (int dt = 0; dt < D / 16; ++dt)
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          acc[t][dt] = __builtin_amdgcn_mfma_f32_16x16x4f32(f.v[dt][e >> 2][e & 3], p[e],
+                                                             acc[t][dt], 0, 0, 0);
+    }
+  }
+}
+
+// Append: the window's keys / values go to this verifier's pages at
+// positions L .. L+k-1 (one workgroup per sequence and KV head).
+template <typename DT, int D>
+__global__ __launch_bounds__(256) void append_window_kernel(AttnParams a) {
+  const int slot = blockIdx.x / a.Hkv, g = blockIdx.x % a.Hkv;
+  const int b = a.seq_ids ? a.seq_ids[slot] : slot;
+  const int L = max(a.ctx_lens[b], 0);
+  const int r0 = a.cu_q[b];
+  const int kb = a.cu_q[b + 1] - r0;
+  const int* pt_row = a.page_table + (size_t)b * a.max_pages;
+  DT* kc = reinterpret_cast<DT*>(a.k_cache);
+  DT* vc = reinterpret_cast<DT*>(a.v_cache);
+  const DT* kn = reinterpret_cast<const DT*>(a.k_new);
+  const DT* vn = reinterpret_cast<const DT*>(a.v_new);
+  for (int e = threadIdx.x; e < kb * D; e += blockDim.x) {
+    const int i = e / D, d = e % D;
+    const int pos = L + i;
+    const int page = clampi(pt_row[clampi(pos >> a.log2ps, 0, a.max_pages - 1)], 0, a.num_pages - 1);
+    const int sl = pos & (a.page_size - 1);
+    const size_t src = ((size_t)(r0 + i) * a.Hkv + g) * D + d;
+    kc[((size_t)(page * a.Hkv + g) * a.page_size + sl) * D + d] = kn[src];
+    vc[((size_t)(page * a.Hkv + g) * D + d) * a.page_size + sl] = vn[src];
+  }
+}
+
+template <typename DT, int D, int QT>
+__global__ __launch_bounds__(256) void verify_attn_kernel(AttnParams a) {
+  const int c = blockIdx.x, qg = blockIdx.y;
+  const int slot = blockIdx.z / a.Hkv, g = blockIdx.z % a.Hkv;
+  const int b = a.seq_ids ? a.seq_ids[slot] : slot;
+  const int L = max(a.ctx_lens[b], 0);
+  const int r0 = a.cu_q[b];
+  const int kb = a.cu_q[b + 1] - r0;
+  const int G = a.G;
+  const int rows_total = kb * G;
+  const int pr0 = qg * kRows;
+  if (pr0 >= rows_total) return;
+  const int pr_last = min(rows_total, pr0 + kRows) - 1;
+  const int n_keys = L + pr_last / G + 1;
+  const int n_chunks = min((n_keys + a.chunk - 1) / a.chunk, a.max_chunks);
+  const int tid = threadIdx.x;
+  const int w = tid / kWave;
+  const int lane = lane_id();
+  const int c16 = lane & 15, j = lane >> 4;
+  const int* pt_row = a.page_table + (size_t)b * a.max_pages;
+
+  if (c >= n_chunks) return;
+
+  // The group's query rows (shared by the four waves) go to LDS; the same
+  // buffer later holds the cross-wave merge.
+  constexpr int kQBytes = kRows * (D + kQPad) * (int)sizeof(DT);
+  constexpr int kAccBytes = 2 * QT * (D / 16) * kWave * (int)sizeof(floatx4);
+  __shared__ __attribute__((aligned(16))) char s_buf[kQBytes > kAccBytes ? kQBytes : kAccBytes];
+  DT* s_q = reinterpret_cast<DT*>(s_buf);
+  {
+    constexpr int EPL = 16 / (int)sizeof(DT);
+    constexpr int LPR = D / EPL;
+    for (int e = tid; e < kRows * LPR; e += blockDim.x) {
+      const int r = e / LPR, cc = e % LPR;
+      const int pr = pr0 + r;
+      typedef __attribute__((__vector_size__(16))) int i32x4;
+      i32x4 v = {0, 0, 0, 0};
+      if (pr <= pr_last) {
+        const int i = pr / G, hl = pr % G;
+        v = ld16<i32x4>(reinterpret_cast<const DT*>(a.q) + ((size_t)(r0 + i) * a.Hq + g * G + hl) * D + EPL * cc);
+      }
+      *reinterpret_cast<i32x4*>(s_q + r * (D + kQPad) + EPL * cc) = v;
+    }
+  }
+  int qlimit[QT];   // keys < qlimit are visible to the lane's row of tile t
+#pragma unroll
+  for (int t = 0; t < QT; ++t) qlimit[t] = L + min(pr0 + 16 * t + c16, pr_last) / G + 1;
+  __syncthreads();
+
+  floatx4 acc[QT][D / 16];
+  float m_run[QT], l_run[QT];
+#pragma unroll
+  for (int t = 0; t < QT; ++t) {
+    m_run[t] = -INFINITY;
+    l_run[t] = 0.f;
+#pragma unroll
+    for (int dt = 0; dt < D / 16; ++dt) acc[t][dt] = floatx4{0.f, 0.f, 0.f, 0.f};
+  }
+
+  const int t_begin = c * a.chunk + w * a.sub;
+  const int t_end = min(t_begin + a.sub, n_keys);
+  if (t_begin < t_end) {
+    const int pbase = t_begin >> a.log2ps;
+    const int my_page = clampi(pt_row[clampi(pbase + lane, 0, a.max_pages - 1)], 0, a.num_pages - 1);
+    // Full blocks of cached keys, two register sets in ping-pong: the next
+    // block's loads are in flight while the current one is computed.  The
+    // prefetch is unconditional (past the end it re-reads the last block,
+    // an L1/L2 hit) so that the compiler can wait on exactly the older loads.
+    const int main_end = min(t_end, L & ~(kBlk - 1));
+    const int nb = main_end > t_begin ? (main_end - t_begin) / kBlk : 0;
+    if (nb > 0) {
+      Frags<DT, D> fa, fb;
+      load_block<DT, D, false>(a, fa, t_begin, n_keys, g, my_page, pbase);
+      for (int n = 0; n < nb; n += 2) {
+        load_block<DT, D, false>(a, fb, t_begin + kBlk * min(n + 1, nb - 1), n_keys, g, my_page, pbase);
+        attend_block<DT, D, QT, false>(a, fa, s_q, qlimit, t_begin + kBlk * n, acc, m_run, l_run);
+        load_block<DT, D, false>(a, fa, t_begin + kBlk * min(n + 2, nb - 1), n_keys, g, my_page, pbase);
+        if (n + 1 < nb)
+          attend_block<DT, D, QT, false>(a, fb, s_q, qlimit, t_begin + kBlk * (n + 1), acc, m_run, l_run);
+      }
+    }
+    // The block that reaches past the last visible key, or needs the causal mask.
+    for (int t0 = t_begin + kBlk * nb; t0 < t_end; t0 += kBlk) {
+      Frags<DT, D> ft;
+      load_block<DT, D, true>(a, ft, t0, n_keys, g, my_page, pbase);
+      attend_block<DT, D, QT, true>(a, ft, s_q, qlimit, t0, acc, m_run, l_run);
+    }
+  }
+
+  // Row sums are partial per lane group: reduce over the 4 groups.
+#pragma unroll
+  for (int t = 0; t < QT; ++t) {
+    l_run[t] += __shfl_xor(l_run[t], 16, kWave);
+    l_run[t] += __shfl_xor(l_run[t], 32, kWave);
+  }
+
+  // Merge the four waves' partials.
+  __shared__ float s_m[kWaves][kRows];
+  __shared__ float s_l[kWaves][kRows];
+  typedef floatx4 AccBuf[QT][D / 16][kWave];
+  AccBuf* s_acc = reinterpret_cast<AccBuf*>(s_buf);
+  __syncthreads();   // every wave is done reading the query rows
+  if (j == 0) {
+#pragma unroll
+    for (int t = 0; t < QT; ++t) {
+      s_m[w][16 * t + c16] = m_run[t];
+      s_l[w][16 * t + c16] = l_run[t];
+    }
+  }
+  __syncthreads();
+  float l_tot[QT], m_tot[QT];
+#pragma unroll
+  for (int t = 0; t < QT; ++t) {
+    float M = -INFINITY;
+#pragma unroll
+    for (int ww = 0; ww < kWaves; ++ww) M = fmaxf(M, s_m[ww][16 * t + c16]);
+    const float Mu = (M == -INFINITY) ? 0.f : M;
+    float Ls = 0.f;
+#pragma unroll
+    for (int ww = 0; ww < kWaves; ++ww) Ls += s_l[ww][16 * t + c16] * fast_exp2(s_m[ww][16 * t + c16] - Mu);
+    const float f = fast_exp2(m_run[t] - Mu);
+#pragma unroll
+    for (int dt = 0; dt < D / 16; ++dt) acc[t][dt] *= f;
+    l_tot[t] = Ls;
+    m_tot[t] = M;
+  }
+  if (w >= 2) {
+#pragma unroll
+    for (int t = 0; t < QT; ++t)
+#pragma unroll
+      for (int dt = 0; dt < D / 16; ++dt) s_acc[w - 2][t][dt][lane] = acc[t][dt];
+  }
+  __syncthreads();
+  if (w < 2) {
+#pragma unroll
+    for (int t = 0; t < QT; ++t)
+#pragma unroll
+      for (int dt = 0; dt < D / 16; ++dt) acc[t][dt] += s_acc[w][t][dt][lane];
+  }
+  __syncthreads();
+  if (w == 1) {
+#pragma unroll
+    for (int t = 0; t < QT; ++t)
+#pragma unroll
+      for (int dt = 0; dt < D / 16; ++dt) s_acc[0][t][dt][lane] = acc[t][dt];
+  }
+  __syncthreads();
+  if (w != 0) return;
+
+  const bool single = n_chunks == 1;
+  const size_t pslot = (((size_t)slot * a.Hkv + g) * a.n_qg + qg) * a.max_chunks + c;
+#pragma unroll
+  for (int t = 0; t < QT; ++t) {
+    const int pr = pr0 + 16 * t + c16;
+    const float inv = l_tot[t] > 0.f ? 1.f / l_tot[t] : 0.f;
+    floatx4 o[D / 16];
+#pragma unroll
+    for (int dt = 0; dt < D / 16; ++dt) o[dt] = (acc[t][dt] + s_acc[0][t][dt][lane]) * inv;
+    if (pr > pr_last) continue;
+    if (single) {
+      const int i = pr / G, hl = pr % G;
+      DT* orow = reinterpret_cast<DT*>(a.out) + ((size_t)(r0 + i) * a.Hq + g * G + hl) * D;
+#pragma unroll
+      for (int dt = 0; dt < D / 16; ++dt) {
+        if constexpr (sizeof(DT) == 2) {
+          bf16x4 v;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] = static_cast<bf16>(o[dt][e]);
+          *reinterpret_cast<bf16x4*>(orow + 16 * dt + 4 * j) = v;
+        } else {
+          *reinterpret_cast<floatx4*>(orow + 16 * dt + 4 * j) = o[dt];
+        }
+      }
+    } else {
+      float* po = a.part_o + (pslot * kRows + (16 * t + c16)) * D;
+#pragma unroll
+      for (int dt = 0; dt < D / 16; ++dt) *reinterpret_cast<floatx4*>(po + 16 * dt + 4 * j) = o[dt];
+      if (j == 0)
+        a.part_lse[pslot * kRows + 16 * t + c16] =
+            l_tot[t] > 0.f ? m_tot[t] + fast_log2(l_tot[t]) : -INFINITY;
+    }
+  }
+}
+
+// Merge the chunk partials of every (sequence, KV head, row group) that spans
+// more than one chunk: out = sum_c 2^(lse_c - M) o_c / sum_c 2^(lse_c - M).
+template <typename DT, int D>
+__global__ __launch_bounds__(256) void attn_combine_kernel(AttnParams a) {
+  const int qg = blockIdx.x;
+  const int slot = blockIdx.y / a.Hkv, g = blockIdx.y % a.Hkv;
+  const int b = a.seq_ids ? a.seq_ids[slot] : slot;
+  const int L = max(a.ctx_lens[b], 0);
+  const int r0 = a.cu_q[b];
+  const int kb = a.cu_q[b + 1] - r0;
+  const int G = a.G;
+  const int pr0 = qg * kRows;
+  if (pr0 >= kb * G) return;
+  const int pr_last = min(kb * G, pr0 + kRows) - 1;
+  const int n_keys = L + pr_last / G + 1;
+  const int n_chunks = min((n_keys + a.chunk - 1) / a.chunk, a.max_chunks);
+  if (n_chunks <= 1) return;
+  const int r = threadIdx.x / 4;            // packed row within the group
+  const int dq = (threadIdx.x % 4) * (D / 4);
+  const int pr = pr0 + r;
+  if (pr > pr_last) return;
+  const size_t base = (((size_t)slot * a.Hkv + g) * a.n_qg + qg) * a.max_chunks;
+  float M = -INFINITY;
+  for (int cc = 0; cc < n_chunks; ++cc) M = fmaxf(M, a.part_lse[(base + cc) * kRows + r]);
+  const float Mu = (M == -INFINITY) ? 0.f : M;
+  float o[D / 4];
+#pragma unroll
+  for (int e = 0; e < D / 4; ++e) o[e] = 0.f;
+  float wsum = 0.f;
+  for (int cc = 0; cc < n_chunks; ++cc) {
+    const float wgt = fast_exp2(a.part_lse[(base + cc) * kRows + r] - Mu);
+    wsum += wgt;
+    const float* po = a.part_o + ((base + cc) * kRows + r) * D + dq;
+#pragma unroll
+    for (int e = 0; e < D / 4; e += 4) {
+      floatx4 v = ld16<floatx4>(po + e);
+      o[e] += wgt * v[0];
+      o[e + 1] += wgt * v[1];
+      o[e + 2] += wgt * v[2];
+      o[e + 3] += wgt * v[3];
+    }
+  }
+  const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
+  const int i = pr / G, hl = pr % G;
+  DT* orow = reinterpret_cast<DT*>(a.out) + ((size_t)(r0 + i) * a.Hq + g * G + hl) * D + dq;
+#pragma unroll
+  for (int e = 0; e < D / 4; ++e) orow[e] = from_f32<DT>(o[e] * inv);
+}
+
+template <typename DT, int D, int QT>
+hipError_t launch_t(const AttnParams& p, dim3 grid, dim3 cgrid, hipStream_t st) {
+  hipLaunchKernelGGL((append_window_kernel<DT, D>), dim3(cgrid.y), dim3(256), 0, st, p);
+  hipError_t e0 = hipGetLastError();
+  if (e0 != hipSuccess) return e0;
+  hipLaunchKernelGGL((verify_attn_kernel<DT, D, QT>), grid, dim3(256), 0, st, p);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((attn_combine_kernel<DT, D>), cgrid, dim3(256), 0, st, p);
+  return hipGetLastError();
+}
+
+template <typename DT, int D>
+hipError_t launch_d(const AttnParams& p, int qt, dim3 grid, dim3 cgrid, hipStream_t st) {
+  switch (qt) {
+    case 1: return launch_t<DT, D, 1>(p, grid, cgrid, st);
+    case 2: return launch_t<DT, D, 2>(p, grid, cgrid, st);
+    case 3: return launch_t<DT, D, 3>(p, grid, cgrid, st);
+    default: return launch_t<DT, D, 4>(p, grid, cgrid, st);
+  }
+}
+
+}  // namespace
+
+AttnPlan attn_plan(int n_seq, int Hq, int Hkv, int D, int max_q, int max_pages, int page_size) {
+  AttnPlan pl{};
+  const int G = Hq / Hkv;
+  const long rows = (long)max_q * G;
+  pl.n_qg = (int)((rows + kRows - 1) / kRows);
+  pl.qt = rows >= kRows ? 4 : (int)((rows + 15) / 16);
+  pl.sub = attn_sub_tokens();
+  pl.chunk = kWaves * pl.sub;
+  const long max_keys = (long)max_pages * page_size;
+  int mc = (int)((max_keys + pl.chunk - 1) / pl.chunk);
+  mc = (mc + 7) / 8 * 8;   // row groups of one chunk land on one XCD (id % 8)
+  pl.max_chunks = mc;
+  const size_t slots = (size_t)n_seq * Hkv * pl.n_qg * pl.max_chunks;
+  pl.part_o_bytes = slots * kRows * D * sizeof(float);
+  pl.part_lse_bytes = slots * kRows * sizeof(float);
+  pl.workspace_bytes = pl.part_o_bytes + pl.part_lse_bytes + 256;
+  return pl;
+}
+
+hipError_t launch_verify_attn(const AttnLaunch& L, const AttnPlan& pl, hipStream_t st) {
+  AttnParams p{};
+  p.q = L.q;
+  p.k_new = L.k_new;
+  p.v_new = L.v_new;
+  p.k_cache = L.k_cache;
+  p.v_cache = L.v_cache;
+  p.page_table = L.page_table;
+  p.ctx_lens = L.ctx_lens;
+  p.cu_q = L.cu_q;
+  p.seq_ids = L.seq_ids;
+  p.out = L.out;
+  p.part_o = reinterpret_cast<float*>(L.workspace);
+  p.part_lse = reinterpret_cast<float*>(reinterpret_cast<char*>(L.workspace) + pl.part_o_bytes);
+  p.max_pages = L.max_pages;
+  p.Hq = L.Hq;
+  p.Hkv = L.Hkv;
+  p.G = L.Hq / L.Hkv;
+  p.page_size = L.page_size;
+  p.log2ps = __builtin_ctz(L.page_size);
+  p.num_pages = L.num_pages;
+  p.chunk = pl.chunk;
+  p.sub = pl.sub;
+  p.max_chunks = pl.max_chunks;
+  p.n_qg = pl.n_qg;
+  p.scale_log2 = L.scale * 1.4426950408889634f;
+  dim3 grid(pl.max_chunks, pl.n_qg, L.n_seq * L.Hkv);
+  dim3 cgrid(pl.n_qg, L.n_seq * L.Hkv);
+  if (L.dtype_bf16) {
+    return L.D == 64 ? launch_d<bf16, 64>(p, pl.qt, grid, cgrid, st)
+                     : launch_d<bf16, 128>(p, pl.qt, grid, cgrid, st);
+  }
+  return L.D == 64 ? launch_d<float, 64>(p, pl.qt, grid, cgrid, st)
+                   : launch_d<float, 128>(p, pl.qt, grid, cgrid, st);
+}
+
+}  // namespace ipdv

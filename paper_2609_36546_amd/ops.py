@@ -1,0 +1,243 @@
+"""Thin ctypes binding of libipdv.so (argument marshalling only).
+
+Every function takes device tensors, checks dtype / device / contiguity /
+shape, passes raw pointers and the current HIP stream to the C ABI of the
+same name, and raises RuntimeError with the library's message on a non-OK
+status.  All arithmetic runs in the library's gfx950 kernels; there is no
+other path.  Outputs and workspaces can be passed in (to keep a call free of
+allocations) or are allocated here with torch.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+from typing import Optional
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libipdv.so")
+
+IPDV_F32 = 0
+IPDV_BF16 = 1
+MAX_K = 32
+
+_lib = None
+
+
+class IpdvError(RuntimeError):
+    def __init__(self, func: str, status: int, msg: str):
+        super().__init__(f"{func} failed with status {status}: {msg}")
+        self.status = status
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded library (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "`python -m paper_2609_36546_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i32p, u8p, f32p = ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p
+        ci, cf, cs = ctypes.c_int, ctypes.c_float, ctypes.c_size_t
+        L.ipdv_attn_workspace_size.argtypes = [ci] * 7
+        L.ipdv_attn_workspace_size.restype = cs
+        L.verify_attn_paged.argtypes = [vp, vp, vp, vp, vp, i32p, ci, i32p, i32p, i32p, ci, ci, vp,
+                                        ci, ci, ci, ci, ci, cf, ci, vp, cs, vp]
+        L.verify_attn_paged.restype = ci
+        L.ipdv_lmhead_workspace_size.argtypes = [ci] * 4
+        L.ipdv_lmhead_workspace_size.restype = cs
+        L.lmhead_logsoftmax_verify.argtypes = [vp, vp, i32p, i32p, ci, ci, ci, ci, f32p, f32p, i32p,
+                                               i32p, f32p, f32p, ci, vp, cs, vp]
+        L.lmhead_logsoftmax_verify.restype = ci
+        L.accept_scan.argtypes = [i32p, i32p, i32p, ci, u8p, i32p, i32p, ctypes.c_int32,
+                                  ctypes.c_int32, ci, i32p, i32p, u8p, u8p, i32p, u8p, vp]
+        L.accept_scan.restype = ci
+        L.ipdv_last_error.restype = ctypes.c_char_p
+        L.ipdv_version.restype = ctypes.c_char_p
+        _lib = L
+    return _lib
+
+
+def _check(func: str, status: int):
+    if status != 0:
+        raise IpdvError(func, status, lib().ipdv_last_error().decode())
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(device: torch.device):
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _need(t: torch.Tensor, name: str, dtype=None, device=None, ndim=None):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if device is not None and t.device != device:
+        raise ValueError(f"{name} must be on {device} (is on {t.device})")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be a GPU tensor")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype} (is {t.dtype})")
+    if ndim is not None and t.dim() != ndim:
+        raise ValueError(f"{name} must have {ndim} dims (has {t.dim()})")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def _dtype_code(dt: torch.dtype) -> int:
+    if dt == torch.bfloat16:
+        return IPDV_BF16
+    if dt == torch.float32:
+        return IPDV_F32
+    raise ValueError(f"unsupported dtype {dt}")
+
+
+def version() -> str:
+    return lib().ipdv_version().decode()
+
+
+# ---------------------------------------------------------------------------
+
+def attn_workspace_size(n_seq, Hq, Hkv, D, max_q, max_pages, page_size) -> int:
+    return int(lib().ipdv_attn_workspace_size(n_seq, Hq, Hkv, D, max_q, max_pages, page_size))
+
+
+def verify_attn_paged(q, k_new, v_new, k_cache, v_cache, page_table, ctx_lens, cu_q,
+                      max_q: int, seq_ids=None, n_seq: Optional[int] = None,
+                      scale: Optional[float] = None, out=None, workspace=None):
+    """Append the window to the paged cache and attend (see include/ipdv.h).
+
+    q [T,Hq,D], k_new/v_new [T,Hkv,D], k_cache [P,Hkv,ps,D], v_cache [P,Hkv,D,ps]
+    (bf16 or fp32), page_table [B,maxp] int32, ctx_lens [B] int32, cu_q [B+1]
+    int32, seq_ids [n] int32 or None.  Returns out [T,Hq,D].
+    """
+    dev = q.device
+    dt = q.dtype
+    _need(q, "q", dt, dev, 3)
+    T, Hq, D = q.shape
+    _need(k_new, "k_new", dt, dev, 3)
+    _need(v_new, "v_new", dt, dev, 3)
+    Hkv = k_new.shape[1]
+    _need(k_cache, "k_cache", dt, dev, 4)
+    _need(v_cache, "v_cache", dt, dev, 4)
+    P, _, ps, _ = k_cache.shape
+    if tuple(k_cache.shape) != (P, Hkv, ps, D) or tuple(v_cache.shape) != (P, Hkv, D, ps):
+        raise ValueError("k_cache must be [P,Hkv,ps,D] and v_cache [P,Hkv,D,ps]")
+    if tuple(k_new.shape) != (T, Hkv, D) or tuple(v_new.shape) != (T, Hkv, D):
+        raise ValueError("k_new / v_new must be [T,Hkv,D]")
+    _need(page_table, "page_table", torch.int32, dev, 2)
+    _need(ctx_lens, "ctx_lens", torch.int32, dev, 1)
+    _need(cu_q, "cu_q", torch.int32, dev, 1)
+    B = ctx_lens.shape[0]
+    if cu_q.shape[0] != B + 1 or page_table.shape[0] != B:
+        raise ValueError("cu_q must be [B+1] and page_table [B, maxp]")
+    if seq_ids is not None:
+        _need(seq_ids, "seq_ids", torch.int32, dev, 1)
+        n_seq = seq_ids.shape[0] if n_seq is None else n_seq
+    elif n_seq is None:
+        n_seq = B
+    if scale is None:
+        scale = 1.0 / math.sqrt(D)
+    if out is None:
+        out = torch.empty_like(q)
+    else:
+        _need(out, "out", dt, dev, 3)
+    maxp = page_table.shape[1]
+    need = attn_workspace_size(n_seq, Hq, Hkv, D, max_q, maxp, ps)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    st = lib().verify_attn_paged(
+        _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(k_cache), _ptr(v_cache), _ptr(page_table),
+        maxp, _ptr(ctx_lens), _ptr(cu_q), _ptr(seq_ids), n_seq, max_q, _ptr(out),
+        Hq, Hkv, D, ps, P, float(scale), _dtype_code(dt), _ptr(workspace),
+        workspace.numel() * workspace.element_size(), _stream(dev))
+    _check("verify_attn_paged", st)
+    return out
+
+
+def lmhead_workspace_size(M, Hd, V, K) -> int:
+    return int(lib().ipdv_lmhead_workspace_size(M, Hd, V, K))
+
+
+def lmhead_logsoftmax_verify(hidden, W, prop_tok, K: int, out_rows=None, n_out_rows=None,
+                             with_entropy: bool = True, outs=None, workspace=None):
+    """Verifier log-softmax outputs for each row (see include/ipdv.h).
+
+    hidden [M,Hd], W [V,Hd] (bf16 or fp32), prop_tok [M] int32, out_rows [M]
+    int32 or None.  Returns dict lse, logp_prop, argmax, topk_idx, topk_logp,
+    entropy (rows = n_out_rows if out_rows is given, else M).
+    """
+    dev = hidden.device
+    dt = hidden.dtype
+    _need(hidden, "hidden", dt, dev, 2)
+    _need(W, "W", dt, dev, 2)
+    M, Hd = hidden.shape
+    V = W.shape[0]
+    if W.shape[1] != Hd:
+        raise ValueError("W must be [V, Hd]")
+    _need(prop_tok, "prop_tok", torch.int32, dev, 1)
+    if prop_tok.shape[0] != M:
+        raise ValueError("prop_tok must be [M]")
+    if out_rows is not None:
+        _need(out_rows, "out_rows", torch.int32, dev, 1)
+        R = int(n_out_rows)
+    else:
+        R = M
+    if outs is None:
+        outs = {
+            "lse": torch.empty(R, dtype=torch.float32, device=dev),
+            "logp_prop": torch.empty(R, dtype=torch.float32, device=dev),
+            "argmax": torch.empty(R, dtype=torch.int32, device=dev),
+            "topk_idx": torch.empty(R, K, dtype=torch.int32, device=dev),
+            "topk_logp": torch.empty(R, K, dtype=torch.float32, device=dev),
+            "entropy": torch.empty(R, dtype=torch.float32, device=dev) if with_entropy else None,
+        }
+    need = lmhead_workspace_size(M, Hd, V, K)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    st = lib().lmhead_logsoftmax_verify(
+        _ptr(hidden), _ptr(W), _ptr(prop_tok), _ptr(out_rows), M, Hd, V, K,
+        _ptr(outs["lse"]), _ptr(outs["logp_prop"]), _ptr(outs["argmax"]), _ptr(outs["topk_idx"]),
+        _ptr(outs["topk_logp"]), _ptr(outs["entropy"]), _dtype_code(dt), _ptr(workspace),
+        workspace.numel() * workspace.element_size(), _stream(dev))
+    _check("lmhead_logsoftmax_verify", st)
+    return outs
+
+
+def accept_scan(cu_q, prop_tok, topk_idx, K: int, driver, ctx_lens, seq_lens, eos_id: int,
+                max_len: int, outs=None):
+    """Verdict for each sequence's window (see include/ipdv.h).  Returns dict
+    n_acc, event_row, next_driver, finished, new_cache_len, src."""
+    dev = cu_q.device
+    _need(cu_q, "cu_q", torch.int32, dev, 1)
+    B = cu_q.shape[0] - 1
+    _need(prop_tok, "prop_tok", torch.int32, dev, 1)
+    T = prop_tok.shape[0]
+    if K > 0:
+        _need(topk_idx, "topk_idx", torch.int32, dev, 2)
+        if topk_idx.shape[0] != T or topk_idx.shape[1] != K:
+            raise ValueError("topk_idx must be [T, K]")
+    _need(driver, "driver", torch.uint8, dev, 1)
+    _need(ctx_lens, "ctx_lens", torch.int32, dev, 1)
+    _need(seq_lens, "seq_lens", torch.int32, dev, 1)
+    if outs is None:
+        outs = {
+            "n_acc": torch.empty(B, dtype=torch.int32, device=dev),
+            "event_row": torch.empty(B, dtype=torch.int32, device=dev),
+            "next_driver": torch.empty(B, dtype=torch.uint8, device=dev),
+            "finished": torch.empty(B, dtype=torch.uint8, device=dev),
+            "new_cache_len": torch.empty(B, dtype=torch.int32, device=dev),
+            "src": torch.empty(T, dtype=torch.uint8, device=dev),
+        }
+    st = lib().accept_scan(
+        _ptr(cu_q), _ptr(prop_tok), _ptr(topk_idx) if K > 0 else None, K, _ptr(driver),
+        _ptr(ctx_lens), _ptr(seq_lens), int(eos_id), int(max_len), B,
+        _ptr(outs["n_acc"]), _ptr(outs["event_row"]), _ptr(outs["next_driver"]),
+        _ptr(outs["finished"]), _ptr(outs["new_cache_len"]), _ptr(outs["src"]), _stream(dev))
+    _check("accept_scan", st)
+    return outs

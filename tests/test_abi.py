@@ -1,0 +1,109 @@
+"""The C-ABI library loads and exports every symbol include/ipdv.h declares;
+host-side validation returns the documented statuses (no GPU calls)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2609_36546_amd import ops
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ipdv.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b([a-z_][a-z0-9_]*)\s*\(", text)) -
+                  {"sizeof", "defined", "if", "extern"})
+
+
+def test_header_declares_the_three_entry_points():
+    names = declared_functions()
+    for n in ("verify_attn_paged", "lmhead_logsoftmax_verify", "accept_scan"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol():
+    L = ops.lib()
+    for n in declared_functions():
+        assert hasattr(L, n), f"libipdv.so does not export {n}"
+    assert "gfx950" in ops.version()
+
+
+def _attn(**kw):
+    args = dict(q=1, k_new=1, v_new=1, k_cache=1, v_cache=1, page_table=1, maxp=4, ctx=1, cu=1,
+                seq_ids=None, n_seq=2, max_q=4, out=1, Hq=4, Hkv=2, D=64, ps=16, P=8,
+                scale=0.125, dtype=ops.IPDV_BF16, ws=1, wsb=1 << 30, stream=None)
+    args.update(kw)
+    a = args
+    vp = lambda x: None if x is None else ctypes.c_void_p(x)
+    return ops.lib().verify_attn_paged(
+        vp(a["q"]), vp(a["k_new"]), vp(a["v_new"]), vp(a["k_cache"]), vp(a["v_cache"]),
+        vp(a["page_table"]), a["maxp"], vp(a["ctx"]), vp(a["cu"]), vp(a["seq_ids"]), a["n_seq"],
+        a["max_q"], vp(a["out"]), a["Hq"], a["Hkv"], a["D"], a["ps"], a["P"], a["scale"],
+        a["dtype"], vp(a["ws"]), a["wsb"], vp(a["stream"]))
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(D=96), -2), (dict(ps=8), -2), (dict(ps=48), -2), (dict(Hq=6, Hkv=4), -1),
+    (dict(q=None), -1), (dict(max_q=0), -1), (dict(n_seq=-1), -1), (dict(dtype=7), -2),
+    (dict(wsb=10), -3), (dict(ws=None), -3), (dict(scale=float("inf")), -1),
+    (dict(P=0), -1), (dict(maxp=0), -1)])
+def test_attention_argument_errors(kw, status):
+    assert _attn(**kw) == status
+    assert ops.lib().ipdv_last_error().decode() != ""
+
+
+def test_attention_empty_batch_is_ok_without_gpu():
+    assert _attn(n_seq=0, q=None) == 0
+
+
+def test_workspace_size_queries():
+    assert ops.attn_workspace_size(64, 32, 4, 128, 8, 513, 16) > 0
+    assert ops.attn_workspace_size(64, 32, 4, 96, 8, 513, 16) == 0
+    assert ops.lmhead_workspace_size(512, 2048, 151936, 16) > 0
+    assert ops.lmhead_workspace_size(512, 2048, 151936, 33) == 0
+    assert ops.lmhead_workspace_size(8, 100, 1024, 16) == 0
+
+
+def _lm(**kw):
+    a = dict(h=1, W=1, prop=1, rows=None, M=8, Hd=256, V=1024, K=16, lse=1, lp=1, am=1, ti=1, tl=1,
+             ent=None, dtype=ops.IPDV_F32, ws=1, wsb=1 << 30)
+    a.update(kw)
+    vp = lambda x: None if x is None else ctypes.c_void_p(x)
+    return ops.lib().lmhead_logsoftmax_verify(
+        vp(a["h"]), vp(a["W"]), vp(a["prop"]), vp(a["rows"]), a["M"], a["Hd"], a["V"], a["K"],
+        vp(a["lse"]), vp(a["lp"]), vp(a["am"]), vp(a["ti"]), vp(a["tl"]), vp(a["ent"]), a["dtype"],
+        vp(a["ws"]), a["wsb"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(K=0), -1), (dict(K=33), -1), (dict(K=17, V=16), -1), (dict(Hd=100), -2),
+    (dict(M=-1), -1), (dict(V=0), -1), (dict(W=None), -1), (dict(dtype=3), -2),
+    (dict(wsb=0), -3)])
+def test_lmhead_argument_errors(kw, status):
+    assert _lm(**kw) == status
+
+
+def test_lmhead_empty_is_ok_without_gpu():
+    assert _lm(M=0, h=None) == 0
+
+
+def test_scan_argument_errors():
+    L = ops.lib()
+    vp = ctypes.c_void_p
+    args = [vp(1), vp(1), vp(1), 4, vp(1), vp(1), vp(1), 0, 100, 3] + [vp(1)] * 6 + [None]
+    bad_K = list(args)
+    bad_K[3] = 33
+    assert L.accept_scan(*bad_K) == -1
+    bad_B = list(args)
+    bad_B[9] = -2
+    assert L.accept_scan(*bad_B) == -1
+    null_out = list(args)
+    null_out[12] = None
+    assert L.accept_scan(*null_out) == -1
+    empty = list(args)
+    empty[9] = 0
+    assert L.accept_scan(*empty) == 0
