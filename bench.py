@@ -1,0 +1,314 @@
+"""Benchmark of one verify step (attention -> LM head -> accept scan) on MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 3] [--no-cpu]
+
+A step is one pass of the whole verifier-side hot path over one synthetic
+batch: verify_attn_paged (window append, split-KV paged attention, split
+combine), lmhead_logsoftmax_verify (GEMM with fused log-softmax / top-K
+epilogue, merge) and accept_scan, with every input resident in HBM.  The
+default workload is the teacher shape (Qwen3-30B-A3B-like verify layer:
+32 query / 4 KV heads, head dim 128, hidden 2048, vocab 151936; 64 sequences,
+contexts uniform in [1024, 8192], 8-token windows, 16-token pages), random
+synthetic data, seed 0.
+
+Prints one JSON line: verified tokens/s (window rows scored per second), the
+roofline of the dominant kernel (timed with HIP events that the library
+records around each of its kernels) and the fp64 CPU oracle timed on a
+bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+from paper_2609_36546_amd import inputs, ops  # noqa: E402
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+METRIC = "verified tokens/sec at Qwen3-30B-A3B teacher shape; HBM GB/s vs peak"
+KERNELS = ["append", "attention", "combine", "lmhead_gemm", "lmhead_merge", "accept_scan"]
+PROFILES = os.path.join(ROOT, "profiles")
+
+
+def synth_proposals(batch, mdl, dev):
+    """Synthetic proposer for timing runs: per row, the verifier's argmax with
+    probability p_argmax, else a uniform token or a sample of softmax(l/T).
+    Logits from a plain fp32 torch matmul (setup only, outside the timing)."""
+    cfg = batch.cfg
+    M = mdl.hidden.shape[0]
+    out = torch.empty(M, dtype=torch.int64, device=dev)
+    um = torch.from_numpy(batch.u_mode[to_host_rows(mdl)]).to(dev)
+    ut = torch.from_numpy(batch.u_tok[to_host_rows(mdl)]).to(dev)
+    for r0 in range(0, M, 64):
+        l = mdl.hidden[r0:r0 + 64].float() @ mdl.W.float().T
+        am = l.argmax(1)
+        if cfg.alt_mode == "uniform":
+            alt = torch.clamp((ut[r0:r0 + 64] * l.shape[1]).long(), max=l.shape[1] - 1)
+        else:
+            p = torch.softmax(l.double() / cfg.alt_temperature, 1)
+            cdf = p.cumsum(1)
+            alt = torch.searchsorted(cdf, (ut[r0:r0 + 64] * cdf[:, -1]).unsqueeze(1)).squeeze(1)
+            alt = torch.clamp(alt, max=l.shape[1] - 1)
+        out[r0:r0 + 64] = torch.where(um[r0:r0 + 64] < cfg.p_argmax, am, alt)
+    return out.int()
+
+
+def to_host_rows(mdl):
+    return mdl.rows.cpu().numpy().astype(np.int64)
+
+
+class Step:
+    """Device buffers and the launches of one verify step."""
+
+    def __init__(self, batch, dev):
+        self.b = batch
+        cfg = batch.cfg
+        self.dev = dev
+        T = batch.T
+        K = cfg.K
+        self.K = K
+        t = lambda a, dt: torch.from_numpy(np.asarray(a, dt)).to(dev)
+        self.ctx = t(batch.ctx_lens, np.int32)
+        self.cu = t(batch.cu_q, np.int32)
+        self.driver = t(batch.driver, np.uint8)
+        self.seq_lens = t(batch.seq_lens, np.int32)
+        self.max_q = int(batch.k.max())
+        self.prop = torch.zeros(T, dtype=torch.int32, device=dev)
+        self.per_model = []
+        for m in batch.models:
+            if m.hidden.shape[0] == 0:
+                continue
+            p = synth_proposals(batch, m, dev)
+            self.prop[m.rows.long()] = p
+            n_seq = m.seq_ids.shape[0]
+            ws_a = torch.empty(ops.attn_workspace_size(n_seq, m.shape.Hq, m.shape.Hkv, m.shape.D,
+                                                       self.max_q, m.page_table.shape[1],
+                                                       cfg.page_size), dtype=torch.uint8, device=dev)
+            ws_l = torch.empty(ops.lmhead_workspace_size(m.hidden.shape[0], m.shape.hidden,
+                                                         m.shape.vocab, K), dtype=torch.uint8, device=dev)
+            self.per_model.append(dict(m=m, ws_a=ws_a, ws_l=ws_l, prop=p.contiguous(),
+                                       out=torch.empty_like(m.q)))
+        self.outs = {
+            "lse": torch.empty(T, device=dev), "logp_prop": torch.empty(T, device=dev),
+            "argmax": torch.empty(T, dtype=torch.int32, device=dev),
+            "topk_idx": torch.empty(T, K, dtype=torch.int32, device=dev),
+            "topk_logp": torch.empty(T, K, device=dev), "entropy": torch.empty(T, device=dev)}
+        self.scan_outs = None
+
+    def run(self):
+        for pm in self.per_model:
+            m = pm["m"]
+            ops.verify_attn_paged(m.q, m.k_new, m.v_new, m.k_pool, m.v_pool, m.page_table,
+                                  self.ctx, self.cu, self.max_q, seq_ids=m.seq_ids,
+                                  out=pm["out"], workspace=pm["ws_a"])
+            ops.lmhead_logsoftmax_verify(m.hidden, m.W, pm["prop"], self.K, out_rows=m.rows,
+                                         n_out_rows=self.b.T, outs=self.outs, workspace=pm["ws_l"])
+        self.scan_outs = ops.accept_scan(self.cu, self.prop, self.outs["topk_idx"], self.K,
+                                         self.driver, self.ctx, self.seq_lens, self.b.eos_id,
+                                         self.b.max_len, outs=self.scan_outs)
+
+
+def work_per_launch(batch):
+    """Algorithmic bytes and flops of the attention and LM-head GEMM kernels."""
+    res = {"attention": [0.0, 0.0], "lmhead_gemm": [0.0, 0.0]}
+    s = 2 if batch.cfg.dtype == "bf16" else 4
+    for m in batch.models:
+        seqs = m.seq_ids.cpu().numpy()
+        if len(seqs) == 0:
+            continue
+        sh = m.shape
+        L = batch.ctx_lens[seqs].astype(np.float64)
+        k = batch.k[seqs].astype(np.float64)
+        kv = ((L + k) * sh.Hkv * sh.D * 2 * s).sum()
+        qo = (k * sh.Hq * sh.D * 2 * s).sum()
+        res["attention"][0] += kv + qo
+        # each row i attends to L + i + 1 keys: QK^T and PV
+        res["attention"][1] += (4.0 * sh.Hq * sh.D * (k * (L + 1) + k * (k - 1) / 2)).sum()
+        M = float(m.hidden.shape[0])
+        res["lmhead_gemm"][0] += (sh.vocab + M) * sh.hidden * s
+        res["lmhead_gemm"][1] += 2.0 * M * sh.vocab * sh.hidden
+    return res
+
+
+def source_digest():
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2609_36546_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(f.encode())
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(kernel, workload):
+    """HBM bytes per launch from the committed counter summary, if it was
+    taken on the current kernel sources (else None)."""
+    path = os.path.join(PROFILES, f"{kernel}_{workload}_counters.md")
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    for line in open(path):
+        if ":" in line and line.strip().startswith("- "):
+            k, v = line.strip()[2:].split(":", 1)
+            vals[k.strip()] = v.strip().strip("`")
+    if vals.get("source_digest") != source_digest():
+        return None
+    try:
+        return float(vals["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(batch, budget_s=20.0):
+    """The fp64 oracle on a bounded sample of the workload, on this host."""
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    except Exception:
+        cores = len(os.sched_getaffinity(0))
+    mdl = batch.models[0]
+    sh = mdl.shape
+    ps = batch.cfg.page_size
+    host = lambda x: (x.float() if x.dtype == torch.bfloat16 else x).cpu().numpy()
+    pt = mdl.page_table.cpu().numpy().astype(np.int64)
+    order = np.random.default_rng(0).permutation(mdl.seq_ids.cpu().numpy())
+    W = host(mdl.W)
+    rows_done, seqs_done = 0, 0
+    t_total = 0.0
+    for b in order:
+        b = int(b)
+        need = -(-(int(batch.ctx_lens[b]) + int(batch.k[b])) // ps)
+        pages = torch.from_numpy(pt[b, :need]).to(mdl.k_pool.device)
+        kc, vc = host(mdl.k_pool.index_select(0, pages)), host(mdl.v_pool.index_select(0, pages))
+        sub_pt = np.arange(need)[None, :]
+        r0, r1 = int(batch.cu_q[b]), int(batch.cu_q[b + 1])
+        q, kn, vn = host(mdl.q[r0:r1]), host(mdl.k_new[r0:r1]), host(mdl.v_new[r0:r1])
+        hid = host(mdl.hidden[r0:r1])
+        t0 = time.perf_counter()
+        oracle.verify_attn_paged(q, kn, vn, kc, vc, sub_pt, batch.ctx_lens[b:b + 1],
+                                 np.array([0, r1 - r0]), 1.0 / np.sqrt(sh.D))
+        res = oracle.lmhead_logsoftmax(hid, W, np.zeros(r1 - r0, np.int64), batch.cfg.K)
+        oracle.accept_scan(np.array([0, r1 - r0]), res["argmax"], res["topk_idx"], batch.cfg.K,
+                           batch.driver[b:b + 1], batch.ctx_lens[b:b + 1], batch.seq_lens[b:b + 1],
+                           batch.eos_id, batch.max_len)
+        t_total += time.perf_counter() - t0
+        rows_done += r1 - r0
+        seqs_done += 1
+        if t_total >= budget_s:
+            break
+    return {"value": rows_done / t_total, "unit": "verified tokens/s", "cores": int(cores),
+            "kind": "oracle",
+            "sample": f"{seqs_done} of {batch.cfg.B} sequences ({rows_done} of {batch.T} window "
+                      f"rows), fp64 numpy oracle, {t_total:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", type=int, default=3)
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: the verify path shards by request with no "
+              "exchange, so N GPUs run N independent copies (see the design notes).",
+              file=sys.stderr)
+        sys.exit(2)
+    dev = torch.device("cuda:0")
+    cfg = inputs.CONFIGS[args.config]
+    batch = inputs.make_batch(cfg, seed=args.seed, device=dev, poison=False)
+    step = Step(batch, dev)
+    for _ in range(args.warmup):
+        step.run()
+    torch.cuda.synchronize()
+
+    # per-kernel timing: the library records these events around its kernels
+    n_models = len(step.per_model)
+    per_step = 7 * n_models + 2
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(per_step)] for _ in range(args.steps)]
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for s in range(args.steps):
+        ops.trace_events(evs[s])
+        step.run()
+    stop.record()
+    ops.trace_events(None)
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(stop) / args.steps
+
+    names = []
+    for _ in range(n_models):
+        names += ["append", "attention", "combine", "lmhead_gemm", "lmhead_merge"]
+    names += ["accept_scan"]
+    kt = {k: 0.0 for k in KERNELS}
+    for s in range(args.steps):
+        e = evs[s]
+        # per model: attention call records 4 events, lmhead call 3 events
+        i = 0
+        for _ in range(n_models):
+            kt["append"] += e[i].elapsed_time(e[i + 1])
+            kt["attention"] += e[i + 1].elapsed_time(e[i + 2])
+            kt["combine"] += e[i + 2].elapsed_time(e[i + 3])
+            kt["lmhead_gemm"] += e[i + 4].elapsed_time(e[i + 5])
+            kt["lmhead_merge"] += e[i + 5].elapsed_time(e[i + 6])
+            i += 7
+        kt["accept_scan"] += e[i].elapsed_time(e[i + 1])
+    kt = {k: v / args.steps for k, v in kt.items()}
+
+    work = work_per_launch(batch)
+    dom = "lmhead_gemm" if kt["lmhead_gemm"] >= kt["attention"] else "attention"
+    t_dom = kt[dom] * 1e-3 / n_models
+    workload = f"config{args.config}"
+    if dom == "attention" or batch.T < 320:
+        bytes_, flops_ = work[dom]
+        achieved = bytes_ / n_models / t_dom / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4)}
+    else:
+        bytes_, flops_ = work[dom]
+        achieved = flops_ / n_models / t_dom / 1e12
+        roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": BF16_PEAK_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(achieved / BF16_PEAK_TFLOPS, 4)}
+    roof["kernel"] = dom
+    roof["traffic"] = measured_traffic(dom, workload)
+
+    attn_bytes = work["attention"][0]
+    res = {
+        "metric": METRIC,
+        "value": round(batch.T / (ms * 1e-3), 1),
+        "unit": "verified tokens/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16" if cfg.dtype == "bf16" else "f32", "data": "synthetic",
+        "config": {"workload": f"{cfg.name} (config {args.config}): B={cfg.B}, "
+                               f"ctx U[{cfg.ctx_lo},{cfg.ctx_hi}], k={list(cfg.k_choices)}, "
+                               f"{'+'.join(f'{m.Hq}q/{m.Hkv}kv/D{m.D}' for m in cfg.models)}, "
+                               f"hidden {cfg.models[0].hidden}, vocab {cfg.models[0].vocab}, K={cfg.K}",
+                   "window_rows": batch.T, "parallelism": "single GPU"},
+        "roofline": roof,
+        "kernels_us": {k: round(v * 1e3, 2) for k, v in kt.items()},
+        "attention_hbm_gbs": round(attn_bytes / (kt["attention"] * 1e-3) / 1e9, 1),
+        "lmhead_tflops": round(work["lmhead_gemm"][1] / (kt["lmhead_gemm"] * 1e-3) / 1e12, 1),
+    }
+    if not args.no_cpu:
+        res["cpu_baseline"] = cpu_baseline(batch)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -23,7 +23,7 @@
  *   - All array arguments are DEVICE pointers owned by the caller (except the
  *     host-side shape arguments of the *_workspace_size queries).  The library
  *     allocates no device memory and keeps no state besides a thread-local
- *     error message.
+ *     error message and the optional thread-local timing hook below.
  *   - Every call only enqueues work on `hip_stream` (a hipStream_t; NULL = the
  *     default stream) and returns; it never synchronises.
  *   - Arrays are dense, row-major, with the shapes given below.  Floating
@@ -214,6 +214,21 @@ int accept_scan(const int32_t* cu_q, const int32_t* prop_tok,
                 int32_t* n_acc, int32_t* event_row, uint8_t* next_driver,
                 uint8_t* finished, int32_t* new_cache_len, uint8_t* src,
                 void* hip_stream);
+
+/*
+ * Optional timing hook for profilers and benchmarks (thread-local).  While
+ * set, each kernel an entry point launches is bracketed by hipEventRecord of
+ * the caller's events (hipEvent_t handles cast to void*), taken from
+ * `events` in order: the first kernel of a call records one event before and
+ * one after it, every further kernel one after it.  Recording stops when
+ * `capacity` events are used.  NULL / 0 turns it off.  Returns IPDV_OK.
+ * ipdv_trace_count() returns how many events have been recorded since the
+ * hook was last set.  Kernels per call: verify_attn_paged 3 (append,
+ * attention, split combine), lmhead_logsoftmax_verify 2 (GEMM + epilogue,
+ * merge), accept_scan 1.
+ */
+int ipdv_trace_events(void* const* events, int capacity);
+int ipdv_trace_count(void);
 
 /* Thread-local description of the last non-OK status ("" if none). */
 const char* ipdv_last_error(void);

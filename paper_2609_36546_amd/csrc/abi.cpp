@@ -14,6 +14,9 @@
 namespace {
 
 thread_local char g_err[512] = "";
+thread_local void* const* g_trace = nullptr;
+thread_local int g_trace_cap = 0;
+thread_local int g_trace_n = 0;
 
 int fail(int status, const char* fmt, ...) {
   va_list ap;
@@ -50,9 +53,29 @@ int attn_sub_tokens() {
   return v;
 }
 
+void trace_begin(hipStream_t st) { trace_mark(st); }
+
+void trace_mark(hipStream_t st) {
+  if (g_trace && g_trace_n < g_trace_cap) {
+    // A bad handle must not turn into a launch failure: clear its error.
+    if (hipEventRecord(reinterpret_cast<hipEvent_t>(g_trace[g_trace_n]), st) != hipSuccess)
+      (void)hipGetLastError();
+    ++g_trace_n;
+  }
+}
+
 }  // namespace ipdv
 
 extern "C" {
+
+int ipdv_trace_events(void* const* events, int capacity) {
+  g_trace = (events && capacity > 0) ? events : nullptr;
+  g_trace_cap = g_trace ? capacity : 0;
+  g_trace_n = 0;
+  return IPDV_OK;
+}
+
+int ipdv_trace_count(void) { return g_trace_n; }
 
 const char* ipdv_last_error(void) { return g_err; }
 

@@ -96,8 +96,11 @@ hipError_t launch_accept_scan(const ScanLaunch& L, hipStream_t st) {
   ScanParams p{L.cu_q, L.prop_tok, L.topk_idx, L.K, L.driver, L.ctx_lens, L.seq_lens,
                L.eos_id, L.max_len, L.B, L.n_acc, L.event_row, L.next_driver, L.finished,
                L.new_cache_len, L.src};
+  trace_begin(st);
   hipLaunchKernelGGL(accept_scan_kernel, dim3((L.B + 3) / 4), dim3(256), 0, st, p);
-  return hipGetLastError();
+  hipError_t e = hipGetLastError();
+  trace_mark(st);
+  return e;
 }
 
 }  // namespace ipdv

@@ -10,6 +10,11 @@
 
 namespace ipdv {
 
+// Timing hook (see ipdv_trace_events): trace_begin() at the start of an entry
+// point's launches, trace_mark() after each kernel.
+void trace_begin(hipStream_t st);
+void trace_mark(hipStream_t st);
+
 // ---- verification-stage attention ----
 struct AttnPlan {
   int n_qg;            // 64-row query groups per (sequence, KV head)

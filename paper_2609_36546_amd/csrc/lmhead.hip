@@ -463,11 +463,15 @@ template <typename DT, int RB>
 hipError_t launch_rb(const LmParams& p, hipStream_t st) {
   const int n_vt_pad = (p.n_vt + 7) / 8 * 8;
   dim3 grid(n_vt_pad * p.n_rt);
+  trace_begin(st);
   hipLaunchKernelGGL((lmhead_gemm_kernel<DT, RB>), grid, dim3(256), 0, st, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  trace_mark(st);
   hipLaunchKernelGGL((lmhead_merge_kernel<DT>), dim3(p.M), dim3(kMT), 0, st, p);
-  return hipGetLastError();
+  e = hipGetLastError();
+  trace_mark(st);
+  return e;
 }
 
 }  // namespace

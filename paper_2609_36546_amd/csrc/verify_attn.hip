@@ -486,14 +486,19 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(AttnParams a) {
 
 template <typename DT, int D, int QT>
 hipError_t launch_t(const AttnParams& p, dim3 grid, dim3 cgrid, hipStream_t st) {
+  trace_begin(st);
   hipLaunchKernelGGL((append_window_kernel<DT, D>), dim3(cgrid.y), dim3(256), 0, st, p);
-  hipError_t e0 = hipGetLastError();
-  if (e0 != hipSuccess) return e0;
-  hipLaunchKernelGGL((verify_attn_kernel<DT, D, QT>), grid, dim3(256), 0, st, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  trace_mark(st);
+  hipLaunchKernelGGL((verify_attn_kernel<DT, D, QT>), grid, dim3(256), 0, st, p);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  trace_mark(st);
   hipLaunchKernelGGL((attn_combine_kernel<DT, D>), cgrid, dim3(256), 0, st, p);
-  return hipGetLastError();
+  e = hipGetLastError();
+  trace_mark(st);
+  return e;
 }
 
 template <typename DT, int D>

@@ -55,6 +55,9 @@ def lib() -> ctypes.CDLL:
         L.accept_scan.argtypes = [i32p, i32p, i32p, ci, u8p, i32p, i32p, ctypes.c_int32,
                                   ctypes.c_int32, ci, i32p, i32p, u8p, u8p, i32p, u8p, vp]
         L.accept_scan.restype = ci
+        L.ipdv_trace_events.argtypes = [ctypes.c_void_p, ci]
+        L.ipdv_trace_events.restype = ci
+        L.ipdv_trace_count.restype = ci
         L.ipdv_last_error.restype = ctypes.c_char_p
         L.ipdv_version.restype = ctypes.c_char_p
         _lib = L
@@ -95,6 +98,29 @@ def _dtype_code(dt: torch.dtype) -> int:
     if dt == torch.float32:
         return IPDV_F32
     raise ValueError(f"unsupported dtype {dt}")
+
+
+def trace_events(events) -> None:
+    """Bracket every kernel the library launches with these torch.cuda.Event
+    objects (in order; see ipdv_trace_events).  None turns tracing off."""
+    global _trace_keep
+    if not events:
+        lib().ipdv_trace_events(None, 0)
+        _trace_keep = None
+        return
+    for e in events:            # torch creates the HIP event on first record
+        if e.cuda_event == 0:
+            e.record()
+    arr = (ctypes.c_void_p * len(events))(*[e.cuda_event for e in events])
+    _trace_keep = arr
+    lib().ipdv_trace_events(ctypes.cast(arr, ctypes.c_void_p), len(events))
+
+
+def trace_count() -> int:
+    return int(lib().ipdv_trace_count())
+
+
+_trace_keep = None
 
 
 def version() -> str:
