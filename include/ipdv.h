@@ -101,8 +101,11 @@ size_t ipdv_attn_workspace_size(int n_seq, int Hq, int Hkv, int D, int max_q,
  * q       [T, Hq, D]    window queries (dtype)
  * k_new   [T, Hkv, D]   window keys    (dtype)
  * v_new   [T, Hkv, D]   window values  (dtype)
- * k_cache [num_pages, Hkv, page_size, D]   key pages: per KV head, one key
- *                                          vector per slot (dtype, in/out)
+ * k_cache [num_pages, Hkv, D/32, page_size, 32]
+ *                       key pages: per KV head and 32-channel slice, the
+ *                       slice of each slot in turn (channel d of a slot at
+ *                       [page][g][d/32][slot][d%32]); 16-key MFMA operand
+ *                       loads then read whole cache lines (dtype, in/out)
  * v_cache [num_pages, Hkv, D, page_size]   value pages, channel-major: per
  *                                          KV head and channel, one value per
  *                                          slot (dtype, in/out)
@@ -121,15 +124,15 @@ size_t ipdv_attn_workspace_size(int n_seq, int Hq, int Hkv, int D, int max_q,
  *                       sequences are neither read nor written.
  * max_q                 >= k_b for every handled sequence (host-side bound)
  * out     [T, Hq, D]    attention output (dtype)
- * Hq, Hkv, D            Hq % Hkv == 0; D in {64, 128}
+ * Hq, Hkv, D            Hq % Hkv == 0; D in {64, 128} for bf16, D = 64 for fp32
  * page_size             16, 32 or 64
- * scale                 softmax scale (normally 1/sqrt(D))
+ * scale                 softmax scale, > 0 (normally 1/sqrt(D))
  * workspace             device buffer of >= ipdv_attn_workspace_size(...)
  *                       bytes (split-KV partial results); contents on entry
  *                       are ignored.
  *
  * Errors: IPDV_EINVAL (null pointer, n_seq < 0, max_q < 1, bad head counts,
- * scale not finite), IPDV_EUNSUPPORTED (D, page_size, dtype),
+ * scale not positive and finite), IPDV_EUNSUPPORTED (D, page_size, dtype),
  * IPDV_EWORKSPACE, IPDV_EHIP.
  */
 int verify_attn_paged(const void* q, const void* k_new, const void* v_new,
@@ -166,7 +169,7 @@ size_t ipdv_lmhead_workspace_size(int M, int Hd, int V, int K);
  * out_rows [M] int32 or NULL
  * lse, logp_prop, entropy: float [rows];  argmax int32 [rows];
  * topk_idx int32 [rows, K];  topk_logp float [rows, K]
- * Requirements: M >= 0, Hd % 64 == 0, 1 <= K <= min(IPDV_MAX_K, V).
+ * Requirements: M >= 0, Hd % 64 == 0, 1 <= V <= 262144, 1 <= K <= min(IPDV_MAX_K, V).
  *
  * Errors: IPDV_EINVAL, IPDV_EUNSUPPORTED (dtype, Hd), IPDV_EWORKSPACE, IPDV_EHIP.
  */

@@ -26,8 +26,8 @@ rollback lengths, EOS inside a window, length cap) are listed in the
 repository's design notes; each is restated at the function that uses it.
 
 Cache layouts (the library's documented layouts):
-``k_cache[num_pages, Hkv, page_size, D]`` and
-``v_cache[num_pages, Hkv, D, page_size]``.
+``k_cache[num_pages, Hkv, D/32, page_size, 32]`` -- key channel d of a slot is
+at [.., d // 32, slot, d % 32] -- and ``v_cache[num_pages, Hkv, D, page_size]``.
 """
 from __future__ import annotations
 
@@ -61,7 +61,7 @@ def append_window(k_cache, v_cache, k_new, v_new, page_table, ctx_lens, cu_q,
     page ``page_table[b][(L_b+i) // ps]``, slot ``(L_b+i) % ps`` -- appending
     externally proposed tokens to a live request's cache (Section 3.2.3).
     """
-    ps = k_cache.shape[2]
+    Hkv, nslice, ps, x = k_cache.shape[1:]
     n_seq = len(ctx_lens) if n_seq is None else n_seq
     for b in _seq_list(n_seq, seq_ids):
         L = int(ctx_lens[b])
@@ -69,19 +69,19 @@ def append_window(k_cache, v_cache, k_new, v_new, page_table, ctx_lens, cu_q,
             row = int(cu_q[b]) + i
             pos = L + i
             page = int(page_table[b][pos // ps])
-            k_cache[page, :, pos % ps, :] = k_new[row]
+            k_cache[page, :, :, pos % ps, :] = np.reshape(k_new[row], (Hkv, nslice, x))
             v_cache[page, :, :, pos % ps] = v_new[row]
 
 
 def gather_sequence(k_cache, v_cache, page_table, b, n_tokens):
     """Keys and values of positions [0, n_tokens) of sequence b, as fp64
     arrays [n_tokens, Hkv, D]."""
-    ps = k_cache.shape[2]
+    Hkv, nslice, ps, x = k_cache.shape[1:]
     pos = np.arange(n_tokens)
     pages = np.asarray(page_table[b])[pos // ps].astype(np.int64)
     slots = pos % ps
-    K = _f64(k_cache[pages, :, slots, :])          # [n, Hkv, D]
-    V = _f64(v_cache[pages, :, :, slots])          # [n, Hkv, D]
+    K = _f64(k_cache[pages, :, :, slots, :]).reshape(n_tokens, Hkv, nslice * x)   # [n, Hkv, D]
+    V = _f64(v_cache[pages, :, :, slots])                                           # [n, Hkv, D]
     return K, V
 
 

@@ -41,13 +41,13 @@ bool is_pow2(int x) { return x > 0 && (x & (x - 1)) == 0; }
 
 namespace ipdv {
 
-// Keys streamed by one wave per split (a multiple of 32).  IPDV_ATTN_SUB
-// overrides the default for tuning sweeps.
+// Keys streamed by one wave per split, from IPDV_ATTN_SUB (a multiple of 32
+// in [32, 1024]) for tuning sweeps; 0 = the planner's choice.
 int attn_sub_tokens() {
   static int v = [] {
     const char* s = getenv("IPDV_ATTN_SUB");
     int x = s ? atoi(s) : 0;
-    if (x < 32 || x > 1024 || x % 32 != 0) x = 256;
+    if (x < 32 || x > 1024 || x % 32 != 0) x = 0;
     return x;
   }();
   return v;
@@ -111,8 +111,9 @@ int verify_attn_paged(const void* q, const void* k_new, const void* v_new, void*
   int st = attn_shape_check(n_seq, Hq, Hkv, D, max_q, max_pages_per_seq, page_size);
   if (st != IPDV_OK) return st;
   if (dtype != IPDV_F32 && dtype != IPDV_BF16) return fail(IPDV_EUNSUPPORTED, "dtype %d", dtype);
+  if (dtype == IPDV_F32 && D != 64) return fail(IPDV_EUNSUPPORTED, "fp32 attention supports D=64 only");
   if (num_pages < 1) return fail(IPDV_EINVAL, "num_pages must be >= 1 (got %d)", num_pages);
-  if (!std::isfinite(scale)) return fail(IPDV_EINVAL, "scale must be finite");
+  if (!std::isfinite(scale) || !(scale > 0.f)) return fail(IPDV_EINVAL, "scale must be positive and finite");
   if (n_seq == 0) return ok();
   if (!q || !k_new || !v_new || !k_cache || !v_cache || !page_table || !ctx_lens || !cu_q || !out)
     return fail(IPDV_EINVAL, "null required pointer");
@@ -134,6 +135,7 @@ static int lm_shape_check(int M, int Hd, int V, int K) {
   if (K < 1 || K > IPDV_MAX_K || K > V)
     return fail(IPDV_EINVAL, "K=%d must satisfy 1 <= K <= min(%d, V=%d)", K, IPDV_MAX_K, V);
   if (Hd < 64 || Hd % 64 != 0) return fail(IPDV_EUNSUPPORTED, "Hd=%d must be a positive multiple of 64", Hd);
+  if (V > 262144) return fail(IPDV_EUNSUPPORTED, "V=%d exceeds 262144", V);
   if (M > 2147483647 / 2) return fail(IPDV_EUNSUPPORTED, "M too large");
   return IPDV_OK;
 }

@@ -280,23 +280,6 @@ __device__ __forceinline__ bool before(float a, int ia, float b, int ib) {
   return a > b || (a == b && ia < ib);
 }
 
-// Block-wide argbest over per-thread candidates (value, index).
-__device__ void block_best(float& v, int& ix, float* s_v, int* s_i) {
-  for (int o = 32; o > 0; o >>= 1) {
-    const float ov = __shfl_xor(v, o, kWave);
-    const int oi = __shfl_xor(ix, o, kWave);
-    if (before(ov, oi, v, ix)) { v = ov; ix = oi; }
-  }
-  const int w = threadIdx.x >> 6;
-  __syncthreads();
-  if (lane_id() == 0) { s_v[w] = v; s_i[w] = ix; }
-  __syncthreads();
-  v = s_v[0];
-  ix = s_i[0];
-  for (int ww = 1; ww < kMT / kWave; ++ww)
-    if (before(s_v[ww], s_i[ww], v, ix)) { v = s_v[ww]; ix = s_i[ww]; }
-}
-
 __device__ float block_sum(float x, float* s) {
   for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o, kWave);
   const int w = threadIdx.x >> 6;
@@ -347,16 +330,54 @@ __device__ float wave_dot(const LmParams& p, int m, int v) {
   return acc;
 }
 
+// Groups per merge thread held in registers: V <= kMT * kMaxGPT * kGroup.
+constexpr int kMaxGPT = 16;
+
+// Wave-wide best (value desc, index asc) of one candidate per lane.
+__device__ __forceinline__ void wave_best(float& v, int& ix) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float ov = __shfl_xor(v, o, kWave);
+    const int oi = __shfl_xor(ix, o, kWave);
+    if (before(ov, oi, v, ix)) { v = ov; ix = oi; }
+  }
+}
+
+// K picks in order from the lane-held candidates c[0..n) plus extra LDS
+// candidates; out_v / out_i receive the wave's top-K (lane 0 writes).
+template <int N>
+__device__ __forceinline__ void wave_topk(const float (&cv)[N], const int (&ci)[N],
+                                          const float* xv, const int* xi, int nx, int K,
+                                          float* out_v, int* out_i) {
+  float last_v = INFINITY;
+  int last_i = -1;
+  for (int k = 0; k < K; ++k) {
+    float bv = -INFINITY;
+    int bi = 0x7fffffff;
+#pragma unroll
+    for (int c = 0; c < N; ++c)
+      if (before(last_v, last_i, cv[c], ci[c]) && before(cv[c], ci[c], bv, bi)) { bv = cv[c]; bi = ci[c]; }
+    for (int c = lane_id(); c < nx; c += kWave)
+      if (before(last_v, last_i, xv[c], xi[c]) && before(xv[c], xi[c], bv, bi)) { bv = xv[c]; bi = xi[c]; }
+    wave_best(bv, bi);
+    if (lane_id() == 0) { out_v[k] = bv; out_i[k] = bi; }
+    last_v = bv;
+    last_i = bi;
+  }
+}
+
 template <typename DT>
 __global__ __launch_bounds__(kMT) void lmhead_merge_kernel(LmParams p) {
   const int m = blockIdx.x;
   const int tid = threadIdx.x;
   const int wv = tid >> 6;
   const int G = p.n_groups;
+  const int K = p.K;
   const size_t base = (size_t)m * G;
+  constexpr int NW = kMT / kWave;
   __shared__ float s_red[8];
-  __shared__ float s_bv[8];
-  __shared__ int s_bi[8];
+  __shared__ float s_wv[NW][IPDV_MAX_K_DEV];
+  __shared__ int s_wi[NW][IPDV_MAX_K_DEV];
   __shared__ float s_top_v[IPDV_MAX_K_DEV];
   __shared__ int s_top_i[IPDV_MAX_K_DEV];
   __shared__ int s_split[kMaxSplit];
@@ -364,71 +385,78 @@ __global__ __launch_bounds__(kMT) void lmhead_merge_kernel(LmParams p) {
   __shared__ float s_cv[kSplitCand];   // recomputed logits of split groups
   __shared__ int s_ci[kSplitCand];
 
-  // Log-sum-exp and entropy sums (group maxima are the v1 records).
+  // This thread's groups: tid, tid + kMT, ... (register resident).
+  float cv[2 * kMaxGPT];
+  int ci[2 * kMaxGPT];
   float mx = -INFINITY;
-  for (int gi = tid; gi < G; gi += kMT) mx = fmaxf(mx, p.rec_v1[base + gi]);
+#pragma unroll
+  for (int u = 0; u < kMaxGPT; ++u) {
+    const int gi = tid + kMT * u;
+    const bool ok = gi < G;
+    cv[2 * u] = ok ? p.rec_v1[base + gi] : -INFINITY;
+    ci[2 * u] = ok ? p.rec_idx[base + gi] : 0x7fffffff;
+    cv[2 * u + 1] = ok ? p.rec_v2[base + gi] : -INFINITY;
+    ci[2 * u + 1] = ok ? p.rec_i2[base + gi] : 0x7fffffff;
+    mx = fmaxf(mx, cv[2 * u]);
+  }
+
+  // Log-sum-exp and entropy sums (group maxima are the v1 records).
   const float M = block_max(mx, s_red);
   const float Mu = (M == -INFINITY) ? 0.f : M;
   float S = 0.f, E = 0.f;
-  for (int gi = tid; gi < G; gi += kMT) {
-    const float wgt = fast_exp2((p.rec_v1[base + gi] - Mu) * kLog2e);
-    S += p.rec_s[base + gi] * wgt;
-    E += p.rec_e[base + gi] * wgt;
+#pragma unroll
+  for (int u = 0; u < kMaxGPT; ++u) {
+    const int gi = tid + kMT * u;
+    if (gi < G) {
+      const float wgt = fast_exp2((cv[2 * u] - Mu) * kLog2e);
+      S += p.rec_s[base + gi] * wgt;
+      E += p.rec_e[base + gi] * wgt;
+    }
   }
   S = block_sum(S, s_red);
   E = block_sum(E, s_red);
   const float lse = Mu + fast_log2(S) * kLn2;
 
-  // Exact top-K: round 0 selects from the recorded (v1, v2) pairs; groups
-  // whose v2 is in that list are recomputed in full and round 1 selects again
-  // (then every element left out ranks after the K-th pick).
-  const int K = p.K;
-  if (tid == 0) s_nsplit = 0;
+  // Exact top-K.  Round 0 picks from the recorded (v1, v2) pairs.  A group
+  // with two picks may hide a third member, so its 64 logits are recomputed
+  // and round 1 picks again from the records of the other groups plus every
+  // recomputed value; then each element left out ranks after the K-th pick.
+  int nsplit = 0;
   for (int round = 0; round < 2; ++round) {
+    wave_topk(cv, ci, s_cv, s_ci, nsplit * kGroup, K, s_wv[wv], s_wi[wv]);
     __syncthreads();
-    const int nsplit = s_nsplit;
-    float last_v = INFINITY;
-    int last_i = -1;
-    for (int k = 0; k < K; ++k) {
-      float bv = -INFINITY;
-      int bi = 0x7fffffff;
-      for (int gi = tid; gi < G; gi += kMT) {
-        bool split = false;
-        for (int s = 0; s < nsplit; ++s) split |= (s_split[s] == gi);
-        if (split) continue;
-        const float a = p.rec_v1[base + gi];
-        const int ia = p.rec_idx[base + gi];
-        if (before(last_v, last_i, a, ia) && before(a, ia, bv, bi)) { bv = a; bi = ia; }
-        const float b = p.rec_v2[base + gi];
-        const int ib = p.rec_i2[base + gi];
-        if (before(last_v, last_i, b, ib) && before(b, ib, bv, bi)) { bv = b; bi = ib; }
+    if (wv == 0) {
+      float xv0 = -INFINITY, xv1 = -INFINITY;
+      int xi0 = 0x7fffffff, xi1 = 0x7fffffff;
+      const int lane = lane_id();
+      if (lane < NW * K) { xv0 = s_wv[lane / K][lane % K]; xi0 = s_wi[lane / K][lane % K]; }
+      if (lane + kWave < NW * K) {
+        xv1 = s_wv[(lane + kWave) / K][(lane + kWave) % K];
+        xi1 = s_wi[(lane + kWave) / K][(lane + kWave) % K];
       }
-      for (int c = tid; c < nsplit * kGroup; c += kMT) {
-        const float a = s_cv[c];
-        const int ia = s_ci[c];
-        if (before(last_v, last_i, a, ia) && before(a, ia, bv, bi)) { bv = a; bi = ia; }
-      }
-      block_best(bv, bi, s_bv, s_bi);
-      if (tid == 0) { s_top_v[k] = bv; s_top_i[k] = bi; }
-      last_v = bv;
-      last_i = bi;
+      const float fv[2] = {xv0, xv1};
+      const int fi[2] = {xi0, xi1};
+      wave_topk(fv, fi, s_cv, s_ci, 0, K, s_top_v, s_top_i);
     }
+    __syncthreads();
     if (round == 1) break;
-    __syncthreads();
-    for (int gi = tid; gi < G; gi += kMT) {
-      const int ib = p.rec_i2[base + gi];
-      if (ib == 0x7fffffff) continue;
-      bool in = false;
-      for (int k = 0; k < K; ++k) in |= (s_top_i[k] == ib);
-      if (in) {
-        const int slot = atomicAdd(&s_nsplit, 1);
-        if (slot < kMaxSplit) s_split[slot] = gi;
-      }
+    // Groups picked twice.
+    if (tid == 0) {
+      int n = 0;
+      for (int a = 0; a < K; ++a)
+        for (int b2 = a + 1; b2 < K; ++b2)
+          if (s_top_i[a] != 0x7fffffff && s_top_i[a] / kGroup == s_top_i[b2] / kGroup) {
+            const int gsp = s_top_i[a] / kGroup;
+            bool seen = false;
+            for (int t = 0; t < n; ++t) seen |= (s_split[t] == gsp);
+            if (!seen && n < kMaxSplit) s_split[n++] = gsp;
+          }
+      s_nsplit = n;
     }
     __syncthreads();
-    const int ns = min(s_nsplit, kMaxSplit);
-    if (ns == 0) break;
-    for (int c = wv; c < ns * kGroup; c += kMT / kWave) {
+    nsplit = s_nsplit;
+    if (nsplit == 0) break;
+    for (int c = wv; c < nsplit * kGroup; c += NW) {
       const int v = s_split[c / kGroup] * kGroup + (c % kGroup);
       const bool ok = v < p.V;
       const float x = ok ? wave_dot<DT>(p, m, v) : -INFINITY;
@@ -437,8 +465,19 @@ __global__ __launch_bounds__(kMT) void lmhead_merge_kernel(LmParams p) {
         s_ci[c] = ok ? v : 0x7fffffff;
       }
     }
+    // drop the split groups' records: their members now come from s_cv
+#pragma unroll
+    for (int u = 0; u < kMaxGPT; ++u) {
+      const int gi = tid + kMT * u;
+      bool sp = false;
+      for (int t = 0; t < nsplit; ++t) sp |= (s_split[t] == gi);
+      if (sp) {
+        cv[2 * u] = cv[2 * u + 1] = -INFINITY;
+        ci[2 * u] = ci[2 * u + 1] = 0x7fffffff;
+      }
+    }
+    __syncthreads();
   }
-  __syncthreads();
 
   const int orow = p.out_rows ? p.out_rows[m] : m;
   if (tid < K) {

@@ -26,7 +26,9 @@
 //
 // The value pages are channel-major ([page][head][D][slot]), so the A operand
 // of the PV product -- 8 consecutive keys of one channel -- is one 16-byte
-// load, and P never leaves registers.  MFMA rows of the QK product are
+// load, and P never leaves registers.  The key pages are sliced by 32
+// channels ([page][head][D/32][slot][32]) so that every 16-key QK operand load
+// reads whole cache lines.  MFMA rows of the QK product are
 // permuted (row r <-> key 8(r/4) + 4s + r%4 in sub-tile s) so that each lane
 // ends up holding exactly the 8 consecutive keys its PV operand needs.
 //
@@ -63,7 +65,7 @@ struct AttnParams {
   int Hq, Hkv, G;
   int page_size, log2ps, num_pages;
   int chunk, sub;     // keys per workgroup chunk / per wave
-  int max_chunks, n_qg;
+  int max_chunks, n_qg, n_seq;
   float scale_log2;   // softmax scale * log2(e)
 };
 
@@ -101,19 +103,24 @@ __device__ __forceinline__ void load_block(const AttnParams& a, Frags<DT, D>& f,
   // sub-tiles' keys share one 8-aligned group, hence one page.
   const int kgrp = t0 + 8 * (c16 >> 2);
   const int kpage = __shfl(my_page, clampi((kgrp >> a.log2ps) - pbase, 0, kWave - 1), kWave);
+  // Key pages are [D/32][slot][32]: for sub-tile s and k-step ks the 64 lanes
+  // read 4 runs of 4 consecutive slots x 64 bytes -- whole cache lines.
   const DT* kbase = reinterpret_cast<const DT*>(a.k_cache) +
                     (size_t)(kpage * a.Hkv + g) * a.page_size * D;
 #pragma unroll
   for (int s = 0; s < 2; ++s) {
-    const int pos = kgrp + 4 * s + (c16 & 3);
-    const DT* row = kbase + (pos & (a.page_size - 1)) * D;
+    const int slot = (kgrp + 4 * s + (c16 & 3)) & (a.page_size - 1);
     if constexpr (sizeof(DT) == 2) {
 #pragma unroll
-      for (int ks = 0; ks < D / 32; ++ks) f.k[s][ks] = ld16<bf16x8>(row + 8 * j + 32 * ks);
+      for (int ks = 0; ks < D / 32; ++ks)
+        f.k[s][ks] = ld16<bf16x8>(kbase + ((size_t)ks * a.page_size + slot) * 32 + 8 * j);
     } else {
+      // fp32: lane group j holds channels j*D/4 .. j*D/4 + D/4 - 1 (one slice run)
+      const int d0 = j * (D / 4);
+      const DT* row = kbase + ((size_t)(d0 / 32) * a.page_size + slot) * 32 + (d0 & 31);
 #pragma unroll
       for (int c = 0; c < D / 16; ++c) {
-        floatx4 v = ld16<floatx4>(row + j * (D / 4) + 4 * c);
+        floatx4 v = ld16<floatx4>(row + 4 * c);
         f.k[s][4 * c + 0] = v[0];
         f.k[s][4 * c + 1] = v[1];
         f.k[s][4 * c + 2] = v[2];
@@ -148,8 +155,9 @@ __device__ __forceinline__ void load_block(const AttnParams& a, Frags<DT, D>& f,
   }
 }
 
-// One 32-key block for every query tile: S^T = K Q^T, online softmax in
-// exp2 units, O^T += V^T P^T.
+// One 32-key block for every query tile: S^T = K Q^T for all tiles first
+// (independent MFMA chains), then the online softmax in exp2 units with the
+// scale folded into one FMA per score, then O^T += V^T P^T.
 template <typename DT, int D, int QT, bool TAIL>
 __device__ __forceinline__ void attend_block(const AttnParams& a, const Frags<DT, D>& f,
                                              const DT* s_q, const int (&qlimit)[QT],
@@ -157,54 +165,74 @@ __device__ __forceinline__ void attend_block(const AttnParams& a, const Frags<DT
                                              float (&m_run)[QT], float (&l_run)[QT]) {
   const int lane = lane_id();
   const int j = lane >> 4, c16 = lane & 15;
+  floatx4 s[QT][2];
+#pragma unroll
+  for (int t = 0; t < QT; ++t) s[t][0] = s[t][1] = floatx4{0.f, 0.f, 0.f, 0.f};
+  if constexpr (sizeof(DT) == 2) {
+#pragma unroll
+    for (int ks = 0; ks < D / 32; ++ks)
+#pragma unroll
+      for (int t = 0; t < QT; ++t) {
+        const bf16x8 qv = *reinterpret_cast<const bf16x8*>(s_q + (16 * t + c16) * (D + kQPad) + 8 * j + 32 * ks);
+#pragma unroll
+        for (int st = 0; st < 2; ++st)
+          s[t][st] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f.k[st][ks], qv, s[t][st], 0, 0, 0);
+      }
+  } else {
+#pragma unroll
+    for (int ks = 0; ks < D / 4; ++ks)
+#pragma unroll
+      for (int t = 0; t < QT; ++t) {
+        const float qv = s_q[(16 * t + c16) * (D + kQPad) + j * (D / 4) + ks];
+#pragma unroll
+        for (int st = 0; st < 2; ++st)
+          s[t][st] = __builtin_amdgcn_mfma_f32_16x16x4f32(f.k[st][ks], qv, s[t][st], 0, 0, 0);
+      }
+  }
+  // s[t][st][e] is the raw score of key t0 + 8j + 4st + e for the lane's row.
+  float bm[QT];
 #pragma unroll
   for (int t = 0; t < QT; ++t) {
-    // B operand (Q^T) of tile t from the LDS copy of the query rows.
-    const DT* qrow = s_q + (16 * t + c16) * (D + kQPad);
-    floatx4 s[2];
-#pragma unroll
-    for (int st = 0; st < 2; ++st) {
-      floatx4 z = {0.f, 0.f, 0.f, 0.f};
-      if constexpr (sizeof(DT) == 2) {
-#pragma unroll
-        for (int ks = 0; ks < D / 32; ++ks) {
-          const bf16x8 qv = *reinterpret_cast<const bf16x8*>(qrow + 8 * j + 32 * ks);
-          z = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f.k[st][ks], qv, z, 0, 0, 0);
-        }
-      } else {
-#pragma unroll
-        for (int ks = 0; ks < D / 4; ++ks)
-          z = __builtin_amdgcn_mfma_f32_16x16x4f32(f.k[st][ks], qrow[j * (D / 4) + ks], z, 0, 0, 0);
-      }
-      s[st] = z;
-    }
-    // s[st][e] is the score of key t0 + 8j + 4st + e for the lane's row.
-    float x[8];
-    float bm = -INFINITY;
+    bm[t] = -INFINITY;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      float v = s[e >> 2][e & 3] * a.scale_log2;
-      if (TAIL && (t0 + 8 * j + e) >= qlimit[t]) v = -INFINITY;
-      x[e] = v;
-      bm = fmaxf(bm, v);
+      if (TAIL && (t0 + 8 * j + e) >= qlimit[t]) s[t][e >> 2][e & 3] = -INFINITY;
+      bm[t] = fmaxf(bm[t], s[t][e >> 2][e & 3]);
     }
-    bm = wave_max_xor(bm, 16);
-    bm = wave_max_xor(bm, 32);
+  }
+#pragma unroll
+  for (int t = 0; t < QT; ++t) bm[t] = wave_max_xor(bm[t], 16);
+#pragma unroll
+  for (int t = 0; t < QT; ++t) bm[t] = wave_max_xor(bm[t], 32);
+  const float c = a.scale_log2;
+  float m_use[QT];
+  bool rescale = false;
+#pragma unroll
+  for (int t = 0; t < QT; ++t) {
+    const float bx = bm[t] * c;
     const float m_old = m_run[t];
-    const float m_new = (bm > m_old + kRescaleSlack || m_old == -INFINITY) ? fmaxf(bm, m_old) : m_old;
-    const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-    if (__any(m_new != m_old)) {
-      const float alpha = fast_exp2(m_old - m_use);
+    const float m_new = (bx > m_old + kRescaleSlack || m_old == -INFINITY) ? fmaxf(bx, m_old) : m_old;
+    m_use[t] = (m_new == -INFINITY) ? 0.f : m_new;
+    rescale |= m_new != m_old;
+    bm[t] = m_old;          // keep the old running max for the rescale factor
+    m_run[t] = m_new;
+  }
+  if (__any(rescale)) {
+#pragma unroll
+    for (int t = 0; t < QT; ++t) {
+      const float alpha = fast_exp2(bm[t] - m_use[t]);
       l_run[t] *= alpha;
 #pragma unroll
       for (int dt = 0; dt < D / 16; ++dt) acc[t][dt] *= alpha;
     }
-    m_run[t] = m_new;
+  }
+#pragma unroll
+  for (int t = 0; t < QT; ++t) {
     float p[8];
     float ps = 0.f;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      p[e] = fast_exp2(x[e] - m_use);
+      p[e] = fast_exp2(fmaf(s[t][e >> 2][e & 3], c, -m_use[t]));
       ps += p[e];
     }
     l_run[t] += ps;
@@ -246,15 +274,21 @@ __global__ __launch_bounds__(256) void append_window_kernel(AttnParams a) {
     const int page = clampi(pt_row[clampi(pos >> a.log2ps, 0, a.max_pages - 1)], 0, a.num_pages - 1);
     const int sl = pos & (a.page_size - 1);
     const size_t src = ((size_t)(r0 + i) * a.Hkv + g) * D + d;
-    kc[((size_t)(page * a.Hkv + g) * a.page_size + sl) * D + d] = kn[src];
+    kc[((size_t)((page * a.Hkv + g) * (D / 32) + d / 32) * a.page_size + sl) * 32 + (d & 31)] = kn[src];
     vc[((size_t)(page * a.Hkv + g) * D + d) * a.page_size + sl] = vn[src];
   }
 }
 
 template <typename DT, int D, int QT>
 __global__ __launch_bounds__(256) void verify_attn_kernel(AttnParams a) {
-  const int c = blockIdx.x, qg = blockIdx.y;
-  const int slot = blockIdx.z / a.Hkv, g = blockIdx.z % a.Hkv;
+  // Grid: x = (sequence, KV head) -- fastest, so consecutive workgroups (which
+  // the hardware deals out to the 8 XCDs round-robin) spread every chunk
+  // index over all XCDs; y = row group; z = chunk.  x is padded to a
+  // multiple of 8, so the row groups of one chunk (ids x apart) share an
+  // XCD and its L2.
+  if (blockIdx.x >= a.n_seq * a.Hkv) return;
+  const int c = blockIdx.z, qg = blockIdx.y;
+  const int slot = blockIdx.x / a.Hkv, g = blockIdx.x % a.Hkv;
   const int b = a.seq_ids ? a.seq_ids[slot] : slot;
   const int L = max(a.ctx_lens[b], 0);
   const int r0 = a.cu_q[b];
@@ -519,11 +553,22 @@ AttnPlan attn_plan(int n_seq, int Hq, int Hkv, int D, int max_q, int max_pages, 
   const long rows = (long)max_q * G;
   pl.n_qg = (int)((rows + kRows - 1) / kRows);
   pl.qt = rows >= kRows ? 4 : (int)((rows + 15) / 16);
+  // Keys per wave: the largest split that still yields enough workgroups
+  // (>= 4 per CU, by the host-side upper bound of the key count) for the
+  // hardware to balance ragged lengths.  IPDV_ATTN_SUB overrides it.
   pl.sub = attn_sub_tokens();
+  if (pl.sub == 0) {
+    const long max_keys_ub = (long)max_pages * page_size;
+    pl.sub = 128;
+    for (int s = 1024; s >= 256; s /= 2) {
+      const long items = (long)n_seq * Hkv * pl.n_qg * ((max_keys_ub + 4L * s - 1) / (4L * s));
+      if (items >= 4L * 256) { pl.sub = s; break; }
+    }
+    while (pl.sub > 32 && pl.sub > 63 * page_size) pl.sub /= 2;
+  }
   pl.chunk = kWaves * pl.sub;
   const long max_keys = (long)max_pages * page_size;
   int mc = (int)((max_keys + pl.chunk - 1) / pl.chunk);
-  mc = (mc + 7) / 8 * 8;   // row groups of one chunk land on one XCD (id % 8)
   pl.max_chunks = mc;
   const size_t slots = (size_t)n_seq * Hkv * pl.n_qg * pl.max_chunks;
   pl.part_o_bytes = slots * kRows * D * sizeof(float);
@@ -557,15 +602,15 @@ hipError_t launch_verify_attn(const AttnLaunch& L, const AttnPlan& pl, hipStream
   p.sub = pl.sub;
   p.max_chunks = pl.max_chunks;
   p.n_qg = pl.n_qg;
+  p.n_seq = L.n_seq;
   p.scale_log2 = L.scale * 1.4426950408889634f;
-  dim3 grid(pl.max_chunks, pl.n_qg, L.n_seq * L.Hkv);
+  dim3 grid((L.n_seq * L.Hkv + 7) / 8 * 8, pl.n_qg, pl.max_chunks);
   dim3 cgrid(pl.n_qg, L.n_seq * L.Hkv);
   if (L.dtype_bf16) {
     return L.D == 64 ? launch_d<bf16, 64>(p, pl.qt, grid, cgrid, st)
                      : launch_d<bf16, 128>(p, pl.qt, grid, cgrid, st);
   }
-  return L.D == 64 ? launch_d<float, 64>(p, pl.qt, grid, cgrid, st)
-                   : launch_d<float, 128>(p, pl.qt, grid, cgrid, st);
+  return launch_d<float, 64>(p, pl.qt, grid, cgrid, st);   // fp32: D = 64 only
 }
 
 }  // namespace ipdv

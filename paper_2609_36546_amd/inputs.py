@@ -24,8 +24,9 @@ data and weights are not used):
 
 KV pool layouts (the library's documented layouts):
 
-* ``k_pool[num_pages, Hkv, page_size, D]`` -- a page holds, per KV head, its
-  tokens' key vectors one after another;
+* ``k_pool[num_pages, Hkv, D/32, page_size, 32]`` -- a page holds, per KV
+  head and per 32-channel slice, its tokens' 32 key channels one after another
+  (key channel d of a slot is at [.., d // 32, slot, d % 32]);
 * ``v_pool[num_pages, Hkv, D, page_size]`` -- a page holds, per KV head and
   per channel, the values of its tokens one after another (channel-major).
 """
@@ -132,7 +133,7 @@ class ModelInputs:
     rows: torch.Tensor           # int32 [M]: batch rows of those sequences, in order
     page_table: torch.Tensor     # int32 [B, max_pages]
     num_pages: int
-    k_pool: torch.Tensor         # [num_pages, Hkv, ps, D]
+    k_pool: torch.Tensor         # [num_pages, Hkv, D/32, ps, 32]
     v_pool: torch.Tensor         # [num_pages, Hkv, D, ps]
     q: torch.Tensor              # [T, Hq, D] (rows of other models' sequences are zero)
     k_new: torch.Tensor          # [T, Hkv, D]
@@ -242,10 +243,10 @@ def make_batch(cfg: WorkloadConfig, seed: int = 0, device="cpu", poison: bool = 
 
         fill = float("nan") if poison else 0.0
         if fill_pool:
-            k_pool = torch.full((num_pages, Hkv, ps, D), fill, dtype=dt, device=device)
+            k_pool = torch.full((num_pages, Hkv, D // 32, ps, 32), fill, dtype=dt, device=device)
             v_pool = torch.full((num_pages, Hkv, D, ps), fill, dtype=dt, device=device)
         else:
-            k_pool = torch.empty((num_pages, Hkv, ps, D), dtype=dt, device=device)
+            k_pool = torch.empty((num_pages, Hkv, D // 32, ps, 32), dtype=dt, device=device)
             v_pool = torch.empty((num_pages, Hkv, D, ps), dtype=dt, device=device)
         # Cached tokens: positions [0, L_b) of each verified sequence.
         for b in seqs:
@@ -255,7 +256,7 @@ def make_batch(cfg: WorkloadConfig, seed: int = 0, device="cpu", poison: bool = 
             pos = torch.arange(L, device=device)
             pages = torch.from_numpy(pt[b]).to(device).long()[pos // ps]
             slots = pos % ps
-            k_pool[pages, :, slots, :] = kc
+            k_pool[pages, :, :, slots, :] = kc.reshape(L, Hkv, D // 32, 32)
             v_pool[pages, :, :, slots] = vc
         q = torch.zeros((T, Hq, D), dtype=dt, device=device)
         k_new = torch.zeros((T, Hkv, D), dtype=dt, device=device)

@@ -138,7 +138,7 @@ def verify_attn_paged(q, k_new, v_new, k_cache, v_cache, page_table, ctx_lens, c
                       scale: Optional[float] = None, out=None, workspace=None):
     """Append the window to the paged cache and attend (see include/ipdv.h).
 
-    q [T,Hq,D], k_new/v_new [T,Hkv,D], k_cache [P,Hkv,ps,D], v_cache [P,Hkv,D,ps]
+    q [T,Hq,D], k_new/v_new [T,Hkv,D], k_cache [P,Hkv,D/32,ps,32], v_cache [P,Hkv,D,ps]
     (bf16 or fp32), page_table [B,maxp] int32, ctx_lens [B] int32, cu_q [B+1]
     int32, seq_ids [n] int32 or None.  Returns out [T,Hq,D].
     """
@@ -149,11 +149,11 @@ def verify_attn_paged(q, k_new, v_new, k_cache, v_cache, page_table, ctx_lens, c
     _need(k_new, "k_new", dt, dev, 3)
     _need(v_new, "v_new", dt, dev, 3)
     Hkv = k_new.shape[1]
-    _need(k_cache, "k_cache", dt, dev, 4)
+    _need(k_cache, "k_cache", dt, dev, 5)
     _need(v_cache, "v_cache", dt, dev, 4)
-    P, _, ps, _ = k_cache.shape
-    if tuple(k_cache.shape) != (P, Hkv, ps, D) or tuple(v_cache.shape) != (P, Hkv, D, ps):
-        raise ValueError("k_cache must be [P,Hkv,ps,D] and v_cache [P,Hkv,D,ps]")
+    P, ps = k_cache.shape[0], k_cache.shape[3]
+    if tuple(k_cache.shape) != (P, Hkv, D // 32, ps, 32) or tuple(v_cache.shape) != (P, Hkv, D, ps):
+        raise ValueError("k_cache must be [P,Hkv,D/32,ps,32] and v_cache [P,Hkv,D,ps]")
     if tuple(k_new.shape) != (T, Hkv, D) or tuple(v_new.shape) != (T, Hkv, D):
         raise ValueError("k_new / v_new must be [T,Hkv,D]")
     _need(page_table, "page_table", torch.int32, dev, 2)

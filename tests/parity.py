@@ -126,7 +126,7 @@ def compare_scan(gpu, ref, seqs=None):
 def oracle_attention_subset(mdl, batch, seqs, D):
     """Oracle attention for a few sequences of a large batch: only their pages
     are copied to the host (page table remapped), then the oracle runs on them."""
-    ps = mdl.k_pool.shape[2]
+    ps = mdl.k_pool.shape[3]
     pt = to_np(mdl.page_table).astype(np.int64)
     need = {int(b): -(-(int(batch.ctx_lens[b]) + int(batch.k[b])) // ps) for b in seqs}
     pages = sorted({int(p) for b in seqs for p in pt[b, :need[b]]})

@@ -49,8 +49,8 @@ def _attn(**kw):
 @pytest.mark.parametrize("kw,status", [
     (dict(D=96), -2), (dict(ps=8), -2), (dict(ps=48), -2), (dict(Hq=6, Hkv=4), -1),
     (dict(q=None), -1), (dict(max_q=0), -1), (dict(n_seq=-1), -1), (dict(dtype=7), -2),
-    (dict(wsb=10), -3), (dict(ws=None), -3), (dict(scale=float("inf")), -1),
-    (dict(P=0), -1), (dict(maxp=0), -1)])
+    (dict(wsb=10), -3), (dict(ws=None), -3), (dict(scale=float("inf")), -1), (dict(scale=-0.1), -1),
+    (dict(P=0), -1), (dict(maxp=0), -1), (dict(dtype=ops.IPDV_F32, D=128), -2)])
 def test_attention_argument_errors(kw, status):
     assert _attn(**kw) == status
     assert ops.lib().ipdv_last_error().decode() != ""
@@ -107,3 +107,7 @@ def test_scan_argument_errors():
     empty = list(args)
     empty[9] = 0
     assert L.accept_scan(*empty) == 0
+
+
+def test_lmhead_vocab_limit():
+    assert _lm(V=262145, K=16) == -2

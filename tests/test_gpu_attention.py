@@ -116,10 +116,10 @@ def test_eviction_recompute_matches_cached_verify():
     L, k = int(b.ctx_lens[0]), int(b.k[0])
     cached, kc_after, vc_after = parity.run_gpu_attention(mdl, b)
     # rebuild the whole prefix's K/V from the appended cache
-    ps = mdl.k_pool.shape[2]
+    ps = mdl.k_pool.shape[3]
     pos = torch.arange(L + k, device=dev)
     pages = mdl.page_table[0].long()[pos // ps]
-    Kall = kc_after[pages, :, pos % ps, :].contiguous()
+    Kall = kc_after[pages, :, :, pos % ps, :].reshape(L + k, mdl.shape.Hkv, mdl.shape.D).contiguous()
     Vall = vc_after[pages, :, :, pos % ps].contiguous()
     qpre = torch.randn(L, mdl.shape.Hq, mdl.shape.D, device=dev).to(mdl.q.dtype)
     qall = torch.cat([qpre, mdl.q[:k]]).contiguous()

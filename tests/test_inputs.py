@@ -29,8 +29,8 @@ def test_tiny_config_structure_and_poison():
     # cached slots are finite, slots at and after L are poison
     L = b.ctx_lens[0]
     page = pt[0, L // ps]
-    assert np.all(np.isnan(kp[page, :, L % ps, :]))
-    assert np.all(np.isfinite(kp[pt[0, 0], :, 0, :]))
+    assert np.all(np.isnan(kp[page, :, :, L % ps, :]))
+    assert np.all(np.isfinite(kp[pt[0, 0], :, :, 0, :]))
 
 
 def test_seeded_and_reproducible():

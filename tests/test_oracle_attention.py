@@ -19,10 +19,11 @@ RNG = np.random.default_rng(1234)
 def build_paged(Kseq, Vseq, ps, num_pages, pages):
     """Test-side writer of the documented layouts from contiguous K/V [n, Hkv, D]."""
     n, Hkv, D = Kseq.shape
-    kc = np.full((num_pages, Hkv, ps, D), np.nan)
+    kc = np.full((num_pages, Hkv, D // 32, ps, 32), np.nan)
     vc = np.full((num_pages, Hkv, D, ps), np.nan)
     for p in range(n):
-        kc[pages[p // ps], :, p % ps, :] = Kseq[p]
+        for d in range(D):
+            kc[pages[p // ps], :, d // 32, p % ps, d % 32] = Kseq[p, :, d]
         vc[pages[p // ps], :, :, p % ps] = Vseq[p]
     return kc, vc
 
@@ -66,8 +67,8 @@ def sdpa_reference(q, Kall, Vall, L, scale):
 
 
 @pytest.mark.parametrize("L,k,Hq,Hkv,D,ps", [
-    (37, 4, 4, 2, 16, 16), (0, 5, 4, 4, 8, 16), (64, 1, 8, 2, 32, 16),
-    (100, 8, 6, 3, 16, 32), (15, 3, 2, 1, 8, 8)])
+    (37, 4, 4, 2, 32, 16), (0, 5, 4, 4, 32, 16), (64, 1, 8, 2, 64, 16),
+    (100, 8, 6, 3, 32, 32), (15, 3, 2, 1, 64, 8)])
 def test_matches_torch_sdpa_fp64(L, k, Hq, Hkv, D, ps):
     c = one_seq_case(L, k, Hq, Hkv, D, ps)
     scale = 1.0 / np.sqrt(D)
@@ -77,7 +78,7 @@ def test_matches_torch_sdpa_fp64(L, k, Hq, Hkv, D, ps):
 
 
 def test_window_rows_appended_into_pages():
-    c = one_seq_case(20, 6, 4, 2, 8, 16)
+    c = one_seq_case(20, 6, 4, 2, 32, 16)
     _, kc, vc = run(c, 0.3)
     K, V = oracle.gather_sequence(kc, vc, c["pt"], 0, 26)
     np.testing.assert_array_equal(K, c["Kall"])
@@ -85,7 +86,7 @@ def test_window_rows_appended_into_pages():
 
 
 def test_constant_values_give_constant_output():
-    c = one_seq_case(33, 4, 4, 2, 16, 16)
+    c = one_seq_case(33, 4, 4, 2, 32, 16)
     c["vc"][:] = 2.5
     c["v_new"][:] = 2.5
     out, _, _ = run(c, 0.25)
@@ -94,7 +95,7 @@ def test_constant_values_give_constant_output():
 
 def test_zero_query_gives_mean_of_visible_values():
     L, k = 29, 5
-    c = one_seq_case(L, k, 4, 2, 16, 16)
+    c = one_seq_case(L, k, 4, 2, 32, 16)
     c["q"][:] = 0.0
     out, _, _ = run(c, 0.25)
     G = 2
@@ -105,7 +106,7 @@ def test_zero_query_gives_mean_of_visible_values():
 
 
 def test_dominant_key_selects_its_value():
-    L, k, D = 40, 3, 16
+    L, k, D = 40, 3, 32
     c = one_seq_case(L, k, 2, 1, D, 16)
     j = 17
     c["q"][:] = 0.0
@@ -121,7 +122,7 @@ def test_dominant_key_selects_its_value():
 
 
 def test_k_window_equals_sequential_decode_with_append():
-    L, k, Hq, Hkv, D, ps = 45, 6, 4, 2, 16, 16
+    L, k, Hq, Hkv, D, ps = 45, 6, 4, 2, 32, 16
     c = one_seq_case(L, k, Hq, Hkv, D, ps)
     scale = 0.2
     win, _, _ = run(c, scale)
@@ -135,7 +136,7 @@ def test_k_window_equals_sequential_decode_with_append():
 
 def test_k1_verify_equals_single_token_decode():
     """k = 1: one query over L cached keys plus its own, written directly."""
-    L, Hq, Hkv, D = 50, 4, 4, 8
+    L, Hq, Hkv, D = 50, 4, 4, 32
     c = one_seq_case(L, 1, Hq, Hkv, D, 16)
     out, _, _ = run(c, 0.5)
     for h in range(Hq):
@@ -149,8 +150,8 @@ def test_k1_verify_equals_single_token_decode():
 def test_paged_equals_contiguous_and_page_permutation_invariant():
     rng1 = np.random.default_rng(7)
     rng2 = np.random.default_rng(7)
-    a = one_seq_case(70, 5, 4, 2, 16, 16, rng=rng1, permute=False)
-    b = one_seq_case(70, 5, 4, 2, 16, 16, rng=rng2, permute=True)
+    a = one_seq_case(70, 5, 4, 2, 32, 16, rng=rng1, permute=False)
+    b = one_seq_case(70, 5, 4, 2, 32, 16, rng=rng2, permute=True)
     assert not np.array_equal(a["pt"], b["pt"])
     oa, _, _ = run(a, 0.25)
     ob, _, _ = run(b, 0.25)
@@ -158,7 +159,7 @@ def test_paged_equals_contiguous_and_page_permutation_invariant():
 
 
 def test_gqa_equals_mha_with_repeated_kv_heads():
-    L, k, Hq, Hkv, D = 31, 4, 8, 2, 16
+    L, k, Hq, Hkv, D = 31, 4, 8, 2, 32
     c = one_seq_case(L, k, Hq, Hkv, D, 16)
     out, _, _ = run(c, 0.25)
     G = Hq // Hkv
@@ -177,7 +178,7 @@ def test_eviction_recompute_equals_cached_verify():
     """A preempted request recomputes its whole prefix (Section 3.2.3): a
     from-scratch pass with no cached tokens over all L+k rows must give the
     cached verify's k rows as its last k rows."""
-    L, k, Hq, Hkv, D, ps = 23, 4, 4, 2, 16, 16
+    L, k, Hq, Hkv, D, ps = 23, 4, 4, 2, 32, 16
     c = one_seq_case(L, k, Hq, Hkv, D, ps)
     rng = np.random.default_rng(99)
     q_prefix = rng.standard_normal((L, Hq, D))
@@ -192,7 +193,7 @@ def test_eviction_recompute_equals_cached_verify():
 
 def test_seq_ids_subset_and_multi_sequence_rows():
     rng = np.random.default_rng(5)
-    Hq, Hkv, D, ps = 4, 2, 8, 16
+    Hq, Hkv, D, ps = 4, 2, 32, 16
     Ls, ks = [10, 0, 33], [3, 2, 1]
     cu = np.concatenate([[0], np.cumsum(ks)])
     T = cu[-1]
@@ -200,7 +201,7 @@ def test_seq_ids_subset_and_multi_sequence_rows():
     kn = rng.standard_normal((T, Hkv, D))
     vn = rng.standard_normal((T, Hkv, D))
     npg = 20
-    kc = rng.standard_normal((npg, Hkv, ps, D))
+    kc = rng.standard_normal((npg, Hkv, D // 32, ps, 32))
     vc = rng.standard_normal((npg, Hkv, D, ps))
     pt = np.array([[3, 4, 19], [5, 19, 19], [6, 7, 8]])
     full, _, _ = oracle.verify_attn_paged(q, kn, vn, kc, vc, pt, np.array(Ls), cu, 0.3)
@@ -222,14 +223,14 @@ def test_large_scores_stay_finite_and_match_shifted_case():
     """Softmax is shift-invariant: adding a constant to every score of a row
     (here via a shared key component the query projects onto strongly) must
     not change the output, even when exp of the raw scores would overflow."""
-    L, k, D = 12, 2, 8
+    L, k, D = 12, 2, 32
     c = one_seq_case(L, k, 1, 1, D, 16)
     c["q"][:] = 0.0
     c["q"][:, :, 0] = 1.0
     base, _, _ = run(c, 1.0)
     shifted = dict(c)
     shifted["kc"] = c["kc"].copy()
-    shifted["kc"][:, :, :, 0] += 5000.0
+    shifted["kc"][:, :, 0, :, 0] += 5000.0
     shifted["k_new"] = c["k_new"].copy()
     shifted["k_new"][:, :, 0] += 5000.0
     out, _, _ = run(shifted, 1.0)
