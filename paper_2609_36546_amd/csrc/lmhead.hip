@@ -6,34 +6,35 @@
 // of the coverage rule (Eq. (5)) and the entropy.
 //
 // Kernel 1 (GEMM + epilogue).  logits^T = W . hidden^T with
-// v_mfma_f32_32x32x16_bf16: A = 32 vocabulary rows of W (read straight from
-// HBM into registers: each W element is used by exactly one wave), B = 32
-// hidden rows staged through LDS (shared by the four waves).  A workgroup
-// owns 256 vocabulary entries x up to 128 hidden rows; wave w owns the
-// vocabulary quarter [64w, 64w+64).  In the accumulator layout a lane holds
-// one hidden row and 16 vocabulary entries per 32x32 block, so every per-row
-// reduction over the vocabulary is in-lane plus one exchange with lane l^32.
-// For each (row, 64-entry group) the epilogue emits a 20-byte record: the
-// largest logit v1 and its index, the second largest v2 and its index,
+// v_mfma_f32_32x32x16_bf16 (A = 32 vocabulary rows of W, B = 32 hidden rows).
+// A workgroup owns 256 vocabulary entries x 64*RB hidden rows; both tiles are
+// staged through LDS 64 channels at a time (double buffered, 8 lanes per
+// 128-byte line on the global side, padded rows so that the MFMA operand
+// reads are bank-conflict free).  Its 2x2 waves each own 128 vocabulary
+// entries x 32*RB rows: 4 x RB MFMA blocks for 4 + RB operand reads per
+// k-step.  In the accumulator layout a lane holds one hidden row and 16
+// vocabulary entries per 32x32 block, so every per-row reduction over the
+// vocabulary is in-lane plus one exchange with lane l^32.  For each (row,
+// 128-entry group) the epilogue emits a record: the largest logit v1 and its
+// index, the second largest v2 and its index, the third largest value v3,
 // s = sum exp(l - v1) and e = sum exp(l - v1) * l.
 //
 // Kernel 2 (merge, one workgroup per row).  LSE = M + log sum_g s_g e^(v1_g-M),
 // entropy = LSE - (sum_g e_g e^(v1_g-M)) / (sum_g s_g e^(v1_g-M)).  Top-K: the
-// K best of the recorded (v1, v2) candidates; a group whose v2 made it into
-// that list may hide a third element that belongs too, so such a group's 64
-// logits are recomputed exactly and the selection is redone -- the result is
-// the exact top-K of all V logits (ties: lower index first).  The proposal's
-// logit is one dot product.
+// K best of the recorded (v1, v2) candidates; a group with two picks whose
+// recorded third value reaches the K-th pick may hide further members, so
+// such a group's logits are recomputed exactly and the selection is redone --
+// the result is the exact top-K of all V logits (ties: lower index first).  The proposal's logit is one dot product.
 #include "common.h"
 #include "kernels.h"
+
+#include <cstdlib>
 
 namespace ipdv {
 namespace {
 
 constexpr int kVT = 256;      // vocabulary entries per workgroup
-constexpr int kGroup = 64;    // vocabulary entries per record (one wave's share)
-constexpr int kStage = 64;    // hidden channels per pipeline stage
-constexpr int kLdsPad = 8;    // elements of padding per LDS row (bank spread)
+constexpr int kGroup = 128;   // vocabulary entries per record (one wave's share)
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
@@ -50,6 +51,7 @@ struct LmParams {
   float* rec_e;
   int32_t* rec_idx;   // index of v1
   int32_t* rec_i2;    // index of v2
+  float* rec_v3;      // third largest logit of the group (value only)
   float* lse;
   float* logp_prop;
   int32_t* argmax;
@@ -58,62 +60,30 @@ struct LmParams {
   float* entropy;
 };
 
+// MFMA flavour per input type.  STAGE = hidden channels per pipeline stage;
+// a lane supplies its k-step operand from channels koff(ks, h) of the stage
+// (h = lane / 32).  Any bijection works as long as A and B agree.
 template <typename DT> struct Mm;
 
 template <> struct Mm<bf16> {
-  static constexpr int KSTEPS = kStage / 16;      // MFMA k-steps per stage
+  static constexpr int STAGE = 64;
+  static constexpr int KSTEPS = STAGE / 16;
   typedef bf16x8 frag;
   __device__ static floatx16 mma(frag a, frag b, floatx16 c) {
     return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
   }
+  __device__ static int koff(int ks, int h) { return 16 * ks + 8 * h; }
 };
 
 template <> struct Mm<float> {
-  static constexpr int KSTEPS = kStage / 2;
+  static constexpr int STAGE = 32;
+  static constexpr int KSTEPS = STAGE / 2;
   typedef float frag;
   __device__ static floatx16 mma(frag a, frag b, floatx16 c) {
     return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
   }
+  __device__ static int koff(int ks, int h) { return 16 * h + ks; }
 };
-
-// Hidden-channel offset, within a stage, of the value(s) lane half h supplies
-// at k-step ks.  Any bijection works as long as A and B agree; these keep each
-// lane's loads contiguous.
-template <typename DT> __device__ __forceinline__ int koff(int ks, int h);
-template <> __device__ __forceinline__ int koff<bf16>(int ks, int h) { return 16 * ks + 8 * h; }
-template <> __device__ __forceinline__ int koff<float>(int ks, int h) { return 32 * h + ks; }
-
-template <typename DT>
-struct WFrags {
-  typename Mm<DT>::frag a[2][Mm<DT>::KSTEPS];
-};
-
-template <typename DT>
-__device__ __forceinline__ void load_w(const LmParams& p, WFrags<DT>& f, int vbase, int k0) {
-  const int lane = lane_id();
-  const int h = lane >> 5;
-  const DT* W = reinterpret_cast<const DT*>(p.W);
-#pragma unroll
-  for (int vb = 0; vb < 2; ++vb) {
-    const int v = vbase + 32 * vb + (lane & 31);
-    const bool ok = v < p.V;
-    const DT* row = W + (size_t)(ok ? v : 0) * p.Hd + k0;
-    if constexpr (sizeof(DT) == 2) {
-#pragma unroll
-      for (int ks = 0; ks < Mm<DT>::KSTEPS; ++ks) {
-        bf16x8 x = ld16<bf16x8>(row + koff<DT>(ks, h));
-        f.a[vb][ks] = ok ? x : bf16x8{};
-      }
-    } else {
-#pragma unroll
-      for (int c = 0; c < 8; ++c) {
-        floatx4 x = ld16<floatx4>(row + 32 * h + 4 * c);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) f.a[vb][4 * c + e] = ok ? x[e] : 0.f;
-      }
-    }
-  }
-}
 
 // Top-2 (value desc, index asc) insertion of (x, ix).
 __device__ __forceinline__ void top2_push(float x, int ix, float& v1, int& i1, float& v2, int& i2) {
@@ -127,6 +97,78 @@ __device__ __forceinline__ void top2_push(float x, int ix, float& v1, int& i1, f
   i2 = ni2;
 }
 
+// Top-2 with indices plus the third value: (v1, i1) >= (v2, i2) >= v3.
+__device__ __forceinline__ void top3_push(float x, int ix, float& v1, int& i1, float& v2, int& i2,
+                                          float& v3) {
+  v3 = fmaxf(v3, fminf(v2, x));
+  top2_push(x, ix, v1, i1, v2, i2);
+}
+
+typedef __attribute__((__vector_size__(16))) int i32x4;
+
+// Epilogue: per hidden row (lane column) and this wave's 128 vocabulary
+// entries, the group record (v1/i1, v2/i2, v3, s, e).  Register e of block vb
+// holds vocabulary entry vbase + 32 vb + 8 (e / 4) + 4 h + e % 4.
+template <int RB>
+__device__ __forceinline__ void lm_epilogue(const LmParams& p, floatx16 (&acc)[4][RB], int vt, int m0,
+                                            int wv, int wr) {
+  const int lane = lane_id();
+  const int h = lane >> 5;
+  const int vbase = vt * kVT + kGroup * wv;
+  const int g = vt * (kVT / kGroup) + wv;
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    const int m = m0 + 32 * RB * wr + 32 * rb + (lane & 31);
+    float mx = -INFINITY;
+#pragma unroll
+    for (int vb = 0; vb < 4; ++vb)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int v = vbase + 32 * vb + 8 * (e >> 2) + 4 * h + (e & 3);
+        if (v >= p.V) acc[vb][rb][e] = -INFINITY;
+        mx = fmaxf(mx, acc[vb][rb][e]);
+      }
+    mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+    const float mub = ((mx == -INFINITY) ? 0.f : mx) * kLog2e;
+    float s = 0.f, ee = 0.f;
+    float v1 = -INFINITY, v2 = -INFINITY, v3 = -INFINITY;
+    int i1 = 0x7fffffff, i2 = 0x7fffffff;
+#pragma unroll
+    for (int vb = 0; vb < 4; ++vb)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const float x = acc[vb][rb][e];
+        const int v = vbase + 32 * vb + 8 * (e >> 2) + 4 * h + (e & 3);
+        const float pe = fast_exp2(fmaf(x, kLog2e, -mub));
+        s += pe;
+        ee += (v < p.V) ? pe * x : 0.f;
+        top3_push(x, v, v1, i1, v2, i2, v3);
+      }
+    s += __shfl_xor(s, 32, kWave);
+    ee += __shfl_xor(ee, 32, kWave);
+    {
+      // merge the partner lane's (top-2, third value): the third of the union
+      // is max(third after pushing its top-2, its third)
+      const float ov1 = __shfl_xor(v1, 32, kWave), ov2 = __shfl_xor(v2, 32, kWave);
+      const float ov3 = __shfl_xor(v3, 32, kWave);
+      const int oi1 = __shfl_xor(i1, 32, kWave), oi2 = __shfl_xor(i2, 32, kWave);
+      top3_push(ov1, oi1, v1, i1, v2, i2, v3);
+      top3_push(ov2, oi2, v1, i1, v2, i2, v3);
+      v3 = fmaxf(v3, ov3);
+    }
+    if (h == 0 && m < p.M && g < p.n_groups) {
+      const size_t r = (size_t)m * p.n_groups + g;
+      p.rec_v1[r] = v1;
+      p.rec_v2[r] = v2;
+      p.rec_s[r] = (mx == -INFINITY) ? 0.f : s;
+      p.rec_e[r] = (mx == -INFINITY) ? 0.f : ee;
+      p.rec_idx[r] = i1;
+      p.rec_i2[r] = i2;
+      p.rec_v3[r] = v3;
+    }
+  }
+}
+
 template <typename DT, int RB>
 __global__ __launch_bounds__(256) void lmhead_gemm_kernel(LmParams p) {
   // XCD-aware order: the row tiles of one vocabulary tile are consecutive in
@@ -137,136 +179,223 @@ __global__ __launch_bounds__(256) void lmhead_gemm_kernel(LmParams p) {
   const int vt = (local / p.n_rt) * 8 + xcd;
   const int rt = local % p.n_rt;
   if (vt >= p.n_vt) return;
-  constexpr int NM = 32 * RB;
+  typedef Mm<DT> MM;
+  constexpr int NM = 64 * RB;                       // hidden rows per workgroup
+  constexpr int LDW = MM::STAGE + 16 / (int)sizeof(DT);   // LDS row pitch (elements)
+  constexpr int EPL = 16 / (int)sizeof(DT);         // elements per 16-byte load
+  constexpr int CPR = MM::STAGE / EPL;              // 16-byte chunks per row and stage
+  constexpr int NLW = kVT * CPR / 256;              // W loads per thread and stage
+  constexpr int NLH = NM * CPR / 256;               // hidden loads per thread and stage
   const int m0 = rt * NM;
   const int v0 = vt * kVT;
   const int tid = threadIdx.x;
   const int w = tid >> 6;
+  const int wv = w & 1, wr = w >> 1;
   const int lane = lane_id();
   const int h = lane >> 5;
-  const int vbase = v0 + kGroup * w;
 
-  constexpr int LDW = kStage + kLdsPad;
-  __shared__ DT s_h[2][NM * LDW];
+  __shared__ __attribute__((aligned(16))) DT s_w[2][kVT * LDW];
+  __shared__ __attribute__((aligned(16))) DT s_h[2][NM * LDW];
 
-  const DT* hid = reinterpret_cast<const DT*>(p.hidden);
-  // Staging of one hidden stage: NM rows x 64 channels, 16 bytes per thread-load.
-  constexpr int EPL = 16 / sizeof(DT);            // elements per 16-byte load
-  constexpr int LPR = kStage / EPL;               // loads per row
-  constexpr int NLD = (NM * LPR + 255) / 256;     // loads per thread
-  typedef __attribute__((__vector_size__(16))) int i32x4;
-  i32x4 stage_regs[NLD];
+  const DT* Wp = reinterpret_cast<const DT*>(p.W);
+  const DT* Hp = reinterpret_cast<const DT*>(p.hidden);
+  i32x4 rw[NLW], rh[NLH];
+  const int nst = p.Hd / MM::STAGE;
 
-  auto load_hidden = [&](int k0) {
+  auto load_stage = [&](int k0) {
 #pragma unroll
-    for (int u = 0; u < NLD; ++u) {
+    for (int u = 0; u < NLW; ++u) {
       const int e = tid + 256 * u;
-      const int r = e / LPR, c = e % LPR;
-      const int m = m0 + r;
-      i32x4 x = {0, 0, 0, 0};
-      if (r < NM && m < p.M) x = ld16<i32x4>(hid + (size_t)m * p.Hd + k0 + EPL * c);
-      stage_regs[u] = x;
+      const int r = e / CPR, c = e % CPR;
+      const int v = min(v0 + r, p.V - 1);           // rows past V: any valid row, masked later
+      rw[u] = ld16<i32x4>(Wp + (size_t)v * p.Hd + k0 + EPL * c);
+    }
+#pragma unroll
+    for (int u = 0; u < NLH; ++u) {
+      const int e = tid + 256 * u;
+      const int r = e / CPR, c = e % CPR;
+      const int m = min(m0 + r, p.M - 1);           // rows past M: any valid row, never read
+      rh[u] = ld16<i32x4>(Hp + (size_t)m * p.Hd + k0 + EPL * c);
     }
   };
-  auto store_hidden = [&](int buf) {
+  auto store_stage = [&](int buf) {
 #pragma unroll
-    for (int u = 0; u < NLD; ++u) {
+    for (int u = 0; u < NLW; ++u) {
       const int e = tid + 256 * u;
-      const int r = e / LPR, c = e % LPR;
-      if (r < NM) *reinterpret_cast<i32x4*>(&s_h[buf][r * LDW + EPL * c]) = stage_regs[u];
+      *reinterpret_cast<i32x4*>(&s_w[buf][(e / CPR) * LDW + EPL * (e % CPR)]) = rw[u];
+    }
+#pragma unroll
+    for (int u = 0; u < NLH; ++u) {
+      const int e = tid + 256 * u;
+      *reinterpret_cast<i32x4*>(&s_h[buf][(e / CPR) * LDW + EPL * (e % CPR)]) = rh[u];
     }
   };
 
-  floatx16 acc[2][RB];
+  floatx16 acc[4][RB];
 #pragma unroll
-  for (int vb = 0; vb < 2; ++vb)
+  for (int vb = 0; vb < 4; ++vb)
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[vb][rb][e] = 0.f;
 
-  const int nst = p.Hd / kStage;
-  WFrags<DT> fa, fb;
-  load_hidden(0);
-  load_w<DT>(p, fa, vbase, 0);
-  store_hidden(0);
+  load_stage(0);
+  store_stage(0);
   for (int st = 0; st < nst; ++st) {
     const bool more = st + 1 < nst;
-    if (more) {
-      load_hidden((st + 1) * kStage);
-      load_w<DT>(p, fb, vbase, (st + 1) * kStage);
-    }
+    if (more) load_stage((st + 1) * MM::STAGE);
     __syncthreads();
-    const DT* sb = s_h[st & 1];
+    const DT* sw = s_w[st & 1] + (128 * wv + (lane & 31)) * LDW;
+    const DT* sh = s_h[st & 1] + (32 * RB * wr + (lane & 31)) * LDW;
 #pragma unroll
-    for (int ks = 0; ks < Mm<DT>::KSTEPS; ++ks) {
+    for (int ks = 0; ks < MM::KSTEPS; ++ks) {
+      const int ko = MM::koff(ks, h);
+      typename MM::frag a[4], b[RB];
 #pragma unroll
-      for (int rb = 0; rb < RB; ++rb) {
-        const DT* src = sb + (32 * rb + (lane & 31)) * LDW + koff<DT>(ks, h);
-        typename Mm<DT>::frag b;
-        if constexpr (sizeof(DT) == 2) b = *reinterpret_cast<const bf16x8*>(src);
-        else b = *src;
+      for (int vb = 0; vb < 4; ++vb) a[vb] = *reinterpret_cast<const typename MM::frag*>(sw + 32 * vb * LDW + ko);
 #pragma unroll
-        for (int vb = 0; vb < 2; ++vb) acc[vb][rb] = Mm<DT>::mma(fa.a[vb][ks], b, acc[vb][rb]);
-      }
+      for (int rb = 0; rb < RB; ++rb) b[rb] = *reinterpret_cast<const typename MM::frag*>(sh + 32 * rb * LDW + ko);
+#pragma unroll
+      for (int vb = 0; vb < 4; ++vb)
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) acc[vb][rb] = MM::mma(a[vb], b[rb], acc[vb][rb]);
     }
-    if (more) {
-      store_hidden((st + 1) & 1);
-      fa = fb;
-    }
+    if (more) store_stage((st + 1) & 1);
   }
 
-  // Epilogue: per hidden row (lane column) and this wave's 64 vocabulary
-  // entries.  Register e of block vb holds vocabulary entry
-  // vbase + 32 vb + 8 (e / 4) + 4 h + e % 4.
-  const int g = vt * (kVT / kGroup) + w;
+  lm_epilogue<RB>(p, acc, vt, m0, wv, wr);
+}
+
+// ---------------------------------------------------------------------------
+// bf16 GEMM with direct-to-LDS operand loads (global_load_lds_dwordx4).
+//
+// Each 16-byte load lands straight in LDS (lane i of an instruction fills
+// bytes 16 i .. 16 i + 15 of a 1 KB block), so no registers stage the tiles
+// and a 4-deep LDS ring keeps three 32-channel stages in flight while the
+// fourth is multiplied.  Rows are 64 bytes; the 16-byte chunk c of row r sits
+// at position c ^ ((r / 4) % 4), which puts the 16 rows an MFMA operand read
+// touches in distinct bank groups; the loading lane fetches the global chunk
+// that belongs at its position.
+// ---------------------------------------------------------------------------
+
+constexpr int kDStage = 32;   // hidden channels per stage (64 bytes per row)
+
+__device__ __forceinline__ int dl_off(int r, int c) { return 64 * r + 16 * (c ^ ((r >> 2) & 3)); }
+
+// One 16-byte direct-to-LDS load: lane i's bytes land at lds + 16 i (M0 holds
+// the wave-uniform LDS address).  Written as inline assembly so the compiler
+// does not add its own whole-queue waits before every LDS read: the ring's
+// explicit vmcnt wait + barrier order the accesses.  Compiler-generated waits
+// for its own loads stay correct, as vmcnt retires loads in issue order.
+__device__ __forceinline__ void dma16(const void* src, char* lds) {
+  const unsigned lds_addr = (unsigned)(uintptr_t)(__attribute__((address_space(3))) void*)lds;
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off"
+               :
+               : "s"(__builtin_amdgcn_readfirstlane(lds_addr)), "v"(src)
+               : "memory", "m0");
+}
+
+template <int RB>
+__global__ __launch_bounds__(256) void lmhead_gemm_dlds_kernel(LmParams p) {
+  const int id = blockIdx.x;
+  const int xcd = id & 7, local = id >> 3;
+  const int vt = (local / p.n_rt) * 8 + xcd;
+  const int rt = local % p.n_rt;
+  if (vt >= p.n_vt) return;
+  constexpr int NM = 64 * RB;
+  constexpr int WB = kVT * 64;                  // W tile bytes per stage
+  constexpr int SB = WB + NM * 64;              // stage bytes
+  constexpr int NBLK = (kVT + NM) / 16;         // 1 KB load blocks per stage
+  constexpr int PER_WAVE = NBLK / 4;            // load instructions per wave and stage
+  const int m0 = rt * NM;
+  const int v0 = vt * kVT;
+  const int tid = threadIdx.x;
+  const int w = tid >> 6;
+  const int wv = w & 1, wr = w >> 1;
+  const int lane = lane_id();
+  const int h = lane >> 5;
+  const int rr = lane & 31;
+  const int nst = p.Hd / kDStage;
+
+  __shared__ __attribute__((aligned(1024))) char s_b0[SB];
+  __shared__ __attribute__((aligned(1024))) char s_b1[SB];
+  __shared__ __attribute__((aligned(1024))) char s_b2[SB];
+  __shared__ __attribute__((aligned(1024))) char s_b3[SB];
+
+  const bf16* Wp = reinterpret_cast<const bf16*>(p.W);
+  const bf16* Hp = reinterpret_cast<const bf16*>(p.hidden);
+  // This lane's source row and chunk for each of its load blocks.
+  const bf16* src[PER_WAVE];
 #pragma unroll
-  for (int rb = 0; rb < RB; ++rb) {
-    const int m = m0 + 32 * rb + (lane & 31);
-    float mx = -INFINITY;
-#pragma unroll
-    for (int vb = 0; vb < 2; ++vb)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int v = vbase + 32 * vb + 8 * (e >> 2) + 4 * h + (e & 3);
-        if (v >= p.V) acc[vb][rb][e] = -INFINITY;
-        mx = fmaxf(mx, acc[vb][rb][e]);
-      }
-    mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
-    const float mu = (mx == -INFINITY) ? 0.f : mx;
-    const float mub = mu * kLog2e;
-    float s = 0.f, ee = 0.f;
-    float v1 = -INFINITY, v2 = -INFINITY;
-    int i1 = 0x7fffffff, i2 = 0x7fffffff;
-#pragma unroll
-    for (int vb = 0; vb < 2; ++vb)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const float x = acc[vb][rb][e];
-        const int v = vbase + 32 * vb + 8 * (e >> 2) + 4 * h + (e & 3);
-        const float pe = fast_exp2(x * kLog2e - mub);
-        s += pe;
-        ee += (v < p.V) ? pe * x : 0.f;
-        top2_push(x, v, v1, i1, v2, i2);
-      }
-    s += __shfl_xor(s, 32, kWave);
-    ee += __shfl_xor(ee, 32, kWave);
-    {
-      const float ov1 = __shfl_xor(v1, 32, kWave), ov2 = __shfl_xor(v2, 32, kWave);
-      const int oi1 = __shfl_xor(i1, 32, kWave), oi2 = __shfl_xor(i2, 32, kWave);
-      top2_push(ov1, oi1, v1, i1, v2, i2);
-      top2_push(ov2, oi2, v1, i1, v2, i2);
-    }
-    if (h == 0 && m < p.M && g < p.n_groups) {
-      const size_t r = (size_t)m * p.n_groups + g;
-      p.rec_v1[r] = v1;
-      p.rec_v2[r] = v2;
-      p.rec_s[r] = (mx == -INFINITY) ? 0.f : s;
-      p.rec_e[r] = (mx == -INFINITY) ? 0.f : ee;
-      p.rec_idx[r] = i1;
-      p.rec_i2[r] = i2;
+  for (int j = 0; j < PER_WAVE; ++j) {
+    const int u = w + 4 * j;
+    const int r = (u < kVT / 16 ? 16 * u : 16 * (u - kVT / 16)) + (lane >> 2);
+    const int c = (lane & 3) ^ ((r >> 2) & 3);
+    if (u < kVT / 16) {
+      const int v = min(v0 + r, p.V - 1);       // rows past V: any valid row, masked later
+      src[j] = Wp + (size_t)v * p.Hd + 8 * c;
+    } else {
+      const int m = min(m0 + r, p.M - 1);       // rows past M: any valid row, never stored
+      src[j] = Hp + (size_t)m * p.Hd + 8 * c;
     }
   }
+  auto issue = [&](char* buf, int st) {
+    const int k0 = min(st, nst - 1) * kDStage;  // past the end: reload the last stage (unused)
+#pragma unroll
+    for (int j = 0; j < PER_WAVE; ++j) {
+      const int u = w + 4 * j;
+      dma16(src[j] + k0, buf + 1024 * u);
+    }
+  };
+
+  floatx16 acc[4][RB];
+#pragma unroll
+  for (int vb = 0; vb < 4; ++vb)
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[vb][rb][e] = 0.f;
+
+  auto step = [&](const char* cur, char* nxt, int st) {
+    // Own loads of stage st are done once at most two later stages' are
+    // pending; after the barrier every wave's are, and every wave has finished
+    // reading the buffer the next issue overwrites.  A bare s_barrier: the
+    // fence of __syncthreads would wait for the stages still in flight.
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * PER_WAVE) : "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    issue(nxt, st + 3);
+#pragma unroll
+    for (int ks = 0; ks < kDStage / 16; ++ks) {
+      const int c = 2 * ks + h;
+      bf16x8 a[4], b[RB];
+#pragma unroll
+      for (int vb = 0; vb < 4; ++vb)
+        a[vb] = *reinterpret_cast<const bf16x8*>(cur + dl_off(128 * wv + 32 * vb + rr, c));
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb)
+        b[rb] = *reinterpret_cast<const bf16x8*>(cur + WB + dl_off(32 * RB * wr + 32 * rb + rr, c));
+#pragma unroll
+      for (int vb = 0; vb < 4; ++vb)
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb)
+          acc[vb][rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[vb], b[rb], acc[vb][rb], 0, 0, 0);
+    }
+  };
+
+  issue(s_b0, 0);
+  issue(s_b1, 1);
+  issue(s_b2, 2);
+  for (int st = 0; st < nst; st += 4) {     // nst % 4 == 0 (checked by the planner)
+    step(s_b0, s_b3, st);
+    step(s_b1, s_b0, st + 1);
+    step(s_b2, s_b1, st + 2);
+    step(s_b3, s_b2, st + 3);
+  }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // the trailing reloads
+  __syncthreads();
+
+  lm_epilogue<RB>(p, acc, vt, m0, wv, wr);
 }
 
 // ---------------------------------------------------------------------------
@@ -366,23 +495,29 @@ __device__ __forceinline__ void wave_topk(const float (&cv)[N], const int (&ci)[
   }
 }
 
+constexpr int kCap = 2048;     // survivor list capacity (candidates >= theta)
+
 template <typename DT>
 __global__ __launch_bounds__(kMT) void lmhead_merge_kernel(LmParams p) {
   const int m = blockIdx.x;
   const int tid = threadIdx.x;
   const int wv = tid >> 6;
+  const int lane = lane_id();
   const int G = p.n_groups;
   const int K = p.K;
   const size_t base = (size_t)m * G;
   constexpr int NW = kMT / kWave;
   __shared__ float s_red[8];
+  __shared__ float s_theta[NW];
   __shared__ float s_wv[NW][IPDV_MAX_K_DEV];
   __shared__ int s_wi[NW][IPDV_MAX_K_DEV];
   __shared__ float s_top_v[IPDV_MAX_K_DEV];
   __shared__ int s_top_i[IPDV_MAX_K_DEV];
   __shared__ int s_split[kMaxSplit];
-  __shared__ int s_nsplit;
-  __shared__ float s_cv[kSplitCand];   // recomputed logits of split groups
+  __shared__ int s_nsplit, s_n;
+  __shared__ float s_lv[kCap];          // survivors, then survivors + recomputed logits
+  __shared__ int s_li[kCap];
+  __shared__ float s_cv[kSplitCand];    // recomputed logits of split groups
   __shared__ int s_ci[kSplitCand];
 
   // This thread's groups: tid, tid + kMT, ... (register resident).
@@ -399,6 +534,7 @@ __global__ __launch_bounds__(kMT) void lmhead_merge_kernel(LmParams p) {
     ci[2 * u + 1] = ok ? p.rec_i2[base + gi] : 0x7fffffff;
     mx = fmaxf(mx, cv[2 * u]);
   }
+  if (tid == 0) { s_n = 0; s_nsplit = 0; }
 
   // Log-sum-exp and entropy sums (group maxima are the v1 records).
   const float M = block_max(mx, s_red);
@@ -417,36 +553,73 @@ __global__ __launch_bounds__(kMT) void lmhead_merge_kernel(LmParams p) {
   E = block_sum(E, s_red);
   const float lse = Mu + fast_log2(S) * kLn2;
 
-  // Exact top-K.  Round 0 picks from the recorded (v1, v2) pairs.  A group
-  // with two picks may hide a third member, so its 64 logits are recomputed
-  // and round 1 picks again from the records of the other groups plus every
-  // recomputed value; then each element left out ranks after the K-th pick.
-  int nsplit = 0;
+  // theta: a lower bound of the K-th largest logit.  The K largest lane
+  // maxima of a wave are K distinct logits, so the smallest of them bounds
+  // the K-th largest from below; theta is the best of the waves' bounds.
+  {
+    float lm = mx;
+    float th = -INFINITY;
+    for (int k = 0; k < K; ++k) {
+      float bv = lm;
+      int bl = lane;
+      wave_best(bv, bl);
+      if (k == K - 1) th = bv;
+      if (lane == bl) lm = -INFINITY;
+    }
+    if (lane == 0) s_theta[wv] = th;
+  }
+  __syncthreads();
+  float theta = s_theta[0];
+  for (int w2 = 1; w2 < NW; ++w2) theta = fmaxf(theta, s_theta[w2]);
+  // survivors: candidates >= theta
+#pragma unroll
+  for (int c = 0; c < 2 * kMaxGPT; ++c) {
+    if (ci[c] != 0x7fffffff && cv[c] >= theta) {
+      const int slot = atomicAdd(&s_n, 1);
+      if (slot < kCap) { s_lv[slot] = cv[c]; s_li[slot] = ci[c]; }
+    }
+  }
+  __syncthreads();
+  const bool overflow = s_n > kCap;     // many ties at theta: select from all records
+  int n_list = min(s_n, kCap);
+
+  // Exact top-K.  Round 0 picks from the candidates; a group with two picks
+  // may hide a third member, so its logits are recomputed and round 1 picks
+  // again (then every element left out ranks after the K-th pick).
   for (int round = 0; round < 2; ++round) {
-    wave_topk(cv, ci, s_cv, s_ci, nsplit * kGroup, K, s_wv[wv], s_wi[wv]);
-    __syncthreads();
-    if (wv == 0) {
-      float xv0 = -INFINITY, xv1 = -INFINITY;
-      int xi0 = 0x7fffffff, xi1 = 0x7fffffff;
-      const int lane = lane_id();
-      if (lane < NW * K) { xv0 = s_wv[lane / K][lane % K]; xi0 = s_wi[lane / K][lane % K]; }
-      if (lane + kWave < NW * K) {
-        xv1 = s_wv[(lane + kWave) / K][(lane + kWave) % K];
-        xi1 = s_wi[(lane + kWave) / K][(lane + kWave) % K];
+    const int ns = s_nsplit;
+    if (overflow) {
+      wave_topk(cv, ci, s_cv, s_ci, ns * kGroup, K, s_wv[wv], s_wi[wv]);
+      __syncthreads();
+      if (wv == 0) {
+        float xv0 = -INFINITY, xv1 = -INFINITY;
+        int xi0 = 0x7fffffff, xi1 = 0x7fffffff;
+        if (lane < NW * K) { xv0 = s_wv[lane / K][lane % K]; xi0 = s_wi[lane / K][lane % K]; }
+        if (lane + kWave < NW * K) {
+          xv1 = s_wv[(lane + kWave) / K][(lane + kWave) % K];
+          xi1 = s_wi[(lane + kWave) / K][(lane + kWave) % K];
+        }
+        const float fv[2] = {xv0, xv1};
+        const int fi[2] = {xi0, xi1};
+        wave_topk(fv, fi, s_cv, s_ci, 0, K, s_top_v, s_top_i);
       }
-      const float fv[2] = {xv0, xv1};
-      const int fi[2] = {xi0, xi1};
-      wave_topk(fv, fi, s_cv, s_ci, 0, K, s_top_v, s_top_i);
+    } else if (wv == 0) {
+      const float none[1] = {-INFINITY};
+      const int nonei[1] = {0x7fffffff};
+      wave_topk(none, nonei, s_lv, s_li, n_list, K, s_top_v, s_top_i);
     }
     __syncthreads();
     if (round == 1) break;
-    // Groups picked twice.
+    // Groups picked twice whose third value reaches the K-th pick may hide
+    // further members: only those are recomputed.
     if (tid == 0) {
       int n = 0;
-      for (int a = 0; a < K; ++a)
-        for (int b2 = a + 1; b2 < K; ++b2)
-          if (s_top_i[a] != 0x7fffffff && s_top_i[a] / kGroup == s_top_i[b2] / kGroup) {
-            const int gsp = s_top_i[a] / kGroup;
+      const float yk = s_top_v[K - 1];
+      for (int a2 = 0; a2 < K; ++a2)
+        for (int b2 = a2 + 1; b2 < K; ++b2)
+          if (s_top_i[a2] != 0x7fffffff && s_top_i[a2] / kGroup == s_top_i[b2] / kGroup) {
+            const int gsp = s_top_i[a2] / kGroup;
+            if (!(p.rec_v3[base + gsp] >= yk)) continue;
             bool seen = false;
             for (int t = 0; t < n; ++t) seen |= (s_split[t] == gsp);
             if (!seen && n < kMaxSplit) s_split[n++] = gsp;
@@ -454,29 +627,44 @@ __global__ __launch_bounds__(kMT) void lmhead_merge_kernel(LmParams p) {
       s_nsplit = n;
     }
     __syncthreads();
-    nsplit = s_nsplit;
+    const int nsplit = s_nsplit;
     if (nsplit == 0) break;
     for (int c = wv; c < nsplit * kGroup; c += NW) {
       const int v = s_split[c / kGroup] * kGroup + (c % kGroup);
       const bool ok = v < p.V;
       const float x = ok ? wave_dot<DT>(p, m, v) : -INFINITY;
-      if (lane_id() == 0) {
+      if (lane == 0) {
         s_cv[c] = x;
         s_ci[c] = ok ? v : 0x7fffffff;
       }
     }
-    // drop the split groups' records: their members now come from s_cv
+    if (overflow) {
+      // drop the split groups' records: their members now come from s_cv
 #pragma unroll
-    for (int u = 0; u < kMaxGPT; ++u) {
-      const int gi = tid + kMT * u;
-      bool sp = false;
-      for (int t = 0; t < nsplit; ++t) sp |= (s_split[t] == gi);
-      if (sp) {
-        cv[2 * u] = cv[2 * u + 1] = -INFINITY;
-        ci[2 * u] = ci[2 * u + 1] = 0x7fffffff;
+      for (int u = 0; u < kMaxGPT; ++u) {
+        const int gi = tid + kMT * u;
+        bool sp = false;
+        for (int t = 0; t < nsplit; ++t) sp |= (s_split[t] == gi);
+        if (sp) {
+          cv[2 * u] = cv[2 * u + 1] = -INFINITY;
+          ci[2 * u] = ci[2 * u + 1] = 0x7fffffff;
+        }
       }
     }
     __syncthreads();
+    if (!overflow && tid == 0) {
+      // survivors of split groups are replaced by the recomputed values
+      int n = 0;
+      for (int c = 0; c < n_list; ++c) {
+        bool sp = false;
+        for (int t = 0; t < nsplit; ++t) sp |= (s_li[c] / kGroup == s_split[t]);
+        if (!sp) { s_lv[n] = s_lv[c]; s_li[n] = s_li[c]; ++n; }
+      }
+      for (int c = 0; c < nsplit * kGroup && n < kCap; ++c) { s_lv[n] = s_cv[c]; s_li[n] = s_ci[c]; ++n; }
+      s_n = n;
+    }
+    __syncthreads();
+    n_list = s_n;
   }
 
   const int orow = p.out_rows ? p.out_rows[m] : m;
@@ -494,8 +682,23 @@ __global__ __launch_bounds__(kMT) void lmhead_merge_kernel(LmParams p) {
   const bool pok = pv >= 0 && pv < p.V;
   if (wv == 0) {
     const float lp = wave_dot<DT>(p, m, pok ? pv : 0);
-    if (lane_id() == 0) p.logp_prop[orow] = pok ? lp - lse : NAN;
+    if (lane == 0) p.logp_prop[orow] = pok ? lp - lse : NAN;
   }
+}
+
+// GEMM launch per input type: bf16 takes the direct-to-LDS kernel when the
+// hidden size is a multiple of four stages, fp32 the register-staged one.
+template <int RB>
+void launch_gemm(const LmParams& p, dim3 grid, hipStream_t st, bf16) {
+  if (p.Hd % (4 * kDStage) == 0)
+    hipLaunchKernelGGL((lmhead_gemm_dlds_kernel<RB>), grid, dim3(256), 0, st, p);
+  else
+    hipLaunchKernelGGL((lmhead_gemm_kernel<bf16, RB>), grid, dim3(256), 0, st, p);
+}
+
+template <int RB>
+void launch_gemm(const LmParams& p, dim3 grid, hipStream_t st, float) {
+  hipLaunchKernelGGL((lmhead_gemm_kernel<float, RB>), grid, dim3(256), 0, st, p);
 }
 
 template <typename DT, int RB>
@@ -503,7 +706,7 @@ hipError_t launch_rb(const LmParams& p, hipStream_t st) {
   const int n_vt_pad = (p.n_vt + 7) / 8 * 8;
   dim3 grid(n_vt_pad * p.n_rt);
   trace_begin(st);
-  hipLaunchKernelGGL((lmhead_gemm_kernel<DT, RB>), grid, dim3(256), 0, st, p);
+  launch_gemm<RB>(p, grid, st, DT{});
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   trace_mark(st);
@@ -519,13 +722,19 @@ LmPlan lm_plan(int M, int Hd, int V, int K, bool bf16) {
   LmPlan pl{};
   pl.n_groups = (V + kGroup - 1) / kGroup;
   pl.n_vt = (V + kVT - 1) / kVT;
-  const int rows = M < 128 ? M : 128;
-  pl.rb = rows <= 32 ? 1 : rows <= 64 ? 2 : rows <= 96 ? 3 : 4;
-  if (!bf16) pl.rb = 1;   // fp32 tiles keep their LDS stage under 64 KB
-  pl.n_rt = (M + 32 * pl.rb - 1) / (32 * pl.rb);
+  // 64*RB hidden rows per workgroup (RB <= 4); fp32 keeps RB = 1 so that its
+  // double-buffered stage fits the LDS.
+  const int rows = M < 256 ? M : 256;
+  pl.rb = rows <= 64 ? 1 : rows <= 128 ? 2 : rows <= 192 ? 3 : 4;
+  if (const char* e = getenv("IPDV_LM_RB")) {     // tuning sweeps only
+    const int x = atoi(e);
+    if (x >= 1 && x <= 4) pl.rb = x;
+  }
+  if (!bf16) pl.rb = 1;
+  pl.n_rt = (M + 64 * pl.rb - 1) / (64 * pl.rb);
   const size_t recs = (size_t)M * pl.n_groups;
   pl.rec_bytes = recs * sizeof(float);
-  pl.workspace_bytes = 6 * ((pl.rec_bytes + 255) / 256 * 256) + 256;
+  pl.workspace_bytes = 7 * ((pl.rec_bytes + 255) / 256 * 256) + 256;
   (void)Hd;
   (void)K;
   return pl;
@@ -553,6 +762,7 @@ hipError_t launch_lmhead(const LmLaunch& L, const LmPlan& pl, hipStream_t st) {
   p.rec_e = reinterpret_cast<float*>(ws + 3 * stride);
   p.rec_idx = reinterpret_cast<int32_t*>(ws + 4 * stride);
   p.rec_i2 = reinterpret_cast<int32_t*>(ws + 5 * stride);
+  p.rec_v3 = reinterpret_cast<float*>(ws + 6 * stride);
   p.lse = L.lse;
   p.logp_prop = L.logp_prop;
   p.argmax = L.argmax;

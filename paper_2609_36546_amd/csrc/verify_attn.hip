@@ -564,8 +564,9 @@ AttnPlan attn_plan(int n_seq, int Hq, int Hkv, int D, int max_q, int max_pages, 
       const long items = (long)n_seq * Hkv * pl.n_qg * ((max_keys_ub + 4L * s - 1) / (4L * s));
       if (items >= 4L * 256) { pl.sub = s; break; }
     }
-    while (pl.sub > 32 && pl.sub > 63 * page_size) pl.sub /= 2;
   }
+  // A wave's keys must span at most 64 pages (one page id per lane).
+  while (pl.sub > 32 && pl.sub > 63 * page_size) pl.sub /= 2;
   pl.chunk = kWaves * pl.sub;
   const long max_keys = (long)max_pages * page_size;
   int mc = (int)((max_keys + pl.chunk - 1) / pl.chunk);
