@@ -169,7 +169,8 @@ size_t ipdv_lmhead_workspace_size(int M, int Hd, int V, int K);
  * out_rows [M] int32 or NULL
  * lse, logp_prop, entropy: float [rows];  argmax int32 [rows];
  * topk_idx int32 [rows, K];  topk_logp float [rows, K]
- * Requirements: M >= 0, Hd % 64 == 0, 1 <= V <= 262144, 1 <= K <= min(IPDV_MAX_K, V).
+ * Requirements: M >= 0, Hd % 64 == 0 and Hd <= 4096, 1 <= V <= 262144,
+ * 1 <= K <= min(IPDV_MAX_K, V).
  *
  * Errors: IPDV_EINVAL, IPDV_EUNSUPPORTED (dtype, Hd), IPDV_EWORKSPACE, IPDV_EHIP.
  */

@@ -136,6 +136,7 @@ static int lm_shape_check(int M, int Hd, int V, int K) {
     return fail(IPDV_EINVAL, "K=%d must satisfy 1 <= K <= min(%d, V=%d)", K, IPDV_MAX_K, V);
   if (Hd < 64 || Hd % 64 != 0) return fail(IPDV_EUNSUPPORTED, "Hd=%d must be a positive multiple of 64", Hd);
   if (V > 262144) return fail(IPDV_EUNSUPPORTED, "V=%d exceeds 262144", V);
+  if (Hd > 4096) return fail(IPDV_EUNSUPPORTED, "Hd=%d exceeds 4096", Hd);
   if (M > 2147483647 / 2) return fail(IPDV_EUNSUPPORTED, "M too large");
   return IPDV_OK;
 }

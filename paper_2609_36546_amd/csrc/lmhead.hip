@@ -462,14 +462,28 @@ __device__ float wave_dot(const LmParams& p, int m, int v) {
 // Groups per merge thread held in registers: V <= kMT * kMaxGPT * kGroup.
 constexpr int kMaxGPT = 16;
 
-// Wave-wide best (value desc, index asc) of one candidate per lane.
+// One reduction step: combine with the (value, index) DPP moves in from
+// another lane; lanes without a source keep theirs.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ void best_step(float& v, int& ix) {
+  const float ov = __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(-INFINITY), __float_as_int(v),
+                                                              CTRL, ROW_MASK, 0xf, false));
+  const int oi = __builtin_amdgcn_update_dpp(0x7fffffff, ix, CTRL, ROW_MASK, 0xf, false);
+  if (before(ov, oi, v, ix)) { v = ov; ix = oi; }
+}
+
+// Wave-wide best (value desc, index asc) of one candidate per lane, returned
+// to every lane: DPP row shifts 1/2/4/8 and row broadcasts 15/31 carry the
+// best towards lane 63 (a few cycles per step, no LDS round trip).
 __device__ __forceinline__ void wave_best(float& v, int& ix) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    const float ov = __shfl_xor(v, o, kWave);
-    const int oi = __shfl_xor(ix, o, kWave);
-    if (before(ov, oi, v, ix)) { v = ov; ix = oi; }
-  }
+  best_step<0x111, 0xf>(v, ix);   // row_shr:1
+  best_step<0x112, 0xf>(v, ix);   // row_shr:2
+  best_step<0x114, 0xf>(v, ix);   // row_shr:4
+  best_step<0x118, 0xf>(v, ix);   // row_shr:8
+  best_step<0x142, 0xa>(v, ix);   // row_bcast:15 into rows 1, 3
+  best_step<0x143, 0xc>(v, ix);   // row_bcast:31 into rows 2, 3
+  v = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
+  ix = __builtin_amdgcn_readlane(ix, 63);
 }
 
 // K picks in order from the lane-held candidates c[0..n) plus extra LDS
@@ -496,6 +510,43 @@ __device__ __forceinline__ void wave_topk(const float (&cv)[N], const int (&ci)[
 }
 
 constexpr int kCap = 2048;     // survivor list capacity (candidates >= theta)
+constexpr int kMaxHd = 4096;   // hidden sizes the merge can stage in LDS for recomputes
+
+// Exact logits of vocabulary entries v0 .. v0+n-1 for the hidden row staged in
+// s_hid (fp32): one entry per thread, each streaming its W row with 16-byte
+// loads, so the loads of all entries are in flight together.
+template <typename DT>
+__device__ void recompute_logits(const LmParams& p, const float* s_hid, const int* s_split, int ns,
+                                 float* out_v, int* out_i) {
+  const DT* Wp = reinterpret_cast<const DT*>(p.W);
+  constexpr int EPL = 16 / (int)sizeof(DT);
+  for (int c = threadIdx.x; c < ns * kGroup; c += kMT) {
+    const int v = s_split[c / kGroup] * kGroup + (c % kGroup);
+    const bool ok = v < p.V;
+    const DT* wr = Wp + (size_t)(ok ? v : 0) * p.Hd;
+    float a0 = 0.f, a1 = 0.f;
+#pragma unroll 8
+    for (int k = 0; k < p.Hd; k += 2 * EPL) {
+      if constexpr (sizeof(DT) == 2) {
+        const bf16x8 w0 = ld16<bf16x8>(wr + k), w1 = ld16<bf16x8>(wr + k + EPL);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          a0 = fmaf(static_cast<float>(w0[e]), s_hid[k + e], a0);
+          a1 = fmaf(static_cast<float>(w1[e]), s_hid[k + EPL + e], a1);
+        }
+      } else {
+        const floatx4 w0 = ld16<floatx4>(wr + k), w1 = ld16<floatx4>(wr + k + EPL);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          a0 = fmaf(w0[e], s_hid[k + e], a0);
+          a1 = fmaf(w1[e], s_hid[k + EPL + e], a1);
+        }
+      }
+    }
+    out_v[c] = ok ? a0 + a1 : -INFINITY;
+    out_i[c] = ok ? v : 0x7fffffff;
+  }
+}
 
 template <typename DT>
 __global__ __launch_bounds__(kMT) void lmhead_merge_kernel(LmParams p) {
@@ -519,6 +570,9 @@ __global__ __launch_bounds__(kMT) void lmhead_merge_kernel(LmParams p) {
   __shared__ int s_li[kCap];
   __shared__ float s_cv[kSplitCand];    // recomputed logits of split groups
   __shared__ int s_ci[kSplitCand];
+  __shared__ float s_hid[kMaxHd];       // the row's hidden state, for recomputes
+  __shared__ float s_lv2[kCap];         // survivor list after a recompute
+  __shared__ int s_li2[kCap];
 
   // This thread's groups: tid, tid + kMT, ... (register resident).
   float cv[2 * kMaxGPT];
@@ -611,32 +665,30 @@ __global__ __launch_bounds__(kMT) void lmhead_merge_kernel(LmParams p) {
     __syncthreads();
     if (round == 1) break;
     // Groups picked twice whose third value reaches the K-th pick may hide
-    // further members: only those are recomputed.
-    if (tid == 0) {
-      int n = 0;
-      const float yk = s_top_v[K - 1];
-      for (int a2 = 0; a2 < K; ++a2)
-        for (int b2 = a2 + 1; b2 < K; ++b2)
-          if (s_top_i[a2] != 0x7fffffff && s_top_i[a2] / kGroup == s_top_i[b2] / kGroup) {
-            const int gsp = s_top_i[a2] / kGroup;
-            if (!(p.rec_v3[base + gsp] >= yk)) continue;
-            bool seen = false;
-            for (int t = 0; t < n; ++t) seen |= (s_split[t] == gsp);
-            if (!seen && n < kMaxSplit) s_split[n++] = gsp;
-          }
-      s_nsplit = n;
+    // further members: only those are recomputed.  Pick a checks its group
+    // when it is the group's first pick and a later pick shares it.
+    if (tid < K) {
+      const int ia = s_top_i[tid];
+      const int ga = ia / kGroup;
+      bool first = ia != 0x7fffffff, again = false;
+      for (int b2 = 0; b2 < K; ++b2) {
+        const bool same = b2 != tid && s_top_i[b2] != 0x7fffffff && s_top_i[b2] / kGroup == ga;
+        first &= !(same && b2 < tid);
+        again |= same && b2 > tid;
+      }
+      if (first && again && p.rec_v3[base + ga] >= s_top_v[K - 1]) {
+        const int slot = atomicAdd(&s_nsplit, 1);
+        if (slot < kMaxSplit) s_split[slot] = ga;
+      }
     }
     __syncthreads();
-    const int nsplit = s_nsplit;
+    const int nsplit = min(s_nsplit, kMaxSplit);
     if (nsplit == 0) break;
-    for (int c = wv; c < nsplit * kGroup; c += NW) {
-      const int v = s_split[c / kGroup] * kGroup + (c % kGroup);
-      const bool ok = v < p.V;
-      const float x = ok ? wave_dot<DT>(p, m, v) : -INFINITY;
-      if (lane == 0) {
-        s_cv[c] = x;
-        s_ci[c] = ok ? v : 0x7fffffff;
-      }
+    {
+      const DT* hr = reinterpret_cast<const DT*>(p.hidden) + (size_t)m * p.Hd;
+      for (int k = tid; k < p.Hd; k += kMT) s_hid[k] = to_f32(hr[k]);
+      __syncthreads();
+      recompute_logits<DT>(p, s_hid, s_split, nsplit, s_cv, s_ci);
     }
     if (overflow) {
       // drop the split groups' records: their members now come from s_cv
@@ -652,19 +704,29 @@ __global__ __launch_bounds__(kMT) void lmhead_merge_kernel(LmParams p) {
       }
     }
     __syncthreads();
-    if (!overflow && tid == 0) {
+    if (!overflow) {
       // survivors of split groups are replaced by the recomputed values
-      int n = 0;
-      for (int c = 0; c < n_list; ++c) {
+      if (tid == 0) s_n = 0;
+      __syncthreads();
+      for (int c = tid; c < n_list; c += kMT) {
         bool sp = false;
         for (int t = 0; t < nsplit; ++t) sp |= (s_li[c] / kGroup == s_split[t]);
-        if (!sp) { s_lv[n] = s_lv[c]; s_li[n] = s_li[c]; ++n; }
+        if (!sp) {
+          const int slot = atomicAdd(&s_n, 1);
+          if (slot < kCap) { s_lv2[slot] = s_lv[c]; s_li2[slot] = s_li[c]; }
+        }
       }
-      for (int c = 0; c < nsplit * kGroup && n < kCap; ++c) { s_lv[n] = s_cv[c]; s_li[n] = s_ci[c]; ++n; }
-      s_n = n;
+      __syncthreads();
+      const int kept = min(s_n, kCap);
+      for (int c = tid; c < nsplit * kGroup && kept + c < kCap; c += kMT) {
+        s_lv2[kept + c] = s_cv[c];
+        s_li2[kept + c] = s_ci[c];
+      }
+      __syncthreads();
+      n_list = min(kept + nsplit * kGroup, kCap);
+      for (int c = tid; c < n_list; c += kMT) { s_lv[c] = s_lv2[c]; s_li[c] = s_li2[c]; }
     }
     __syncthreads();
-    n_list = s_n;
   }
 
   const int orow = p.out_rows ? p.out_rows[m] : m;
