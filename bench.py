@@ -1,6 +1,7 @@
 """Benchmark of one verify step (attention -> LM head -> accept scan) on MI355X.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 3] [--no-cpu]
+    python bench.py --copy-calibration MIB   # reference copy for HBM counters
 
 A step is one pass of the whole verifier-side hot path over one synthetic
 batch: verify_attn_paged (window append, split-KV paged attention, split
@@ -221,7 +222,19 @@ def main():
     ap.add_argument("--config", type=int, default=3)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only copy MIB MiB device-to-device 5 times (a kernel of known "
+                         "traffic for scaling the HBM byte counters), then exit")
     args = ap.parse_args()
+    if args.copy_calibration:
+        n = args.copy_calibration << 20
+        src = torch.ones(n, dtype=torch.uint8, device="cuda:0")
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes": n, "copies": 5}), flush=True)
+        return
     if args.gpus != 1:
         print("bench.py measures one GPU only: the verify path shards by request with no "
               "exchange, so N GPUs run N independent copies (see the design notes).",
@@ -272,7 +285,7 @@ def main():
     work = work_per_launch(batch)
     dom = "lmhead_gemm" if kt["lmhead_gemm"] >= kt["attention"] else "attention"
     t_dom = kt[dom] * 1e-3 / n_models
-    workload = f"config{args.config}"
+    workload = cfg.name
     if dom == "attention" or batch.T < 320:
         bytes_, flops_ = work[dom]
         achieved = bytes_ / n_models / t_dom / 1e9

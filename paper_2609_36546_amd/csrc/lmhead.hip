@@ -106,46 +106,49 @@ __device__ __forceinline__ void top3_push(float x, int ix, float& v1, int& i1, f
 
 typedef __attribute__((__vector_size__(16))) int i32x4;
 
+// Offset of register e of 32x32 block vb from the lane's first vocabulary
+// entry: block vb covers 32 entries, register e entry 8 (e / 4) + e % 4 (plus
+// 4 for the upper half-wave).  Local index j = 16 vb + e.
+__device__ __forceinline__ constexpr int epi_off(int j) {
+  return 32 * (j >> 4) + 8 * ((j >> 2) & 3) + (j & 3);
+}
+
 // Epilogue: per hidden row (lane column) and this wave's 128 vocabulary
-// entries, the group record (v1/i1, v2/i2, v3, s, e).  Register e of block vb
-// holds vocabulary entry vbase + 32 vb + 8 (e / 4) + 4 h + e % 4.
-template <int RB>
+// entries, the group record (v1/i1, v2/i2, v3, s, e).  A lane holds 64 of the
+// group's entries for its row, in increasing vocabulary order along j, so a
+// later equal value never displaces an earlier one and the running top-3 needs
+// no index comparisons: two medians of three and a max keep the values, two
+// compares and three selects keep the local indices.  The partner lane (l ^ 32)
+// holds the other 64.  FULL: every entry of the tile is < V (no masking).
+template <int RB, bool FULL>
 __device__ __forceinline__ void lm_epilogue(const LmParams& p, floatx16 (&acc)[4][RB], int vt, int m0,
                                             int wv, int wr) {
   const int lane = lane_id();
   const int h = lane >> 5;
-  const int vbase = vt * kVT + kGroup * wv;
+  const int vlane = vt * kVT + kGroup * wv + 4 * h;   // entry of local index 0
   const int g = vt * (kVT / kGroup) + wv;
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
     const int m = m0 + 32 * RB * wr + 32 * rb + (lane & 31);
-    float mx = -INFINITY;
+    if (!FULL) {
 #pragma unroll
-    for (int vb = 0; vb < 4; ++vb)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int v = vbase + 32 * vb + 8 * (e >> 2) + 4 * h + (e & 3);
-        if (v >= p.V) acc[vb][rb][e] = -INFINITY;
-        mx = fmaxf(mx, acc[vb][rb][e]);
-      }
-    mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
-    const float mub = ((mx == -INFINITY) ? 0.f : mx) * kLog2e;
-    float s = 0.f, ee = 0.f;
+      for (int j = 0; j < 64; ++j)
+        acc[j >> 4][rb][j & 15] = (vlane + epi_off(j) < p.V) ? acc[j >> 4][rb][j & 15] : -INFINITY;
+    }
     float v1 = -INFINITY, v2 = -INFINITY, v3 = -INFINITY;
-    int i1 = 0x7fffffff, i2 = 0x7fffffff;
+    int j1 = 0, j2 = 0;
 #pragma unroll
-    for (int vb = 0; vb < 4; ++vb)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const float x = acc[vb][rb][e];
-        const int v = vbase + 32 * vb + 8 * (e >> 2) + 4 * h + (e & 3);
-        const float pe = fast_exp2(fmaf(x, kLog2e, -mub));
-        s += pe;
-        ee += (v < p.V) ? pe * x : 0.f;
-        top3_push(x, v, v1, i1, v2, i2, v3);
-      }
-    s += __shfl_xor(s, 32, kWave);
-    ee += __shfl_xor(ee, 32, kWave);
+    for (int j = 0; j < 64; ++j) {
+      const float x = acc[j >> 4][rb][j & 15];
+      const bool c1 = x > v1, c2 = x > v2;
+      v3 = __builtin_amdgcn_fmed3f(v2, v3, x);
+      v2 = __builtin_amdgcn_fmed3f(v1, v2, x);
+      v1 = fmaxf(v1, x);
+      j2 = c1 ? j1 : (c2 ? j : j2);
+      j1 = c1 ? j : j1;
+    }
+    int i1 = (v1 == -INFINITY) ? 0x7fffffff : vlane + epi_off(j1);
+    int i2 = (v2 == -INFINITY) ? 0x7fffffff : vlane + epi_off(j2);
     {
       // merge the partner lane's (top-2, third value): the third of the union
       // is max(third after pushing its top-2, its third)
@@ -156,17 +159,41 @@ __device__ __forceinline__ void lm_epilogue(const LmParams& p, floatx16 (&acc)[4
       top3_push(ov2, oi2, v1, i1, v2, i2, v3);
       v3 = fmaxf(v3, ov3);
     }
+    // v1 is now the group maximum; exp-sum and entropy numerator against it
+    const float mub = ((v1 == -INFINITY) ? 0.f : v1) * kLog2e;
+    float s = 0.f, ee = 0.f;
+#pragma unroll
+    for (int j = 0; j < 64; ++j) {
+      const float x = acc[j >> 4][rb][j & 15];
+      const float pe = fast_exp2(fmaf(x, kLog2e, -mub));
+      s += pe;
+      if (FULL)
+        ee = fmaf(pe, x, ee);
+      else
+        ee += (x != -INFINITY) ? pe * x : 0.f;
+    }
+    s += __shfl_xor(s, 32, kWave);
+    ee += __shfl_xor(ee, 32, kWave);
     if (h == 0 && m < p.M && g < p.n_groups) {
       const size_t r = (size_t)m * p.n_groups + g;
       p.rec_v1[r] = v1;
       p.rec_v2[r] = v2;
-      p.rec_s[r] = (mx == -INFINITY) ? 0.f : s;
-      p.rec_e[r] = (mx == -INFINITY) ? 0.f : ee;
+      p.rec_s[r] = (v1 == -INFINITY) ? 0.f : s;
+      p.rec_e[r] = (v1 == -INFINITY) ? 0.f : ee;
       p.rec_idx[r] = i1;
       p.rec_i2[r] = i2;
       p.rec_v3[r] = v3;
     }
   }
+}
+
+template <int RB>
+__device__ __forceinline__ void lm_epilogue_any(const LmParams& p, floatx16 (&acc)[4][RB], int vt,
+                                                int m0, int wv, int wr) {
+  if ((vt + 1) * kVT <= p.V)
+    lm_epilogue<RB, true>(p, acc, vt, m0, wv, wr);
+  else
+    lm_epilogue<RB, false>(p, acc, vt, m0, wv, wr);
 }
 
 template <typename DT, int RB>
@@ -263,7 +290,7 @@ __global__ __launch_bounds__(256) void lmhead_gemm_kernel(LmParams p) {
     if (more) store_stage((st + 1) & 1);
   }
 
-  lm_epilogue<RB>(p, acc, vt, m0, wv, wr);
+  lm_epilogue_any<RB>(p, acc, vt, m0, wv, wr);
 }
 
 // ---------------------------------------------------------------------------
@@ -295,8 +322,9 @@ __device__ __forceinline__ void dma16(const void* src, char* lds) {
                : "memory", "m0");
 }
 
-template <int RB>
+template <int RB, int NBUF>
 __global__ __launch_bounds__(256) void lmhead_gemm_dlds_kernel(LmParams p) {
+  static_assert(NBUF >= 3 && NBUF <= 5, "ring depth");
   const int id = blockIdx.x;
   const int xcd = id & 7, local = id >> 3;
   const int vt = (local / p.n_rt) * 8 + xcd;
@@ -306,7 +334,9 @@ __global__ __launch_bounds__(256) void lmhead_gemm_dlds_kernel(LmParams p) {
   constexpr int WB = kVT * 64;                  // W tile bytes per stage
   constexpr int SB = WB + NM * 64;              // stage bytes
   constexpr int NBLK = (kVT + NM) / 16;         // 1 KB load blocks per stage
-  constexpr int PER_WAVE = NBLK / 4;            // load instructions per wave and stage
+  constexpr int PW = NBLK / 4;                  // load instructions per wave and stage
+  constexpr int KS = kDStage / 16;              // MFMA k-steps per stage
+  static_assert(KS == 2 && (NBUF - 2) * PW <= 63, "pipeline shape");
   const int m0 = rt * NM;
   const int v0 = vt * kVT;
   const int tid = threadIdx.x;
@@ -317,17 +347,14 @@ __global__ __launch_bounds__(256) void lmhead_gemm_dlds_kernel(LmParams p) {
   const int rr = lane & 31;
   const int nst = p.Hd / kDStage;
 
-  __shared__ __attribute__((aligned(1024))) char s_b0[SB];
-  __shared__ __attribute__((aligned(1024))) char s_b1[SB];
-  __shared__ __attribute__((aligned(1024))) char s_b2[SB];
-  __shared__ __attribute__((aligned(1024))) char s_b3[SB];
+  __shared__ __attribute__((aligned(1024))) char s_ring[NBUF * SB];
 
   const bf16* Wp = reinterpret_cast<const bf16*>(p.W);
   const bf16* Hp = reinterpret_cast<const bf16*>(p.hidden);
   // This lane's source row and chunk for each of its load blocks.
-  const bf16* src[PER_WAVE];
+  const bf16* src[PW];
 #pragma unroll
-  for (int j = 0; j < PER_WAVE; ++j) {
+  for (int j = 0; j < PW; ++j) {
     const int u = w + 4 * j;
     const int r = (u < kVT / 16 ? 16 * u : 16 * (u - kVT / 16)) + (lane >> 2);
     const int c = (lane & 3) ^ ((r >> 2) & 3);
@@ -339,13 +366,30 @@ __global__ __launch_bounds__(256) void lmhead_gemm_dlds_kernel(LmParams p) {
       src[j] = Hp + (size_t)m * p.Hd + 8 * c;
     }
   }
-  auto issue = [&](char* buf, int st) {
-    const int k0 = min(st, nst - 1) * kDStage;  // past the end: reload the last stage (unused)
+  // Stage st goes to buffer st % NBUF.  Stages past the end reload the last
+  // one into a free buffer, so that every wave has the same number of loads
+  // in flight at every boundary.  dma(st, j0, j1): this wave's load blocks
+  // [j0, j1) of stage st.
+  auto dma = [&](int st, int j0, int j1) {
+    char* buf = s_ring + (st % NBUF) * SB;
+    const int k0 = min(st, nst - 1) * kDStage;
 #pragma unroll
-    for (int j = 0; j < PER_WAVE; ++j) {
-      const int u = w + 4 * j;
-      dma16(src[j] + k0, buf + 1024 * u);
-    }
+    for (int j = j0; j < j1; ++j) dma16(src[j] + k0, buf + 1024 * (w + 4 * j));
+  };
+  // Operand offsets of this lane within a stage.  Chunk 2 ks + h of a row sits
+  // at 16 ((2 ks + h) ^ q), q = row bits 2-3, which is the ks = 0 offset xor
+  // 32 ks; 32-row steps keep q.
+  const int a_off = dl_off(128 * wv + rr, h);
+  const int b_off = WB + dl_off(32 * RB * wr + rr, h);
+  bf16x8 fa[2][4], fb[2][RB];
+  auto load = [&](int set, const char* buf, int ks) {
+    const int x = 32 * ks;
+#pragma unroll
+    for (int vb = 0; vb < 4; ++vb)
+      fa[set][vb] = *reinterpret_cast<const bf16x8*>(buf + ((a_off + 2048 * vb) ^ x));
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb)
+      fb[set][rb] = *reinterpret_cast<const bf16x8*>(buf + ((b_off + 2048 * rb) ^ x));
   };
 
   floatx16 acc[4][RB];
@@ -355,47 +399,78 @@ __global__ __launch_bounds__(256) void lmhead_gemm_dlds_kernel(LmParams p) {
     for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[vb][rb][e] = 0.f;
+  // MFMAs of operand set `set` over vocabulary block vb.
+  auto mma = [&](int set, int vb) {
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb)
+      acc[vb][rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[set][vb], fb[set][rb], acc[vb][rb], 0, 0, 0);
+  };
+#define IPDV_SB __builtin_amdgcn_sched_barrier(0)
 
-  auto step = [&](const char* cur, char* nxt, int st) {
-    // Own loads of stage st are done once at most two later stages' are
-    // pending; after the barrier every wave's are, and every wave has finished
-    // reading the buffer the next issue overwrites.  A bare s_barrier: the
-    // fence of __syncthreads would wait for the stages still in flight.
-    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * PER_WAVE) : "memory");
+  // Boundary into stage b: each wave waits for its own loads of b (NBUF - 3
+  // later stages may stay in flight), the barrier makes every wave's visible,
+  // and buffer (b - 2) % NBUF starts refilling with stage b + NBUF - 2.  Every
+  // wave has consumed stage b - 2: it waited for that stage's last operands
+  // before its final MFMAs, which precede this barrier.  Stage b - 1 may still
+  // be read (its last k-step's operands can be in flight), so it is not
+  // refilled yet.  A bare s_barrier: the fence of __syncthreads would wait for
+  // every stage in flight.  The refill's loads are spread over the MFMAs up to
+  // the next boundary (a burst of them stalls the issuing wave, and with one
+  // wave per SIMD that idles the matrix pipe); the operand reads of the next
+  // k-step sit between MFMAs too.  sched_barrier pins the order.
+  constexpr int Q1 = PW / 4, Q2 = PW / 2, Q3 = 3 * PW / 4;   // refill split points
+#pragma unroll
+  for (int s0 = 0; s0 < NBUF - 1; ++s0) dma(s0, 0, PW);
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"((NBUF - 2) * PW) : "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+  load(0, s_ring, 0);
+  for (int st = 0; st + 1 < nst; ++st) {
+    const char* cur = s_ring + (st % NBUF) * SB;
+    const int pend = st + NBUF - 2;            // refill started at the last boundary
+    mma(0, 0);
+    IPDV_SB;
+    if (st > 0) dma(pend, Q1, Q2);
+    load(1, cur, 1);
+    IPDV_SB;
+    mma(0, 1);
+    IPDV_SB;
+    if (st > 0) dma(pend, Q2, Q3);
+    IPDV_SB;
+    mma(0, 2);
+    IPDV_SB;
+    if (st > 0) dma(pend, Q3, PW);
+    IPDV_SB;
+    mma(0, 3);
+    mma(1, 0);
+    mma(1, 1);
+    IPDV_SB;
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"((NBUF - 3) * PW) : "memory");
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
-    issue(nxt, st + 3);
-#pragma unroll
-    for (int ks = 0; ks < kDStage / 16; ++ks) {
-      const int c = 2 * ks + h;
-      bf16x8 a[4], b[RB];
-#pragma unroll
-      for (int vb = 0; vb < 4; ++vb)
-        a[vb] = *reinterpret_cast<const bf16x8*>(cur + dl_off(128 * wv + 32 * vb + rr, c));
-#pragma unroll
-      for (int rb = 0; rb < RB; ++rb)
-        b[rb] = *reinterpret_cast<const bf16x8*>(cur + WB + dl_off(32 * RB * wr + 32 * rb + rr, c));
-#pragma unroll
-      for (int vb = 0; vb < 4; ++vb)
-#pragma unroll
-        for (int rb = 0; rb < RB; ++rb)
-          acc[vb][rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[vb], b[rb], acc[vb][rb], 0, 0, 0);
-    }
-  };
-
-  issue(s_b0, 0);
-  issue(s_b1, 1);
-  issue(s_b2, 2);
-  for (int st = 0; st < nst; st += 4) {     // nst % 4 == 0 (checked by the planner)
-    step(s_b0, s_b3, st);
-    step(s_b1, s_b0, st + 1);
-    step(s_b2, s_b1, st + 2);
-    step(s_b3, s_b2, st + 3);
+    dma(pend + 1, 0, Q1);
+    load(0, s_ring + ((st + 1) % NBUF) * SB, 0);
+    IPDV_SB;
+    mma(1, 2);
+    mma(1, 3);
+    IPDV_SB;
   }
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // the trailing reloads
-  __syncthreads();
+  {
+    const char* cur = s_ring + ((nst - 1) % NBUF) * SB;
+    mma(0, 0);
+    load(1, cur, 1);
+    mma(0, 1);
+    mma(0, 2);
+    mma(0, 3);
+    mma(1, 0);
+    mma(1, 1);
+    mma(1, 2);
+    mma(1, 3);
+  }
+#undef IPDV_SB
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // reloads past the end still in flight
 
-  lm_epilogue<RB>(p, acc, vt, m0, wv, wr);
+  lm_epilogue_any<RB>(p, acc, vt, m0, wv, wr);
 }
 
 // ---------------------------------------------------------------------------
@@ -752,10 +827,20 @@ __global__ __launch_bounds__(kMT) void lmhead_merge_kernel(LmParams p) {
 // hidden size is a multiple of four stages, fp32 the register-staged one.
 template <int RB>
 void launch_gemm(const LmParams& p, dim3 grid, hipStream_t st, bf16) {
-  if (p.Hd % (4 * kDStage) == 0)
-    hipLaunchKernelGGL((lmhead_gemm_dlds_kernel<RB>), grid, dim3(256), 0, st, p);
-  else
+  // Ring depth (IPDV_LM_NBUF overrides it for tuning sweeps).
+  static const int nbuf_env = [] {
+    const char* e = getenv("IPDV_LM_NBUF");
+    return e ? atoi(e) : 0;
+  }();
+  const int nbuf = (nbuf_env >= 3 && nbuf_env <= 5) ? nbuf_env : 4;
+  if (p.Hd % kDStage != 0)
     hipLaunchKernelGGL((lmhead_gemm_kernel<bf16, RB>), grid, dim3(256), 0, st, p);
+  else if (nbuf == 3)
+    hipLaunchKernelGGL((lmhead_gemm_dlds_kernel<RB, 3>), grid, dim3(256), 0, st, p);
+  else if (nbuf == 5 && RB <= 4)
+    hipLaunchKernelGGL((lmhead_gemm_dlds_kernel<RB, 5>), grid, dim3(256), 0, st, p);
+  else
+    hipLaunchKernelGGL((lmhead_gemm_dlds_kernel<RB, 4>), grid, dim3(256), 0, st, p);
 }
 
 template <int RB>
