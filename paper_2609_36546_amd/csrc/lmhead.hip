@@ -45,13 +45,18 @@ struct LmParams {
   const int32_t* out_rows;
   int M, Hd, V, K;
   int n_groups, n_rt, n_vt;
-  float* rec_v1;      // [M][n_groups]
+  // Group records, [M][n_groups] each: the three largest logits of the group
+  // with their indices, the fourth largest value, sum exp(l - v1) and
+  // sum exp(l - v1) * l.
+  float* rec_v1;
   float* rec_v2;
+  float* rec_v3;
+  float* rec_v4;
   float* rec_s;
   float* rec_e;
-  int32_t* rec_idx;   // index of v1
-  int32_t* rec_i2;    // index of v2
-  float* rec_v3;      // third largest logit of the group (value only)
+  int32_t* rec_i1;
+  int32_t* rec_i2;
+  int32_t* rec_i3;
   float* lse;
   float* logp_prop;
   int32_t* argmax;
@@ -85,23 +90,24 @@ template <> struct Mm<float> {
   __device__ static int koff(int ks, int h) { return 16 * h + ks; }
 };
 
-// Top-2 (value desc, index asc) insertion of (x, ix).
-__device__ __forceinline__ void top2_push(float x, int ix, float& v1, int& i1, float& v2, int& i2) {
+// Top-3 (value desc, index asc) insertion of (x, ix), with the fourth value:
+// (v1, i1) >= (v2, i2) >= (v3, i3) >= v4.
+__device__ __forceinline__ void top3_push(float x, int ix, float& v1, int& i1, float& v2, int& i2,
+                                          float& v3, int& i3, float& v4) {
   const bool c1 = x > v1 || (x == v1 && ix < i1);
   const bool c2 = x > v2 || (x == v2 && ix < i2);
+  const bool c3 = x > v3 || (x == v3 && ix < i3);
+  v4 = __builtin_amdgcn_fmed3f(v3, v4, x);
+  const float nv3 = c2 ? v2 : (c3 ? x : v3);
+  const int ni3 = c2 ? i2 : (c3 ? ix : i3);
   const float nv2 = c1 ? v1 : (c2 ? x : v2);
   const int ni2 = c1 ? i1 : (c2 ? ix : i2);
   v1 = c1 ? x : v1;
   i1 = c1 ? ix : i1;
   v2 = nv2;
   i2 = ni2;
-}
-
-// Top-2 with indices plus the third value: (v1, i1) >= (v2, i2) >= v3.
-__device__ __forceinline__ void top3_push(float x, int ix, float& v1, int& i1, float& v2, int& i2,
-                                          float& v3) {
-  v3 = fmaxf(v3, fminf(v2, x));
-  top2_push(x, ix, v1, i1, v2, i2);
+  v3 = nv3;
+  i3 = ni3;
 }
 
 typedef __attribute__((__vector_size__(16))) int i32x4;
@@ -114,12 +120,13 @@ __device__ __forceinline__ constexpr int epi_off(int j) {
 }
 
 // Epilogue: per hidden row (lane column) and this wave's 128 vocabulary
-// entries, the group record (v1/i1, v2/i2, v3, s, e).  A lane holds 64 of the
-// group's entries for its row, in increasing vocabulary order along j, so a
-// later equal value never displaces an earlier one and the running top-3 needs
-// no index comparisons: two medians of three and a max keep the values, two
-// compares and three selects keep the local indices.  The partner lane (l ^ 32)
-// holds the other 64.  FULL: every entry of the tile is < V (no masking).
+// entries, the group record (top-3 with indices, fourth value, s, e).  A lane
+// holds 64 of the group's entries for its row, in increasing vocabulary order
+// along j, so a later equal value never displaces an earlier one and the
+// running top-4 needs no index comparisons: three medians of three and a
+// select keep the values, three compares and five selects the local indices.
+// The partner lane (l ^ 32) holds the other 64.  FULL: every entry of the tile
+// is < V (no masking).
 template <int RB, bool FULL>
 __device__ __forceinline__ void lm_epilogue(const LmParams& p, floatx16 (&acc)[4][RB], int vt, int m0,
                                             int wv, int wr) {
@@ -135,29 +142,34 @@ __device__ __forceinline__ void lm_epilogue(const LmParams& p, floatx16 (&acc)[4
       for (int j = 0; j < 64; ++j)
         acc[j >> 4][rb][j & 15] = (vlane + epi_off(j) < p.V) ? acc[j >> 4][rb][j & 15] : -INFINITY;
     }
-    float v1 = -INFINITY, v2 = -INFINITY, v3 = -INFINITY;
-    int j1 = 0, j2 = 0;
+    float v1 = -INFINITY, v2 = -INFINITY, v3 = -INFINITY, v4 = -INFINITY;
+    int j1 = 0, j2 = 0, j3 = 0;
 #pragma unroll
     for (int j = 0; j < 64; ++j) {
       const float x = acc[j >> 4][rb][j & 15];
-      const bool c1 = x > v1, c2 = x > v2;
+      const bool c1 = x > v1, c2 = x > v2, c3 = x > v3;
+      v4 = __builtin_amdgcn_fmed3f(v3, v4, x);
       v3 = __builtin_amdgcn_fmed3f(v2, v3, x);
       v2 = __builtin_amdgcn_fmed3f(v1, v2, x);
-      v1 = fmaxf(v1, x);
+      v1 = c1 ? x : v1;   // a select on c1: fmaxf would add a NaN-quieting max per entry
+      j3 = c2 ? j2 : (c3 ? j : j3);
       j2 = c1 ? j1 : (c2 ? j : j2);
       j1 = c1 ? j : j1;
     }
     int i1 = (v1 == -INFINITY) ? 0x7fffffff : vlane + epi_off(j1);
     int i2 = (v2 == -INFINITY) ? 0x7fffffff : vlane + epi_off(j2);
+    int i3 = (v3 == -INFINITY) ? 0x7fffffff : vlane + epi_off(j3);
     {
-      // merge the partner lane's (top-2, third value): the third of the union
-      // is max(third after pushing its top-2, its third)
+      // merge the partner lane's top-3: the fourth of the union is the max of
+      // the fourth after pushing its top-3 and its own fourth
       const float ov1 = __shfl_xor(v1, 32, kWave), ov2 = __shfl_xor(v2, 32, kWave);
-      const float ov3 = __shfl_xor(v3, 32, kWave);
+      const float ov3 = __shfl_xor(v3, 32, kWave), ov4 = __shfl_xor(v4, 32, kWave);
       const int oi1 = __shfl_xor(i1, 32, kWave), oi2 = __shfl_xor(i2, 32, kWave);
-      top3_push(ov1, oi1, v1, i1, v2, i2, v3);
-      top3_push(ov2, oi2, v1, i1, v2, i2, v3);
-      v3 = fmaxf(v3, ov3);
+      const int oi3 = __shfl_xor(i3, 32, kWave);
+      top3_push(ov1, oi1, v1, i1, v2, i2, v3, i3, v4);
+      top3_push(ov2, oi2, v1, i1, v2, i2, v3, i3, v4);
+      top3_push(ov3, oi3, v1, i1, v2, i2, v3, i3, v4);
+      v4 = fmaxf(v4, ov4);
     }
     // v1 is now the group maximum; exp-sum and entropy numerator against it
     const float mub = ((v1 == -INFINITY) ? 0.f : v1) * kLog2e;
@@ -178,11 +190,13 @@ __device__ __forceinline__ void lm_epilogue(const LmParams& p, floatx16 (&acc)[4
       const size_t r = (size_t)m * p.n_groups + g;
       p.rec_v1[r] = v1;
       p.rec_v2[r] = v2;
+      p.rec_v3[r] = v3;
+      p.rec_v4[r] = v4;
       p.rec_s[r] = (v1 == -INFINITY) ? 0.f : s;
       p.rec_e[r] = (v1 == -INFINITY) ? 0.f : ee;
-      p.rec_idx[r] = i1;
+      p.rec_i1[r] = i1;
       p.rec_i2[r] = i2;
-      p.rec_v3[r] = v3;
+      p.rec_i3[r] = i3;
     }
   }
 }
@@ -196,16 +210,28 @@ __device__ __forceinline__ void lm_epilogue_any(const LmParams& p, floatx16 (&ac
     lm_epilogue<RB, false>(p, acc, vt, m0, wv, wr);
 }
 
-template <typename DT, int RB>
-__global__ __launch_bounds__(256) void lmhead_gemm_kernel(LmParams p) {
-  // XCD-aware order: the row tiles of one vocabulary tile are consecutive in
-  // the dispatch sequence of one XCD (workgroup id % 8), so the W tile they
-  // share is fetched from HBM once into that XCD's L2.
+// Tile of this workgroup.  The hardware deals workgroup ids to the 8 XCDs
+// round-robin (id % 8).  XCD x takes a contiguous range of vocabulary tiles,
+// and the row tiles of one vocabulary tile run back to back on it: the W tile
+// they share is fetched from HBM once into that XCD's L2, and every 64-byte
+// line of the group records (16 groups = 8 vocabulary tiles of one row) is
+// completed inside one L2 before it is written back.  The grid holds
+// ceil(n_vt / 8) * 8 * n_rt workgroups; the surplus returns at once.
+__device__ __forceinline__ bool gemm_tile(const LmParams& p, int& vt, int& rt) {
   const int id = blockIdx.x;
   const int xcd = id & 7, local = id >> 3;
-  const int vt = (local / p.n_rt) * 8 + xcd;
-  const int rt = local % p.n_rt;
-  if (vt >= p.n_vt) return;
+  const int per = p.n_vt / 8, extra = p.n_vt % 8;
+  const int j = local / p.n_rt;
+  if (j >= per + (xcd < extra ? 1 : 0)) return false;
+  vt = xcd * per + min(xcd, extra) + j;
+  rt = local % p.n_rt;
+  return true;
+}
+
+template <typename DT, int RB>
+__global__ __launch_bounds__(256) void lmhead_gemm_kernel(LmParams p) {
+  int vt, rt;
+  if (!gemm_tile(p, vt, rt)) return;
   typedef Mm<DT> MM;
   constexpr int NM = 64 * RB;                       // hidden rows per workgroup
   constexpr int LDW = MM::STAGE + 16 / (int)sizeof(DT);   // LDS row pitch (elements)
@@ -325,11 +351,8 @@ __device__ __forceinline__ void dma16(const void* src, char* lds) {
 template <int RB, int NBUF>
 __global__ __launch_bounds__(256) void lmhead_gemm_dlds_kernel(LmParams p) {
   static_assert(NBUF >= 3 && NBUF <= 5, "ring depth");
-  const int id = blockIdx.x;
-  const int xcd = id & 7, local = id >> 3;
-  const int vt = (local / p.n_rt) * 8 + xcd;
-  const int rt = local % p.n_rt;
-  if (vt >= p.n_vt) return;
+  int vt, rt;
+  if (!gemm_tile(p, vt, rt)) return;
   constexpr int NM = 64 * RB;
   constexpr int WB = kVT * 64;                  // W tile bytes per stage
   constexpr int SB = WB + NM * 64;              // stage bytes
@@ -495,6 +518,22 @@ __device__ float block_sum(float x, float* s) {
   return t;
 }
 
+// Block sums of three values at once (s holds 3 * waves floats).
+__device__ void block_sum3(float& a, float& b, float& c, float* s) {
+  for (int o = 32; o > 0; o >>= 1) {
+    a += __shfl_xor(a, o, kWave);
+    b += __shfl_xor(b, o, kWave);
+    c += __shfl_xor(c, o, kWave);
+  }
+  constexpr int NW = kMT / kWave;
+  const int w = threadIdx.x >> 6;
+  __syncthreads();
+  if (lane_id() == 0) { s[w] = a; s[NW + w] = b; s[2 * NW + w] = c; }
+  __syncthreads();
+  a = b = c = 0.f;
+  for (int ww = 0; ww < NW; ++ww) { a += s[ww]; b += s[NW + ww]; c += s[2 * NW + ww]; }
+}
+
 __device__ float block_max(float x, float* s) {
   for (int o = 32; o > 0; o >>= 1) x = fmaxf(x, __shfl_xor(x, o, kWave));
   const int w = threadIdx.x >> 6;
@@ -506,36 +545,15 @@ __device__ float block_max(float x, float* s) {
   return t;
 }
 
-// Candidates per row: two per group plus every element of the groups whose
-// second-best made it into the list.  Such a group contributes two entries
-// to a K-entry list, so at most K/2 groups are ever recomputed.
-constexpr int kMaxSplit = IPDV_MAX_K_DEV / 2;
+// Candidates per row: three per group plus every element of the groups whose
+// third-best made it into the list.  Such a group contributes three entries
+// to a K-entry list, so at most K/3 groups are ever recomputed.
+constexpr int kMaxSplit = IPDV_MAX_K_DEV / 3;
 constexpr int kSplitCand = kMaxSplit * kGroup;
 
-// One wave computes the exact logit of vocabulary entry v for row m.
-template <typename DT>
-__device__ float wave_dot(const LmParams& p, int m, int v) {
-  const DT* hr = reinterpret_cast<const DT*>(p.hidden) + (size_t)m * p.Hd;
-  const DT* wr = reinterpret_cast<const DT*>(p.W) + (size_t)v * p.Hd;
-  constexpr int EPL = 16 / sizeof(DT);
-  float acc = 0.f;
-  for (int k = EPL * lane_id(); k < p.Hd; k += EPL * kWave) {
-    if constexpr (sizeof(DT) == 2) {
-      bf16x8 a = ld16<bf16x8>(hr + k), b = ld16<bf16x8>(wr + k);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) acc = fmaf(static_cast<float>(a[e]), static_cast<float>(b[e]), acc);
-    } else {
-      floatx4 a = ld16<floatx4>(hr + k), b = ld16<floatx4>(wr + k);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) acc = fmaf(a[e], b[e], acc);
-    }
-  }
-  for (int o = 32; o > 0; o >>= 1) acc += __shfl_xor(acc, o, kWave);
-  return acc;
-}
-
 // Groups per merge thread held in registers: V <= kMT * kMaxGPT * kGroup.
-constexpr int kMaxGPT = 16;
+constexpr int kMaxGPT = 8;
+constexpr int kCPG = 3;        // candidates per group (its recorded top-3)
 
 // One reduction step: combine with the (value, index) DPP moves in from
 // another lane; lanes without a source keep theirs.
@@ -587,39 +605,69 @@ __device__ __forceinline__ void wave_topk(const float (&cv)[N], const int (&ci)[
 constexpr int kCap = 2048;     // survivor list capacity (candidates >= theta)
 constexpr int kMaxHd = 4096;   // hidden sizes the merge can stage in LDS for recomputes
 
-// Exact logits of vocabulary entries v0 .. v0+n-1 for the hidden row staged in
-// s_hid (fp32): one entry per thread, each streaming its W row with 16-byte
-// loads, so the loads of all entries are in flight together.
+template <typename DT> struct Frag16;
+template <> struct Frag16<bf16> { typedef bf16x8 type; };
+template <> struct Frag16<float> { typedef floatx4 type; };
+
+// Exact logits of the split groups' entries for the hidden row staged in
+// s_hid (fp32).  A wave takes 4 entries at a time and lane l covers channels
+// EPL l + 64 EPL i of each, so one load instruction reads 64 consecutive
+// 16-byte chunks of a W row and the loads of all 4 entries (4 chunks each)
+// are in flight together; a shuffle reduction finishes each dot product.
 template <typename DT>
 __device__ void recompute_logits(const LmParams& p, const float* s_hid, const int* s_split, int ns,
                                  float* out_v, int* out_i) {
+  typedef typename Frag16<DT>::type frag;
   const DT* Wp = reinterpret_cast<const DT*>(p.W);
   constexpr int EPL = 16 / (int)sizeof(DT);
-  for (int c = threadIdx.x; c < ns * kGroup; c += kMT) {
-    const int v = s_split[c / kGroup] * kGroup + (c % kGroup);
-    const bool ok = v < p.V;
-    const DT* wr = Wp + (size_t)(ok ? v : 0) * p.Hd;
-    float a0 = 0.f, a1 = 0.f;
-#pragma unroll 8
-    for (int k = 0; k < p.Hd; k += 2 * EPL) {
-      if constexpr (sizeof(DT) == 2) {
-        const bf16x8 w0 = ld16<bf16x8>(wr + k), w1 = ld16<bf16x8>(wr + k + EPL);
+  constexpr int NB = 4;                       // entries per batch
+  constexpr int NP = 4;                       // chunks per lane and entry in flight
+  constexpr int NW = kMT / kWave;
+  const int lane = lane_id(), wv = threadIdx.x / kWave;
+  const int n = ns * kGroup;
+  for (int e0 = wv * NB; e0 < n; e0 += NW * NB) {
+    float acc[NB];
+    int vv[NB];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          a0 = fmaf(static_cast<float>(w0[e]), s_hid[k + e], a0);
-          a1 = fmaf(static_cast<float>(w1[e]), s_hid[k + EPL + e], a1);
+    for (int b = 0; b < NB; ++b) {
+      const int e = min(e0 + b, n - 1);
+      vv[b] = s_split[e / kGroup] * kGroup + e % kGroup;
+      acc[b] = 0.f;
+    }
+    for (int c0 = 0; c0 < p.Hd; c0 += NP * kWave * EPL) {
+      frag w[NB][NP];
+#pragma unroll
+      for (int b = 0; b < NB; ++b)
+#pragma unroll
+        for (int i = 0; i < NP; ++i) {
+          // out-of-range rows and channels load a valid chunk; it is masked below
+          const int c = min(c0 + EPL * (lane + kWave * i), p.Hd - EPL);
+          w[b][i] = ld16<frag>(Wp + (size_t)min(vv[b], p.V - 1) * p.Hd + c);
         }
-      } else {
-        const floatx4 w0 = ld16<floatx4>(wr + k), w1 = ld16<floatx4>(wr + k + EPL);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          a0 = fmaf(w0[e], s_hid[k + e], a0);
-          a1 = fmaf(w1[e], s_hid[k + EPL + e], a1);
+      for (int i = 0; i < NP; ++i) {
+        const int c = c0 + EPL * (lane + kWave * i);
+        if (c < p.Hd) {
+          float hv[EPL];
+#pragma unroll
+          for (int e = 0; e < EPL; ++e) hv[e] = s_hid[c + e];
+#pragma unroll
+          for (int b = 0; b < NB; ++b)
+#pragma unroll
+            for (int e = 0; e < EPL; ++e) acc[b] = fmaf(to_f32(w[b][i][e]), hv[e], acc[b]);
         }
       }
     }
-    out_v[c] = ok ? a0 + a1 : -INFINITY;
-    out_i[c] = ok ? v : 0x7fffffff;
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      float a = acc[b];
+      for (int o = 32; o > 0; o >>= 1) a += __shfl_xor(a, o, kWave);
+      if (lane == 0 && e0 + b < n) {
+        const bool ok = vv[b] < p.V;
+        out_v[e0 + b] = ok ? a : -INFINITY;
+        out_i[e0 + b] = ok ? vv[b] : 0x7fffffff;
+      }
+    }
   }
 }
 
@@ -633,7 +681,7 @@ __global__ __launch_bounds__(kMT) void lmhead_merge_kernel(LmParams p) {
   const int K = p.K;
   const size_t base = (size_t)m * G;
   constexpr int NW = kMT / kWave;
-  __shared__ float s_red[8];
+  __shared__ float s_red[3 * NW];
   __shared__ float s_theta[NW];
   __shared__ float s_wv[NW][IPDV_MAX_K_DEV];
   __shared__ int s_wi[NW][IPDV_MAX_K_DEV];
@@ -649,19 +697,43 @@ __global__ __launch_bounds__(kMT) void lmhead_merge_kernel(LmParams p) {
   __shared__ float s_lv2[kCap];         // survivor list after a recompute
   __shared__ int s_li2[kCap];
 
+  // The proposal's logit is one dot product; its loads go out first so that
+  // their latency overlaps the record loads and reductions.
+  typedef typename Frag16<DT>::type frag;
+  constexpr int EPL = 16 / (int)sizeof(DT);
+  constexpr int NPC = kMaxHd / (EPL * kMT);   // chunks of the dot product per thread
+  const int pv = p.prop_tok[m];
+  const bool pok = pv >= 0 && pv < p.V;
+  frag ph[NPC], pw[NPC];
+  {
+    const DT* hr = reinterpret_cast<const DT*>(p.hidden) + (size_t)m * p.Hd;
+    const DT* wr = reinterpret_cast<const DT*>(p.W) + (size_t)(pok ? pv : 0) * p.Hd;
+#pragma unroll
+    for (int u = 0; u < NPC; ++u) {
+      const int k = min(EPL * (tid + kMT * u), p.Hd - EPL);   // past Hd: masked below
+      ph[u] = ld16<frag>(hr + k);
+      pw[u] = ld16<frag>(wr + k);
+    }
+  }
+
   // This thread's groups: tid, tid + kMT, ... (register resident).
-  float cv[2 * kMaxGPT];
-  int ci[2 * kMaxGPT];
+  float cv[kCPG * kMaxGPT];
+  int ci[kCPG * kMaxGPT];
+  float rs[kMaxGPT], re[kMaxGPT];
   float mx = -INFINITY;
 #pragma unroll
   for (int u = 0; u < kMaxGPT; ++u) {
     const int gi = tid + kMT * u;
     const bool ok = gi < G;
-    cv[2 * u] = ok ? p.rec_v1[base + gi] : -INFINITY;
-    ci[2 * u] = ok ? p.rec_idx[base + gi] : 0x7fffffff;
-    cv[2 * u + 1] = ok ? p.rec_v2[base + gi] : -INFINITY;
-    ci[2 * u + 1] = ok ? p.rec_i2[base + gi] : 0x7fffffff;
-    mx = fmaxf(mx, cv[2 * u]);
+    cv[kCPG * u] = ok ? p.rec_v1[base + gi] : -INFINITY;
+    cv[kCPG * u + 1] = ok ? p.rec_v2[base + gi] : -INFINITY;
+    cv[kCPG * u + 2] = ok ? p.rec_v3[base + gi] : -INFINITY;
+    ci[kCPG * u] = ok ? p.rec_i1[base + gi] : 0x7fffffff;
+    ci[kCPG * u + 1] = ok ? p.rec_i2[base + gi] : 0x7fffffff;
+    ci[kCPG * u + 2] = ok ? p.rec_i3[base + gi] : 0x7fffffff;
+    rs[u] = ok ? p.rec_s[base + gi] : 0.f;
+    re[u] = ok ? p.rec_e[base + gi] : 0.f;
+    mx = fmaxf(mx, cv[kCPG * u]);
   }
   if (tid == 0) { s_n = 0; s_nsplit = 0; }
 
@@ -673,13 +745,19 @@ __global__ __launch_bounds__(kMT) void lmhead_merge_kernel(LmParams p) {
   for (int u = 0; u < kMaxGPT; ++u) {
     const int gi = tid + kMT * u;
     if (gi < G) {
-      const float wgt = fast_exp2((cv[2 * u] - Mu) * kLog2e);
-      S += p.rec_s[base + gi] * wgt;
-      E += p.rec_e[base + gi] * wgt;
+      const float wgt = fast_exp2((cv[kCPG * u] - Mu) * kLog2e);
+      S += rs[u] * wgt;
+      E += re[u] * wgt;
     }
   }
-  S = block_sum(S, s_red);
-  E = block_sum(E, s_red);
+  float PD = 0.f;
+#pragma unroll
+  for (int u = 0; u < NPC; ++u)
+    if (EPL * (tid + kMT * u) < p.Hd) {
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) PD = fmaf(to_f32(ph[u][e]), to_f32(pw[u][e]), PD);
+    }
+  block_sum3(S, E, PD, s_red);
   const float lse = Mu + fast_log2(S) * kLn2;
 
   // theta: a lower bound of the K-th largest logit.  The K largest lane
@@ -702,7 +780,7 @@ __global__ __launch_bounds__(kMT) void lmhead_merge_kernel(LmParams p) {
   for (int w2 = 1; w2 < NW; ++w2) theta = fmaxf(theta, s_theta[w2]);
   // survivors: candidates >= theta
 #pragma unroll
-  for (int c = 0; c < 2 * kMaxGPT; ++c) {
+  for (int c = 0; c < kCPG * kMaxGPT; ++c) {
     if (ci[c] != 0x7fffffff && cv[c] >= theta) {
       const int slot = atomicAdd(&s_n, 1);
       if (slot < kCap) { s_lv[slot] = cv[c]; s_li[slot] = ci[c]; }
@@ -712,8 +790,8 @@ __global__ __launch_bounds__(kMT) void lmhead_merge_kernel(LmParams p) {
   const bool overflow = s_n > kCap;     // many ties at theta: select from all records
   int n_list = min(s_n, kCap);
 
-  // Exact top-K.  Round 0 picks from the candidates; a group with two picks
-  // may hide a third member, so its logits are recomputed and round 1 picks
+  // Exact top-K.  Round 0 picks from the candidates; a group with three picks
+  // may hide a fourth member, so its logits are recomputed and round 1 picks
   // again (then every element left out ranks after the K-th pick).
   for (int round = 0; round < 2; ++round) {
     const int ns = s_nsplit;
@@ -739,19 +817,20 @@ __global__ __launch_bounds__(kMT) void lmhead_merge_kernel(LmParams p) {
     }
     __syncthreads();
     if (round == 1) break;
-    // Groups picked twice whose third value reaches the K-th pick may hide
-    // further members: only those are recomputed.  Pick a checks its group
-    // when it is the group's first pick and a later pick shares it.
+    // Groups picked three times whose fourth value reaches the K-th pick may
+    // hide further members: only those are recomputed.  Pick a checks its
+    // group when it is the group's first pick and two later picks share it.
     if (tid < K) {
       const int ia = s_top_i[tid];
       const int ga = ia / kGroup;
-      bool first = ia != 0x7fffffff, again = false;
+      bool first = ia != 0x7fffffff;
+      int later = 0;
       for (int b2 = 0; b2 < K; ++b2) {
         const bool same = b2 != tid && s_top_i[b2] != 0x7fffffff && s_top_i[b2] / kGroup == ga;
         first &= !(same && b2 < tid);
-        again |= same && b2 > tid;
+        later += (same && b2 > tid) ? 1 : 0;
       }
-      if (first && again && p.rec_v3[base + ga] >= s_top_v[K - 1]) {
+      if (first && later >= kCPG - 1 && p.rec_v4[base + ga] >= s_top_v[K - 1]) {
         const int slot = atomicAdd(&s_nsplit, 1);
         if (slot < kMaxSplit) s_split[slot] = ga;
       }
@@ -773,8 +852,11 @@ __global__ __launch_bounds__(kMT) void lmhead_merge_kernel(LmParams p) {
         bool sp = false;
         for (int t = 0; t < nsplit; ++t) sp |= (s_split[t] == gi);
         if (sp) {
-          cv[2 * u] = cv[2 * u + 1] = -INFINITY;
-          ci[2 * u] = ci[2 * u + 1] = 0x7fffffff;
+#pragma unroll
+          for (int c = 0; c < kCPG; ++c) {
+            cv[kCPG * u + c] = -INFINITY;
+            ci[kCPG * u + c] = 0x7fffffff;
+          }
         }
       }
     }
@@ -814,13 +896,7 @@ __global__ __launch_bounds__(kMT) void lmhead_merge_kernel(LmParams p) {
     p.argmax[orow] = s_top_i[0];
     if (p.entropy) p.entropy[orow] = lse - E / S;
   }
-  // The proposal's logit: one dot product.
-  const int pv = p.prop_tok[m];
-  const bool pok = pv >= 0 && pv < p.V;
-  if (wv == 0) {
-    const float lp = wave_dot<DT>(p, m, pok ? pv : 0);
-    if (lane == 0) p.logp_prop[orow] = pok ? lp - lse : NAN;
-  }
+  if (tid == 0) p.logp_prop[orow] = pok ? PD - lse : NAN;
 }
 
 // GEMM launch per input type: bf16 takes the direct-to-LDS kernel when the
@@ -881,7 +957,7 @@ LmPlan lm_plan(int M, int Hd, int V, int K, bool bf16) {
   pl.n_rt = (M + 64 * pl.rb - 1) / (64 * pl.rb);
   const size_t recs = (size_t)M * pl.n_groups;
   pl.rec_bytes = recs * sizeof(float);
-  pl.workspace_bytes = 7 * ((pl.rec_bytes + 255) / 256 * 256) + 256;
+  pl.workspace_bytes = 9 * ((pl.rec_bytes + 255) / 256 * 256) + 256;
   (void)Hd;
   (void)K;
   return pl;
@@ -905,11 +981,13 @@ hipError_t launch_lmhead(const LmLaunch& L, const LmPlan& pl, hipStream_t st) {
   char* ws = reinterpret_cast<char*>(L.workspace);
   p.rec_v1 = reinterpret_cast<float*>(ws);
   p.rec_v2 = reinterpret_cast<float*>(ws + stride);
-  p.rec_s = reinterpret_cast<float*>(ws + 2 * stride);
-  p.rec_e = reinterpret_cast<float*>(ws + 3 * stride);
-  p.rec_idx = reinterpret_cast<int32_t*>(ws + 4 * stride);
-  p.rec_i2 = reinterpret_cast<int32_t*>(ws + 5 * stride);
-  p.rec_v3 = reinterpret_cast<float*>(ws + 6 * stride);
+  p.rec_v3 = reinterpret_cast<float*>(ws + 2 * stride);
+  p.rec_v4 = reinterpret_cast<float*>(ws + 3 * stride);
+  p.rec_s = reinterpret_cast<float*>(ws + 4 * stride);
+  p.rec_e = reinterpret_cast<float*>(ws + 5 * stride);
+  p.rec_i1 = reinterpret_cast<int32_t*>(ws + 6 * stride);
+  p.rec_i2 = reinterpret_cast<int32_t*>(ws + 7 * stride);
+  p.rec_i3 = reinterpret_cast<int32_t*>(ws + 8 * stride);
   p.lse = L.lse;
   p.logp_prop = L.logp_prop;
   p.argmax = L.argmax;
