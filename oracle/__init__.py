@@ -7,4 +7,5 @@ from .ipdv_oracle import (  # noqa: F401
     DRIVER_S, DRIVER_T, SRC_S, SRC_T, SRC_DISCARDED, REPLACEMENT,
     append_window, gather_sequence, attention_rows, verify_attention,
     verify_attn_paged, logits_fp64, lmhead_logsoftmax, accept_scan, eq9_stepper,
+    sample_categorical, sample_takeover,
 )

@@ -20,6 +20,11 @@ What it computes, each part written from the paper's definitions:
   coverage transition of Eq. (9) over a window with the EOS and maximum
   length rules; ``eq9_stepper`` is a second, token-by-token writing of
   Eq. (9) used to cross-check it.
+* ``sample_takeover`` -- the teacher's replacement token at a takeover
+  (Eq. (9), second case: the uncovered student draft is discarded and the
+  teacher samples a replacement from its own distribution at that position,
+  temperature 1), drawn by inverse CDF over the vocabulary in index order
+  from a caller-supplied uniform.
 
 Readings where the paper is silent (tie-break, window/row alignment, cache
 rollback lengths, EOS inside a window, length cap) are listed in the
@@ -317,3 +322,50 @@ def eq9_stepper(drafts, verifier_topk, K, m1, eos_id, room):
         if changed:
             break
     return xs, zs, m, finished
+
+
+# ---------------------------------------------------------------------------
+# Takeover replacement: a draw from the teacher's distribution
+# ---------------------------------------------------------------------------
+
+def sample_categorical(logits, u):
+    """Inverse-CDF draw from softmax(logits) at temperature 1 (the rollout
+    temperature of the paper's setup) with the uniform u in [0, 1): the first
+    vocabulary index v (index order) whose cumulative probability exceeds u.
+
+    Returns (token, margin): margin is the distance of u from the nearer end
+    of the token's cumulative-probability interval [C(v-1), C(v)); a draw whose
+    margin exceeds the numerical error of a computation is the same in any
+    correct implementation of this definition."""
+    l = _f64(logits)
+    p = np.exp(l - l.max())
+    p /= p.sum()
+    c = np.cumsum(p)
+    v = int(np.searchsorted(c, u, side="right"))     # first index with c[v] > u
+    v = min(v, len(l) - 1)
+    lo = c[v - 1] if v > 0 else 0.0
+    return v, float(min(u - lo, c[v] - u))
+
+
+def sample_takeover(cu_q, driver, event_row, logits, u, eos_id):
+    """Replacement tokens for the takeovers of one verify step (Eq. (9),
+    second case; Section 3.2.3: the rejected student token is regenerated by
+    the teacher).  A sequence driven by the student (teacher verifying) whose
+    window has an event at row j -- necessarily a takeover -- gets
+    sample_categorical(logits[cu_q[b] + j], u[b]); the step is finished when
+    that token is EOS (a teacher-generated EOS is accepted directly).  Every
+    other sequence gets -1.
+
+    Returns a dict with ``token [B]``, ``eos [B]`` (bool) and ``margin [B]``
+    (inf where nothing is drawn)."""
+    B = len(driver)
+    token = np.full(B, -1, dtype=np.int64)
+    eos = np.zeros(B, dtype=bool)
+    margin = np.full(B, np.inf)
+    for b in range(B):
+        if int(driver[b]) != DRIVER_S or int(event_row[b]) < 0:
+            continue
+        r = int(cu_q[b]) + int(event_row[b])
+        token[b], margin[b] = sample_categorical(logits[r], float(u[b]))
+        eos[b] = token[b] == eos_id
+    return {"token": token, "eos": eos, "margin": margin}
