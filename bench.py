@@ -6,7 +6,8 @@
 A step is one pass of the whole verifier-side hot path over one synthetic
 batch: verify_attn_paged (window append, split-KV paged attention, split
 combine), lmhead_logsoftmax_verify (GEMM with fused log-softmax / top-K
-epilogue, merge) and accept_scan, with every input resident in HBM.  The
+epilogue, merge), accept_scan and sample_takeover (the teacher's replacement
+token at each takeover), with every input resident in HBM.  The
 default workload is the teacher shape (Qwen3-30B-A3B-like verify layer:
 32 query / 4 KV heads, head dim 128, hidden 2048, vocab 151936; 64 sequences,
 contexts uniform in [1024, 8192], 8-token windows, 16-token pages), random
@@ -37,7 +38,8 @@ from paper_2609_36546_amd import inputs, ops  # noqa: E402
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 METRIC = "verified tokens/sec at Qwen3-30B-A3B teacher shape; HBM GB/s vs peak"
-KERNELS = ["append", "attention", "combine", "lmhead_gemm", "lmhead_merge", "accept_scan"]
+KERNELS = ["append", "attention", "combine", "lmhead_gemm", "lmhead_merge", "accept_scan",
+           "sample_takeover"]
 PROFILES = os.path.join(ROOT, "profiles")
 
 
@@ -97,14 +99,18 @@ class Step:
                                                        cfg.page_size), dtype=torch.uint8, device=dev)
             ws_l = torch.empty(ops.lmhead_workspace_size(m.hidden.shape[0], m.shape.hidden,
                                                          m.shape.vocab, K), dtype=torch.uint8, device=dev)
+            row_local = torch.full((T,), -1, dtype=torch.int32, device=dev)
+            row_local[m.rows.long()] = torch.arange(m.rows.shape[0], dtype=torch.int32, device=dev)
             self.per_model.append(dict(m=m, ws_a=ws_a, ws_l=ws_l, prop=p.contiguous(),
-                                       out=torch.empty_like(m.q)))
+                                       out=torch.empty_like(m.q), row_local=row_local))
         self.outs = {
             "lse": torch.empty(T, device=dev), "logp_prop": torch.empty(T, device=dev),
             "argmax": torch.empty(T, dtype=torch.int32, device=dev),
             "topk_idx": torch.empty(T, K, dtype=torch.int32, device=dev),
             "topk_logp": torch.empty(T, K, device=dev), "entropy": torch.empty(T, device=dev)}
         self.scan_outs = None
+        self.u_repl = t(batch.u_repl, np.float32)
+        self.repl = torch.full((batch.cfg.B,), -1, dtype=torch.int32, device=dev)
 
     def run(self):
         for pm in self.per_model:
@@ -117,6 +123,14 @@ class Step:
         self.scan_outs = ops.accept_scan(self.cu, self.prop, self.outs["topk_idx"], self.K,
                                          self.driver, self.ctx, self.seq_lens, self.b.eos_id,
                                          self.b.max_len, outs=self.scan_outs)
+        # the teacher's replacement at each takeover, drawn by each verifier
+        # from its own LM-head records
+        for pm in self.per_model:
+            m = pm["m"]
+            ops.sample_takeover(m.hidden, m.W, self.K, pm["ws_l"], self.cu, self.driver,
+                                self.scan_outs["event_row"], self.u_repl, self.b.eos_id,
+                                self.scan_outs["finished"], row_local=pm["row_local"],
+                                seq_ids=m.seq_ids, token=self.repl)
 
 
 def work_per_launch(batch):
@@ -136,9 +150,9 @@ def work_per_launch(batch):
         # each row i attends to L + i + 1 keys: QK^T and PV
         res["attention"][1] += (4.0 * sh.Hq * sh.D * (k * (L + 1) + k * (k - 1) / 2)).sum()
         M = float(m.hidden.shape[0])
-        # W and the hidden rows once, plus the group records (nine 4-byte
+        # W and the hidden rows once, plus the group records (twelve 4-byte
         # values per row and 128-entry group)
-        res["lmhead_gemm"][0] += (sh.vocab + M) * sh.hidden * s + M * -(-sh.vocab // 128) * 36
+        res["lmhead_gemm"][0] += (sh.vocab + M) * sh.hidden * s + M * -(-sh.vocab // 128) * 48
         res["lmhead_gemm"][1] += 2.0 * M * sh.vocab * sh.hidden
     return res
 
@@ -172,8 +186,9 @@ def measured_traffic(kernel, workload):
         return None
 
 
-def cpu_baseline(batch, budget_s=20.0):
-    """The fp64 oracle on a bounded sample of the workload, on this host."""
+def cpu_baseline(batch, prop, budget_s=20.0):
+    """The fp64 oracle on a bounded sample of the workload, on this host, with
+    the proposals the GPU step scores (prop [T])."""
     import oracle
     try:
         from threadpoolctl import threadpool_info
@@ -201,10 +216,15 @@ def cpu_baseline(batch, budget_s=20.0):
         t0 = time.perf_counter()
         oracle.verify_attn_paged(q, kn, vn, kc, vc, sub_pt, batch.ctx_lens[b:b + 1],
                                  np.array([0, r1 - r0]), 1.0 / np.sqrt(sh.D))
-        res = oracle.lmhead_logsoftmax(hid, W, np.zeros(r1 - r0, np.int64), batch.cfg.K)
-        oracle.accept_scan(np.array([0, r1 - r0]), res["argmax"], res["topk_idx"], batch.cfg.K,
-                           batch.driver[b:b + 1], batch.ctx_lens[b:b + 1], batch.seq_lens[b:b + 1],
-                           batch.eos_id, batch.max_len)
+        res = oracle.lmhead_logsoftmax(hid, W, prop[r0:r1], batch.cfg.K)
+        sc = oracle.accept_scan(np.array([0, r1 - r0]), prop[r0:r1], res["topk_idx"], batch.cfg.K,
+                                batch.driver[b:b + 1], batch.ctx_lens[b:b + 1],
+                                batch.seq_lens[b:b + 1], batch.eos_id, batch.max_len)
+        ev = int(sc["event_row"][0])
+        if ev >= 0 and int(batch.driver[b]) == oracle.DRIVER_S:
+            row_logits = oracle.logits_fp64(hid[ev:ev + 1], W)
+            oracle.sample_takeover(np.array([0, 1]), batch.driver[b:b + 1], np.array([0]),
+                                   row_logits, batch.u_repl[b:b + 1].astype(np.float64), batch.eos_id)
         t_total += time.perf_counter() - t0
         rows_done += r1 - r0
         seqs_done += 1
@@ -252,7 +272,7 @@ def main():
 
     # per-kernel timing: the library records these events around its kernels
     n_models = len(step.per_model)
-    per_step = 7 * n_models + 2
+    per_step = 9 * n_models + 2
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(per_step)] for _ in range(args.steps)]
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -265,10 +285,6 @@ def main():
     torch.cuda.synchronize()
     ms = start.elapsed_time(stop) / args.steps
 
-    names = []
-    for _ in range(n_models):
-        names += ["append", "attention", "combine", "lmhead_gemm", "lmhead_merge"]
-    names += ["accept_scan"]
     kt = {k: 0.0 for k in KERNELS}
     for s in range(args.steps):
         e = evs[s]
@@ -282,6 +298,10 @@ def main():
             kt["lmhead_merge"] += e[i + 5].elapsed_time(e[i + 6])
             i += 7
         kt["accept_scan"] += e[i].elapsed_time(e[i + 1])
+        i += 2
+        for _ in range(n_models):
+            kt["sample_takeover"] += e[i].elapsed_time(e[i + 1])
+            i += 2
     kt = {k: v / args.steps for k, v in kt.items()}
 
     work = work_per_launch(batch)
@@ -321,7 +341,7 @@ def main():
         "lmhead_tflops": round(work["lmhead_gemm"][1] / (kt["lmhead_gemm"] * 1e-3) / 1e12, 1),
     }
     if not args.no_cpu:
-        res["cpu_baseline"] = cpu_baseline(batch)
+        res["cpu_baseline"] = cpu_baseline(batch, step.prop.cpu().numpy().astype(np.int64))
     print(json.dumps(res), flush=True)
 
 

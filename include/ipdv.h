@@ -2,7 +2,7 @@
  * ipdv.h -- C ABI of the verifier-side window scoring library (libipdv.so)
  * for AMD Instinct MI355X (gfx950).
  *
- * The three entry points are the verifier's calls in one propose-and-verify
+ * The entry points are the verifier's calls in one propose-and-verify
  * step of Interactive-Policy Distillation (Section 3.2.3, "Fused Inference
  * Engine", and Eq. (9)):
  *
@@ -17,7 +17,10 @@
  *   accept_scan              -- the verdict stage: the top-K coverage rule of
  *                               Eq. (9) applied as a first-event scan over each
  *                               window, with the EOS and length rules and the
- *                               rollback length shared by both caches.
+ *                               rollback length shared by both caches;
+ *   sample_takeover          -- the teacher's replacement token at each
+ *                               takeover (Eq. (9), second case), drawn from
+ *                               the verifier's distribution at that row.
  *
  * Conventions common to every entry point:
  *   - All array arguments are DEVICE pointers owned by the caller (except the
@@ -220,6 +223,47 @@ int accept_scan(const int32_t* cu_q, const int32_t* prop_tok,
                 void* hip_stream);
 
 /*
+ * sample_takeover -- the teacher's replacement token at a takeover (Eq. (9),
+ * second case: the uncovered student draft is discarded and the teacher
+ * samples a replacement from its own distribution q(. | c_t) at that position;
+ * Section 3.2.3: the rejected token is regenerated by the teacher).  The
+ * verifier's logits at the takeover row are that distribution, so the draw
+ * reuses the preceding lmhead_logsoftmax_verify call instead of a decode step.
+ *
+ * The call handles the sequences b = seq_ids[i], i < n_seq (seq_ids NULL: b =
+ * i), and writes token / finished of those only, so that the calls of two
+ * verifiers (two models, each with its own rows) compose.  For each such b
+ * with driver[b] == IPDV_DRIVER_S and event_row[b] >= 0 (accept_scan's
+ * outputs: a takeover at row j = event_row[b]) the row is r = cu_q[b] + j and
+ * its hidden row m = row_local ? row_local[r] : r; then
+ *   token[b] = the first vocabulary index v (index order) with
+ *              sum_{w <= v} softmax(l_m)_w > u[b]      (temperature 1)
+ * -- the inverse-CDF draw with the caller's uniform u[b] in [0, 1) -- and
+ * finished[b] is set to 1 when token[b] == eos_id (a teacher EOS is accepted
+ * directly).  The other handled sequences, and those whose m is negative or
+ * not below M, get token -1 and keep their finished flag.
+ *
+ * hidden, W, M, Hd, V, K, dtype and workspace must be those of the preceding
+ * lmhead_logsoftmax_verify call over the rows of hidden, with the workspace
+ * unchanged since (its group records hold each 128-entry group's mass; the
+ * chosen group's 128 logits are recomputed exactly).  seq_ids [n_seq] int32
+ * or NULL; cu_q [B+1] int32, driver [B] uint8, event_row [B] int32, row_local
+ * [T] int32 or NULL, u [B] float (B = the batch's sequences).  Outputs: token
+ * int32 [B]; finished uint8 [B] (updated in place).
+ * The draw agrees with the exact one whenever u[b] is farther than the fp32
+ * rounding of the cumulative probabilities (about 1e-5) from an interval end.
+ *
+ * Errors: IPDV_EINVAL (null pointer, n_seq < 0, the LM-head shape rules),
+ * IPDV_EUNSUPPORTED, IPDV_EWORKSPACE, IPDV_EHIP.
+ */
+int sample_takeover(const void* hidden, const void* W, int M, int Hd, int V, int K,
+                    const void* workspace, size_t workspace_bytes,
+                    const int32_t* seq_ids, int n_seq,
+                    const int32_t* cu_q, const uint8_t* driver, const int32_t* event_row,
+                    const int32_t* row_local, const float* u, int32_t eos_id,
+                    int32_t* token, uint8_t* finished, int dtype, void* hip_stream);
+
+/*
  * Optional timing hook for profilers and benchmarks (thread-local).  While
  * set, each kernel an entry point launches is bracketed by hipEventRecord of
  * the caller's events (hipEvent_t handles cast to void*), taken from
@@ -229,7 +273,7 @@ int accept_scan(const int32_t* cu_q, const int32_t* prop_tok,
  * ipdv_trace_count() returns how many events have been recorded since the
  * hook was last set.  Kernels per call: verify_attn_paged 3 (append,
  * attention, split combine), lmhead_logsoftmax_verify 2 (GEMM + epilogue,
- * merge), accept_scan 1.
+ * merge), accept_scan 1, sample_takeover 1.
  */
 int ipdv_trace_events(void* const* events, int capacity);
 int ipdv_trace_count(void);

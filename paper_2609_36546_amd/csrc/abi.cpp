@@ -169,6 +169,31 @@ int lmhead_logsoftmax_verify(const void* hidden, const void* W, const int32_t* p
   return ok();
 }
 
+int sample_takeover(const void* hidden, const void* W, int M, int Hd, int V, int K,
+                    const void* workspace, size_t workspace_bytes, const int32_t* seq_ids,
+                    int n_seq, const int32_t* cu_q, const uint8_t* driver, const int32_t* event_row,
+                    const int32_t* row_local, const float* u, int32_t eos_id, int32_t* token,
+                    uint8_t* finished, int dtype, void* hip_stream) {
+  int st = lm_shape_check(M, Hd, V, K);
+  if (st != IPDV_OK) return st;
+  if (dtype != IPDV_F32 && dtype != IPDV_BF16) return fail(IPDV_EUNSUPPORTED, "dtype %d", dtype);
+  if (n_seq < 0) return fail(IPDV_EINVAL, "n_seq must be >= 0 (got %d)", n_seq);
+  if (n_seq > 65535 * 32) return fail(IPDV_EUNSUPPORTED, "n_seq too large");
+  if (n_seq == 0) return ok();
+  if (!hidden || !W || !cu_q || !driver || !event_row || !u || !token || !finished)
+    return fail(IPDV_EINVAL, "null required pointer");
+  const ipdv::LmPlan pl = ipdv::lm_plan(M, Hd, V, K, dtype == IPDV_BF16);
+  const size_t need = ipdv::lm_plan(M, Hd, V, K, true).workspace_bytes;
+  if (!workspace || workspace_bytes < need)
+    return fail(IPDV_EWORKSPACE, "workspace of %zu bytes needed (got %zu)", need,
+                workspace ? workspace_bytes : (size_t)0);
+  ipdv::SampleLaunch L{hidden, W, M, Hd, V, K, workspace, seq_ids, n_seq, cu_q, driver, event_row,
+                       row_local, u, eos_id, token, finished, dtype == IPDV_BF16};
+  hipError_t e = ipdv::launch_sample_takeover(L, pl, reinterpret_cast<hipStream_t>(hip_stream));
+  if (e != hipSuccess) return hip_fail("sample_takeover launch", e);
+  return ok();
+}
+
 int accept_scan(const int32_t* cu_q, const int32_t* prop_tok, const int32_t* topk_idx, int K,
                 const uint8_t* driver, const int32_t* ctx_lens, const int32_t* seq_lens,
                 int32_t eos_id, int32_t max_len, int B, int32_t* n_acc, int32_t* event_row,

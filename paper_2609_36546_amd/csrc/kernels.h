@@ -73,6 +73,26 @@ struct LmLaunch {
 LmPlan lm_plan(int M, int Hd, int V, int K, bool bf16);
 hipError_t launch_lmhead(const LmLaunch& L, const LmPlan& pl, hipStream_t st);
 
+struct SampleLaunch {
+  const void* hidden;
+  const void* W;
+  int M, Hd, V, K;
+  const void* workspace;       // the records of the preceding LM-head call
+  const int32_t* seq_ids;      // sequences to draw for (NULL: 0 .. n_seq-1)
+  int n_seq;
+  const int32_t* cu_q;
+  const uint8_t* driver;
+  const int32_t* event_row;
+  const int32_t* row_local;
+  const float* u;
+  int32_t eos_id;
+  int32_t* token;
+  uint8_t* finished;
+  bool dtype_bf16;
+};
+
+hipError_t launch_sample_takeover(const SampleLaunch& L, const LmPlan& pl, hipStream_t st);
+
 // ---- verdict scan ----
 struct ScanLaunch {
   const int32_t* cu_q;

@@ -46,13 +46,14 @@ struct LmParams {
   int M, Hd, V, K;
   int n_groups, n_rt, n_vt;
   // Group records, [M][n_groups] each: the three largest logits of the group
-  // with their indices, the fourth largest value, sum exp(l - v1) and
-  // sum exp(l - v1) * l.
+  // with their indices, the fourth largest value, sum exp(l - v1) over each
+  // 32-entry quarter of the group (rec_sq[q]: entries 32 q .. 32 q + 31) and
+  // sum exp(l - v1) * l over the group.
   float* rec_v1;
   float* rec_v2;
   float* rec_v3;
   float* rec_v4;
-  float* rec_s;
+  float* rec_sq[4];
   float* rec_e;
   int32_t* rec_i1;
   int32_t* rec_i2;
@@ -173,18 +174,20 @@ __device__ __forceinline__ void lm_epilogue(const LmParams& p, floatx16 (&acc)[4
     }
     // v1 is now the group maximum; exp-sum and entropy numerator against it
     const float mub = ((v1 == -INFINITY) ? 0.f : v1) * kLog2e;
-    float s = 0.f, ee = 0.f;
+    // block vb of the accumulators is the group's quarter vb (32 entries)
+    float sq[4] = {0.f, 0.f, 0.f, 0.f}, ee = 0.f;
 #pragma unroll
     for (int j = 0; j < 64; ++j) {
       const float x = acc[j >> 4][rb][j & 15];
       const float pe = fast_exp2(fmaf(x, kLog2e, -mub));
-      s += pe;
+      sq[j >> 4] += pe;
       if (FULL)
         ee = fmaf(pe, x, ee);
       else
         ee += (x != -INFINITY) ? pe * x : 0.f;
     }
-    s += __shfl_xor(s, 32, kWave);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) sq[q] += __shfl_xor(sq[q], 32, kWave);
     ee += __shfl_xor(ee, 32, kWave);
     if (h == 0 && m < p.M && g < p.n_groups) {
       const size_t r = (size_t)m * p.n_groups + g;
@@ -192,7 +195,8 @@ __device__ __forceinline__ void lm_epilogue(const LmParams& p, floatx16 (&acc)[4
       p.rec_v2[r] = v2;
       p.rec_v3[r] = v3;
       p.rec_v4[r] = v4;
-      p.rec_s[r] = (v1 == -INFINITY) ? 0.f : s;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) p.rec_sq[q][r] = (v1 == -INFINITY) ? 0.f : sq[q];
       p.rec_e[r] = (v1 == -INFINITY) ? 0.f : ee;
       p.rec_i1[r] = i1;
       p.rec_i2[r] = i2;
@@ -609,29 +613,26 @@ template <typename DT> struct Frag16;
 template <> struct Frag16<bf16> { typedef bf16x8 type; };
 template <> struct Frag16<float> { typedef floatx4 type; };
 
-// Exact logits of the split groups' entries for the hidden row staged in
-// s_hid (fp32).  A wave takes 4 entries at a time and lane l covers channels
+// Exact logits of n vocabulary entries, vocab_of(e) for e < n (entries past V
+// give -inf), for the hidden row staged in s_hid (fp32).  A wave takes NB entries at a time and lane l covers channels
 // EPL l + 64 EPL i of each, so one load instruction reads 64 consecutive
-// 16-byte chunks of a W row and the loads of all 4 entries (4 chunks each)
+// 16-byte chunks of a W row and the loads of all NB entries (4 chunks each)
 // are in flight together; a shuffle reduction finishes each dot product.
-template <typename DT>
-__device__ void recompute_logits(const LmParams& p, const float* s_hid, const int* s_split, int ns,
-                                 float* out_v, int* out_i) {
+template <typename DT, int NB, typename VOCAB>   // NB: entries per wave and batch
+__device__ void recompute_entries(const LmParams& p, const float* s_hid, int n, VOCAB vocab_of,
+                                  float* out_v, int* out_i) {
   typedef typename Frag16<DT>::type frag;
   const DT* Wp = reinterpret_cast<const DT*>(p.W);
   constexpr int EPL = 16 / (int)sizeof(DT);
-  constexpr int NB = 4;                       // entries per batch
   constexpr int NP = 4;                       // chunks per lane and entry in flight
   constexpr int NW = kMT / kWave;
   const int lane = lane_id(), wv = threadIdx.x / kWave;
-  const int n = ns * kGroup;
   for (int e0 = wv * NB; e0 < n; e0 += NW * NB) {
     float acc[NB];
     int vv[NB];
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
-      const int e = min(e0 + b, n - 1);
-      vv[b] = s_split[e / kGroup] * kGroup + e % kGroup;
+      vv[b] = vocab_of(min(e0 + b, n - 1));
       acc[b] = 0.f;
     }
     for (int c0 = 0; c0 < p.Hd; c0 += NP * kWave * EPL) {
@@ -669,6 +670,15 @@ __device__ void recompute_logits(const LmParams& p, const float* s_hid, const in
       }
     }
   }
+}
+
+// The 128 logits of each listed group (split groups of the merge).
+template <typename DT, int NB = 4>
+__device__ void recompute_logits(const LmParams& p, const float* s_hid, const int* s_split, int ns,
+                                 float* out_v, int* out_i) {
+  recompute_entries<DT, NB>(p, s_hid, ns * kGroup,
+                            [&](int e) { return s_split[e / kGroup] * kGroup + e % kGroup; },
+                            out_v, out_i);
 }
 
 template <typename DT>
@@ -731,7 +741,8 @@ __global__ __launch_bounds__(kMT) void lmhead_merge_kernel(LmParams p) {
     ci[kCPG * u] = ok ? p.rec_i1[base + gi] : 0x7fffffff;
     ci[kCPG * u + 1] = ok ? p.rec_i2[base + gi] : 0x7fffffff;
     ci[kCPG * u + 2] = ok ? p.rec_i3[base + gi] : 0x7fffffff;
-    rs[u] = ok ? p.rec_s[base + gi] : 0.f;
+    rs[u] = ok ? (p.rec_sq[0][base + gi] + p.rec_sq[1][base + gi]) +
+                     (p.rec_sq[2][base + gi] + p.rec_sq[3][base + gi]) : 0.f;
     re[u] = ok ? p.rec_e[base + gi] : 0.f;
     mx = fmaxf(mx, cv[kCPG * u]);
   }
@@ -899,6 +910,184 @@ __global__ __launch_bounds__(kMT) void lmhead_merge_kernel(LmParams p) {
   if (tid == 0) p.logp_prop[orow] = pok ? PD - lse : NAN;
 }
 
+// ---------------------------------------------------------------------------
+// Takeover replacement draw (Eq. (9), second case): one workgroup per
+// sequence.  The inverse CDF over the vocabulary in index order is taken in
+// two levels: the group records give each 128-entry group's mass,
+// s_g exp(v1_g - max), so a block-wide prefix scan over the groups finds the
+// group the uniform falls in; that group's 128 logits are recomputed exactly
+// and the draw finishes inside it, at the same fraction of the group's mass.
+// ---------------------------------------------------------------------------
+
+struct SampleParams {
+  const int32_t* seq_ids;
+  const int32_t* cu_q;
+  const uint8_t* driver;
+  const int32_t* event_row;
+  const int32_t* row_local;
+  const float* u;
+  int32_t eos_id;
+  int32_t* token;
+  uint8_t* finished;
+};
+
+// Inclusive prefix sum over the block (thread order); *total gets the sum.
+__device__ float block_scan(float x, float* s_w, float* total) {
+  const int lane = lane_id(), w = threadIdx.x / kWave;
+  constexpr int NW = kMT / kWave;
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    const float y = __shfl_up(x, o, kWave);
+    if (lane >= o) x += y;
+  }
+  __syncthreads();
+  if (lane == kWave - 1) s_w[w] = x;
+  __syncthreads();
+  float before = 0.f, all = 0.f;
+  for (int ww = 0; ww < NW; ++ww) {
+    before += ww < w ? s_w[ww] : 0.f;
+    all += s_w[ww];
+  }
+  *total = all;
+  return x + before;
+}
+
+template <typename DT>
+__global__ __launch_bounds__(kMT) void sample_takeover_kernel(LmParams p, SampleParams s) {
+  constexpr int NW = kMT / kWave;
+  const int b = s.seq_ids ? s.seq_ids[blockIdx.x] : blockIdx.x;
+  const int tid = threadIdx.x;
+  __shared__ float s_red[3 * NW];
+  __shared__ float s_hid[kMaxHd];
+  __shared__ int s_g[1];
+  __shared__ int s_first, s_last;
+  __shared__ float s_cv[32];
+  __shared__ int s_ci[32];
+  const int ev = s.event_row[b];
+  const int r = ev >= 0 ? s.cu_q[b] + ev : -1;
+  const int m = r < 0 ? -1 : (s.row_local ? s.row_local[r] : r);
+  // only student-driven windows with an event (a takeover) draw
+  if (s.driver[b] != 0 || ev < 0 || m < 0 || m >= p.M) {
+    if (tid == 0) s.token[b] = -1;
+    return;
+  }
+  const int G = p.n_groups;
+  const size_t base = (size_t)m * G;
+  // Thread t holds the records of groups [t per, (t+1) per) in registers; the
+  // hidden row is staged in LDS meanwhile (for the recompute below).
+  const int per = (G + kMT - 1) / kMT;          // <= kMaxGPT (V <= kMT kMaxGPT kGroup)
+  const int g0 = tid * per;
+  float v1r[kMaxGPT], wr[kMaxGPT];
+#pragma unroll
+  for (int i = 0; i < kMaxGPT; ++i) {
+    const bool ok = i < per && g0 + i < G;
+    v1r[i] = ok ? p.rec_v1[base + g0 + i] : -INFINITY;
+    wr[i] = ok ? (p.rec_sq[0][base + g0 + i] + p.rec_sq[1][base + g0 + i]) +
+                     (p.rec_sq[2][base + g0 + i] + p.rec_sq[3][base + g0 + i]) : 0.f;
+  }
+  {
+    const DT* hr = reinterpret_cast<const DT*>(p.hidden) + (size_t)m * p.Hd;
+    for (int k = tid; k < p.Hd; k += kMT) s_hid[k] = to_f32(hr[k]);
+  }
+  float mx = -INFINITY;
+#pragma unroll
+  for (int i = 0; i < kMaxGPT; ++i) mx = fmaxf(mx, v1r[i]);
+  mx = block_max(mx, s_red);
+  float mine = 0.f;                              // this thread's mass
+#pragma unroll
+  for (int i = 0; i < kMaxGPT; ++i) {
+    wr[i] = v1r[i] != -INFINITY ? wr[i] * fast_exp2((v1r[i] - mx) * kLog2e) : 0.f;
+    mine += wr[i];
+  }
+  float tot;
+  const float incl = block_scan(mine, s_red, &tot);
+  const float t = s.u[b] * tot;
+  // the thread whose range holds t walks its groups in order; if rounding put
+  // t above every cumulative sum, the last group with mass is taken
+  if (tid == 0) { s_first = kMT; s_last = -1; s_g[0] = -1; }
+  __syncthreads();
+  if (mine > 0.f && incl > t) atomicMin(&s_first, tid);
+  if (mine > 0.f) atomicMax(&s_last, tid);
+  __syncthreads();
+  const int owner = s_first < kMT ? s_first : s_last;
+  if (tid == owner) {
+    // walk this thread's groups in order: the first whose cumulative mass
+    // passes t; the last with mass when t is above them all (rounding)
+    const bool crossing = s_first < kMT;
+    float c = incl - mine;
+    int gi = -1;
+    float before = 0.f, w = 1.f;
+    bool found = false;
+#pragma unroll
+    for (int i = 0; i < kMaxGPT; ++i) {
+      if (!found && wr[i] > 0.f) {
+        gi = g0 + i;
+        before = c;
+        w = wr[i];
+        found = crossing && c + wr[i] > t;
+      }
+      c += wr[i];
+    }
+    s_g[0] = gi;
+    s_red[2 * NW] = found ? fminf(fmaxf((t - before) / w, 0.f), 1.f) : 1.f;
+  }
+  __syncthreads();
+  const int gsel = s_g[0];
+  const float frac = s_red[2 * NW];
+  if (gsel < 0) {                  // no mass at all (cannot happen for finite logits)
+    if (tid == 0) s.token[b] = -1;
+    return;
+  }
+  // the quarter of the group (32 entries) holding the draw, from its sums
+  const float q0 = p.rec_sq[0][base + gsel], q1 = p.rec_sq[1][base + gsel];
+  const float q2 = p.rec_sq[2][base + gsel], q3 = p.rec_sq[3][base + gsel];
+  const float qs[4] = {q0, q1, q2, q3};
+  const float tq = frac * ((q0 + q1) + (q2 + q3));
+  // first quarter whose cumulative sum passes tq; the last with mass when
+  // rounding leaves tq above them all
+  int qsel = 0;
+  float qbefore = 0.f, cq = 0.f;
+  bool qfound = false;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    if (!qfound && qs[q] > 0.f) {
+      qsel = q;
+      qbefore = cq;
+      qfound = cq + qs[q] > tq;
+    }
+    cq += qs[q];
+  }
+  const float frac2 = qfound ? fminf(fmaxf((tq - qbefore) / qs[qsel], 0.f), 1.f) : 1.f;
+  const int v0 = gsel * kGroup + 32 * qsel;
+  // exact logits of the quarter's 32 entries (one batch: 8 per wave), then
+  // the draw inside it at the same fraction of its mass
+  recompute_entries<DT, 8>(p, s_hid, 32, [&](int e) { return v0 + e; }, s_cv, s_ci);
+  __syncthreads();
+  if (tid < kWave) {
+    const float a = tid < 32 ? s_cv[tid] : -INFINITY;
+    float gm = a;
+    for (int o = 32; o > 0; o >>= 1) gm = fmaxf(gm, __shfl_xor(gm, o, kWave));
+    const float pr = a == -INFINITY ? 0.f : fast_exp2((a - gm) * kLog2e);
+    float c = pr;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+      const float y = __shfl_up(c, o, kWave);
+      if (tid >= o) c += y;
+    }
+    const float S = __shfl(c, kWave - 1, kWave);
+    const float th = frac2 * S;
+    const unsigned long long in = __ballot(pr > 0.f && c > th);
+    const unsigned long long nz = __ballot(pr > 0.f);
+    const int i = in ? __builtin_ctzll(in) : 63 - __builtin_clzll(nz);   // rounding guard
+    if (tid == 0) {
+      const int tok = s_ci[i];
+      s.token[b] = tok;
+      if (tok == s.eos_id) s.finished[b] = 1;
+    }
+  }
+}
+
+
 // GEMM launch per input type: bf16 takes the direct-to-LDS kernel when the
 // hidden size is a multiple of four stages, fp32 the register-staged one.
 template <int RB>
@@ -957,37 +1146,49 @@ LmPlan lm_plan(int M, int Hd, int V, int K, bool bf16) {
   pl.n_rt = (M + 64 * pl.rb - 1) / (64 * pl.rb);
   const size_t recs = (size_t)M * pl.n_groups;
   pl.rec_bytes = recs * sizeof(float);
-  pl.workspace_bytes = 9 * ((pl.rec_bytes + 255) / 256 * 256) + 256;
+  pl.workspace_bytes = 12 * ((pl.rec_bytes + 255) / 256 * 256) + 256;
   (void)Hd;
   (void)K;
   return pl;
 }
 
-hipError_t launch_lmhead(const LmLaunch& L, const LmPlan& pl, hipStream_t st) {
-  if (L.M == 0) return hipSuccess;
+namespace {
+
+// Kernel parameters of an LM-head call: shapes, plan and the record arrays
+// carved out of the workspace.
+LmParams lm_params(const void* hidden, const void* W, int M, int Hd, int V, int K, const LmPlan& pl,
+                   void* workspace) {
   LmParams p{};
-  p.hidden = L.hidden;
-  p.W = L.W;
-  p.prop_tok = L.prop_tok;
-  p.out_rows = L.out_rows;
-  p.M = L.M;
-  p.Hd = L.Hd;
-  p.V = L.V;
-  p.K = L.K;
+  p.hidden = hidden;
+  p.W = W;
+  p.M = M;
+  p.Hd = Hd;
+  p.V = V;
+  p.K = K;
   p.n_groups = pl.n_groups;
   p.n_rt = pl.n_rt;
   p.n_vt = pl.n_vt;
   const size_t stride = (pl.rec_bytes + 255) / 256 * 256;
-  char* ws = reinterpret_cast<char*>(L.workspace);
+  char* ws = reinterpret_cast<char*>(workspace);
   p.rec_v1 = reinterpret_cast<float*>(ws);
   p.rec_v2 = reinterpret_cast<float*>(ws + stride);
   p.rec_v3 = reinterpret_cast<float*>(ws + 2 * stride);
   p.rec_v4 = reinterpret_cast<float*>(ws + 3 * stride);
-  p.rec_s = reinterpret_cast<float*>(ws + 4 * stride);
-  p.rec_e = reinterpret_cast<float*>(ws + 5 * stride);
-  p.rec_i1 = reinterpret_cast<int32_t*>(ws + 6 * stride);
-  p.rec_i2 = reinterpret_cast<int32_t*>(ws + 7 * stride);
-  p.rec_i3 = reinterpret_cast<int32_t*>(ws + 8 * stride);
+  for (int q = 0; q < 4; ++q) p.rec_sq[q] = reinterpret_cast<float*>(ws + (4 + q) * stride);
+  p.rec_e = reinterpret_cast<float*>(ws + 8 * stride);
+  p.rec_i1 = reinterpret_cast<int32_t*>(ws + 9 * stride);
+  p.rec_i2 = reinterpret_cast<int32_t*>(ws + 10 * stride);
+  p.rec_i3 = reinterpret_cast<int32_t*>(ws + 11 * stride);
+  return p;
+}
+
+}  // namespace
+
+hipError_t launch_lmhead(const LmLaunch& L, const LmPlan& pl, hipStream_t st) {
+  if (L.M == 0) return hipSuccess;
+  LmParams p = lm_params(L.hidden, L.W, L.M, L.Hd, L.V, L.K, pl, L.workspace);
+  p.prop_tok = L.prop_tok;
+  p.out_rows = L.out_rows;
   p.lse = L.lse;
   p.logp_prop = L.logp_prop;
   p.argmax = L.argmax;
@@ -1003,6 +1204,21 @@ hipError_t launch_lmhead(const LmLaunch& L, const LmPlan& pl, hipStream_t st) {
     }
   }
   return launch_rb<float, 1>(p, st);
+}
+
+hipError_t launch_sample_takeover(const SampleLaunch& L, const LmPlan& pl, hipStream_t st) {
+  if (L.n_seq == 0) return hipSuccess;
+  const LmParams p = lm_params(L.hidden, L.W, L.M, L.Hd, L.V, L.K, pl, const_cast<void*>(L.workspace));
+  const SampleParams s{L.seq_ids, L.cu_q, L.driver, L.event_row, L.row_local, L.u, L.eos_id, L.token,
+                       L.finished};
+  trace_begin(st);
+  if (L.dtype_bf16)
+    hipLaunchKernelGGL((sample_takeover_kernel<bf16>), dim3(L.n_seq), dim3(kMT), 0, st, p, s);
+  else
+    hipLaunchKernelGGL((sample_takeover_kernel<float>), dim3(L.n_seq), dim3(kMT), 0, st, p, s);
+  const hipError_t e = hipGetLastError();
+  trace_mark(st);
+  return e;
 }
 
 }  // namespace ipdv

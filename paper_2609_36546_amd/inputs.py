@@ -158,6 +158,7 @@ class Batch:
     models: List[ModelInputs] = field(default_factory=list)
     u_mode: np.ndarray = None    # float64 [T]: proposal mode draw
     u_tok: np.ndarray = None     # float64 [T]: proposal token draw
+    u_repl: np.ndarray = None    # float32 [B]: uniform of the replacement draw at a takeover
     eos_id: int = 0
     max_len: int = INT32_MAX
 
@@ -282,6 +283,8 @@ def make_batch(cfg: WorkloadConfig, seed: int = 0, device="cpu", poison: bool = 
     prng = _rng(seed, cfg.id, 1)
     batch.u_mode = prng.random(T)
     batch.u_tok = prng.random(T)
+    # float32 in [0, 1): both the library and the oracle draw with this value
+    batch.u_repl = np.minimum(_rng(seed, cfg.id, 2).random(cfg.B), 1.0 - 2.0 ** -24).astype(np.float32)
     batch.eos_id = cfg.models[0].vocab - 1
     return batch
 

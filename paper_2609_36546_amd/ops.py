@@ -55,6 +55,9 @@ def lib() -> ctypes.CDLL:
         L.accept_scan.argtypes = [i32p, i32p, i32p, ci, u8p, i32p, i32p, ctypes.c_int32,
                                   ctypes.c_int32, ci, i32p, i32p, u8p, u8p, i32p, u8p, vp]
         L.accept_scan.restype = ci
+        L.sample_takeover.argtypes = [vp, vp, ci, ci, ci, ci, vp, cs, i32p, ci, i32p, u8p, i32p,
+                                      i32p, f32p, ctypes.c_int32, i32p, u8p, ci, vp]
+        L.sample_takeover.restype = ci
         L.ipdv_trace_events.argtypes = [ctypes.c_void_p, ci]
         L.ipdv_trace_events.restype = ci
         L.ipdv_trace_count.restype = ci
@@ -267,3 +270,43 @@ def accept_scan(cu_q, prop_tok, topk_idx, K: int, driver, ctx_lens, seq_lens, eo
         _ptr(outs["finished"]), _ptr(outs["new_cache_len"]), _ptr(outs["src"]), _stream(dev))
     _check("accept_scan", st)
     return outs
+
+
+def sample_takeover(hidden, W, K: int, workspace, cu_q, driver, event_row, u, eos_id: int,
+                    finished, row_local=None, seq_ids=None, token=None):
+    """Teacher replacement tokens at the takeovers (see include/ipdv.h).
+
+    hidden, W, K and workspace as passed to the preceding
+    lmhead_logsoftmax_verify call (its records are read); cu_q [B+1] int32,
+    driver [B] uint8, event_row [B] int32 (accept_scan's), u [B] float32
+    uniforms in [0, 1), row_local [T] int32 or None, seq_ids [n] int32 or None
+    (the sequences handled; None: all B), finished [B] uint8 (updated in
+    place).  Returns token [B] int32 (-1: no draw; entries of sequences not
+    handled are left as they were in `token`)."""
+    dev = hidden.device
+    dt = hidden.dtype
+    _need(hidden, "hidden", dt, dev, 2)
+    _need(W, "W", dt, dev, 2)
+    M, Hd = hidden.shape
+    V = W.shape[0]
+    _need(cu_q, "cu_q", torch.int32, dev, 1)
+    B = cu_q.shape[0] - 1
+    _need(driver, "driver", torch.uint8, dev, 1)
+    _need(event_row, "event_row", torch.int32, dev, 1)
+    _need(u, "u", torch.float32, dev, 1)
+    _need(finished, "finished", torch.uint8, dev, 1)
+    if row_local is not None:
+        _need(row_local, "row_local", torch.int32, dev, 1)
+    n_seq = B
+    if seq_ids is not None:
+        _need(seq_ids, "seq_ids", torch.int32, dev, 1)
+        n_seq = seq_ids.shape[0]
+    if token is None:
+        token = torch.full((B,), -1, dtype=torch.int32, device=dev)
+    st = lib().sample_takeover(
+        _ptr(hidden), _ptr(W), M, Hd, V, K, _ptr(workspace),
+        workspace.numel() * workspace.element_size(), _ptr(seq_ids), n_seq, _ptr(cu_q),
+        _ptr(driver), _ptr(event_row), _ptr(row_local), _ptr(u), int(eos_id), _ptr(token),
+        _ptr(finished), _dtype_code(dt), _stream(dev))
+    _check("sample_takeover", st)
+    return token

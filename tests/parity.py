@@ -148,3 +148,42 @@ def oracle_attention_subset(mdl, batch, seqs, D):
     out, _, _ = oracle.verify_attn_paged(q, kn, vn, kc, vc, sub_pt, batch.ctx_lens, batch.cu_q,
                                          1.0 / np.sqrt(D), seq_ids=list(seqs))
     return out, rows
+
+
+# Takeover draws: the numerical error bound of the GPU's cumulative
+# probabilities (fp32 group masses over up to 2048 groups and 128 entries,
+# relative rounding below 2048 * 6e-8 of the total, plus fp32-vs-fp64 logits).
+DRAW_TOL = 1.2e-4
+
+
+def check_takeover_draws(tok, fin, fin0, ref, logits_of_row, cu_q, driver, event_row, u, eos_id,
+                         handled=None):
+    """GPU draws against the oracle's: equal where the oracle margin exceeds
+    DRAW_TOL, otherwise valid (u within DRAW_TOL of the drawn token's
+    cumulative interval); finished set exactly when the draw is EOS.
+    logits_of_row(r) returns the fp64 logits of global row r, or None when the
+    row is not the handling verifier's.  Returns the number of exact draws."""
+    exact = 0
+    B = len(driver)
+    for b in range(B):
+        if handled is not None and b not in handled:
+            continue
+        r = int(cu_q[b]) + int(event_row[b]) if event_row[b] >= 0 else -1
+        l = logits_of_row(r) if r >= 0 else None
+        drawn = int(driver[b]) == oracle.DRIVER_S and l is not None
+        if not drawn:
+            assert tok[b] == -1, b
+            assert fin[b] == fin0[b], b
+            continue
+        if ref["margin"][b] > DRAW_TOL:
+            assert tok[b] == ref["token"][b], (b, tok[b], ref["token"][b], ref["margin"][b])
+            exact += 1
+        else:
+            p = np.exp(l - l.max())
+            p /= p.sum()
+            c = np.cumsum(p)
+            lo = c[tok[b] - 1] if tok[b] > 0 else 0.0
+            assert p[tok[b]] > 0 and lo - DRAW_TOL <= u[b] < c[tok[b]] + DRAW_TOL, \
+                (b, tok[b], u[b], lo, c[tok[b]])
+        assert fin[b] == (1 if tok[b] == eos_id else fin0[b]), b
+    return exact

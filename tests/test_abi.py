@@ -111,3 +111,28 @@ def test_scan_argument_errors():
 
 def test_lmhead_vocab_limit():
     assert _lm(V=262145, K=16) == -2
+
+
+def _sample(**kw):
+    args = dict(hidden=1, W=1, M=8, Hd=256, V=1024, K=16, ws=1, wsb=1 << 30, seq_ids=None, n_seq=2,
+                cu=1, driver=1, ev=1, row_local=None, u=1, eos=1023, token=1, fin=1,
+                dtype=ops.IPDV_BF16)
+    args.update(kw)
+    a = args
+    vp = lambda x: None if x is None else ctypes.c_void_p(x)
+    return ops.lib().sample_takeover(
+        vp(a["hidden"]), vp(a["W"]), a["M"], a["Hd"], a["V"], a["K"], vp(a["ws"]), a["wsb"],
+        vp(a["seq_ids"]), a["n_seq"], vp(a["cu"]), vp(a["driver"]), vp(a["ev"]),
+        vp(a["row_local"]), vp(a["u"]), a["eos"], vp(a["token"]), vp(a["fin"]), a["dtype"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(u=None), -1), (dict(token=None), -1), (dict(W=None), -1), (dict(n_seq=-1), -1),
+    (dict(K=33), -1), (dict(Hd=100), -2), (dict(dtype=5), -2), (dict(wsb=10), -3), (dict(ws=None), -3)])
+def test_sample_argument_errors(kw, status):
+    assert _sample(**kw) == status
+    assert ops.lib().ipdv_last_error().decode() != ""
+
+
+def test_sample_empty_batch_is_ok_without_gpu():
+    assert _sample(n_seq=0, u=None, token=None) == 0

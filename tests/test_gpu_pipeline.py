@@ -1,5 +1,6 @@
-"""End-to-end verify step on the GPU (attention -> LM head -> accept scan)
-against the oracle pipeline, per workload (scaled where the oracle needs it)."""
+"""End-to-end verify step on the GPU (attention -> LM head -> accept scan ->
+takeover draw) against the oracle pipeline, per workload (scaled where the
+oracle needs it)."""
 import numpy as np
 import pytest
 import torch
@@ -65,6 +66,37 @@ def _pipeline(cfg, seed):
     torch.cuda.synchronize()
     parity.compare_scan(g2, ref)
     np.testing.assert_array_equal(to_np(g2["src"]).astype(np.int64), ref["src"])
+    # the teacher's replacement at each takeover (from the scan above, whose
+    # event rows equal the oracle's), drawn by each verifier for its sequences
+    u = b.u_repl
+    fin0 = to_np(g2["finished"]).copy()
+    tok = torch.full((cfg.B,), -1, dtype=torch.int32, device=dev)
+    cu_dev = torch.from_numpy(b.cu_q.astype(np.int32)).to(dev)
+    logits_of = {}
+    for mi, m in enumerate(b.models):
+        if m.seq_ids.shape[0] == 0:
+            continue
+        rows = to_np(m.rows).astype(np.int64)
+        row_local = np.full(T, -1, np.int32)
+        row_local[rows] = np.arange(len(rows))
+        ws = torch.empty(ops.lmhead_workspace_size(m.hidden.shape[0], m.shape.hidden, m.shape.vocab, K),
+                         dtype=torch.uint8, device=dev)
+        ops.lmhead_logsoftmax_verify(m.hidden, m.W, prop_t[m.rows.long()].contiguous(), K,
+                                     workspace=ws)
+        ops.sample_takeover(m.hidden, m.W, K, ws, cu_dev,
+                            torch.from_numpy(b.driver.astype(np.uint8)).to(dev), g2["event_row"],
+                            torch.from_numpy(u).to(dev), b.eos_id, g2["finished"],
+                            row_local=torch.from_numpy(row_local).to(dev), seq_ids=m.seq_ids, token=tok)
+        for j, r in enumerate(rows):
+            logits_of[int(r)] = logits[mi][j]
+    torch.cuda.synchronize()
+    glog = np.stack([logits_of[r] for r in range(T)])
+    ref_d = oracle.sample_takeover(b.cu_q, b.driver, ref["event_row"], glog, u.astype(np.float64), b.eos_id)
+    n_draw = int((ref_d["token"] >= 0).sum())
+    exact = parity.check_takeover_draws(to_np(tok), to_np(g2["finished"]), fin0, ref_d,
+                                        lambda r: glog[r], b.cu_q, b.driver, ref["event_row"],
+                                        u.astype(np.float64), b.eos_id)
+    _say(f"  takeover draws: {n_draw}, {exact} above the margin compared exactly")
     _say(f"  scan: {n_cmp}/{cfg.B} sequences above the margin compared bit-exactly; "
          f"accepted {int(ref['n_acc'].sum())}/{T} drafts")
 
