@@ -1,6 +1,6 @@
 """Benchmark of one verify step (attention -> LM head -> accept scan) on MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 3] [--no-cpu]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload teacher-bf16] [--no-cpu]
     python bench.py --copy-calibration MIB   # reference copy for HBM counters
 
 A step is one pass of the whole verifier-side hot path over one synthetic
@@ -241,7 +241,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--config", type=int, default=3)
+    ap.add_argument("--workload", default="teacher-bf16", choices=sorted(inputs.WORKLOADS))
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -263,7 +263,7 @@ def main():
               file=sys.stderr)
         sys.exit(2)
     dev = torch.device("cuda:0")
-    cfg = inputs.CONFIGS[args.config]
+    cfg = inputs.WORKLOADS[args.workload]
     batch = inputs.make_batch(cfg, seed=args.seed, device=dev, poison=False)
     step = Step(batch, dev)
     for _ in range(args.warmup):
@@ -330,7 +330,7 @@ def main():
         "ms_per_step": round(ms, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16" if cfg.dtype == "bf16" else "f32", "data": "synthetic",
-        "config": {"workload": f"{cfg.name} (config {args.config}): B={cfg.B}, "
+        "config": {"workload": f"{cfg.name}: B={cfg.B}, "
                                f"ctx U[{cfg.ctx_lo},{cfg.ctx_hi}], k={list(cfg.k_choices)}, "
                                f"{'+'.join(f'{m.Hq}q/{m.Hkv}kv/D{m.D}' for m in cfg.models)}, "
                                f"hidden {cfg.models[0].hidden}, vocab {cfg.models[0].vocab}, K={cfg.K}",

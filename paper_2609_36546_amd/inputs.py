@@ -58,7 +58,7 @@ class ModelShape:
 class WorkloadConfig:
     """A verify-step workload: batch, shapes, lengths and proposal recipe."""
 
-    id: int
+    id: int                         # seed-stream id of the workload
     name: str
     dtype: str                      # "f32" or "bf16": storage/compute input type
     B: int
@@ -80,20 +80,20 @@ STUDENT = ModelShape("qwen3-1.7b-like", Hq=16, Hkv=8, D=128, hidden=2048, vocab=
 TEACHER = ModelShape("qwen3-30b-a3b-like", Hq=32, Hkv=4, D=128, hidden=2048, vocab=151936)
 TINY = ModelShape("tiny", Hq=4, Hkv=2, D=64, hidden=256, vocab=1024)
 
-CONFIGS = {
-    1: WorkloadConfig(1, "tiny-f32", "f32", B=2, models=(TINY,), page_size=16,
+WORKLOADS = {
+    "tiny-f32": WorkloadConfig(1, "tiny-f32", "f32", B=2, models=(TINY,), page_size=16,
                       k_choices=(4,), ctx_lo=128, ctx_hi=128, driver_rule="alt",
                       p_argmax=0.7, alt_mode="uniform"),
-    2: WorkloadConfig(2, "student-bf16", "bf16", B=32, models=(STUDENT,), page_size=16,
+    "student-bf16": WorkloadConfig(2, "student-bf16", "bf16", B=32, models=(STUDENT,), page_size=16,
                       k_choices=(8,), ctx_lo=512, ctx_hi=4096, driver_rule="T",
                       p_argmax=0.6, alt_mode="softmax", alt_temperature=1.5),
-    3: WorkloadConfig(3, "teacher-bf16", "bf16", B=64, models=(TEACHER,), page_size=16,
+    "teacher-bf16": WorkloadConfig(3, "teacher-bf16", "bf16", B=64, models=(TEACHER,), page_size=16,
                       k_choices=(8,), ctx_lo=1024, ctx_hi=8192, driver_rule="S",
                       p_argmax=0.6, alt_mode="softmax", alt_temperature=1.5),
-    4: WorkloadConfig(4, "long-teacher-bf16", "bf16", B=16, models=(TEACHER,), page_size=16,
+    "long-teacher-bf16": WorkloadConfig(4, "long-teacher-bf16", "bf16", B=16, models=(TEACHER,), page_size=16,
                       k_choices=(16,), ctx_lo=16384, ctx_hi=32768, driver_rule="S",
                       p_argmax=0.5, alt_mode="uniform", pool_tokens=2 * 1024 * 1024),
-    5: WorkloadConfig(5, "dual-cache-bf16", "bf16", B=128, models=(STUDENT, TEACHER),
+    "dual-cache-bf16": WorkloadConfig(5, "dual-cache-bf16", "bf16", B=128, models=(STUDENT, TEACHER),
                       page_size=16, k_choices=(1, 4, 8, 16), ctx_lo=256, ctx_hi=16384,
                       driver_rule="split64", p_argmax=0.6, alt_mode="softmax",
                       alt_temperature=1.5),

@@ -37,32 +37,35 @@ def _check_all(batch, mi=0):
 
 
 def test_tiny_fp32_config():
-    _check_all(_case(inputs.CONFIGS[1]))
+    _check_all(_case(inputs.WORKLOADS["tiny-f32"]))
 
 
-@pytest.mark.parametrize("cid,B,lo,hi", [(2, 5, 40, 1500), (3, 4, 100, 2600), (3, 3, 1, 40)])
-def test_scaled_bf16_configs(cid, B, lo, hi):
-    cfg = inputs.scaled(inputs.CONFIGS[cid], B=B, ctx_lo=lo, ctx_hi=hi,
-                        models=(inputs.scaled_shape(inputs.CONFIGS[cid].models[0], vocab=512, hidden=64),))
-    _check_all(_case(cfg, seed=cid))
+@pytest.mark.parametrize("name,B,lo,hi,seed", [("student-bf16", 5, 40, 1500, 2),
+                                               ("teacher-bf16", 4, 100, 2600, 3),
+                                               ("teacher-bf16", 3, 1, 40, 3)])
+def test_scaled_bf16_configs(name, B, lo, hi, seed):
+    base = inputs.WORKLOADS[name]
+    cfg = inputs.scaled(base, B=B, ctx_lo=lo, ctx_hi=hi,
+                        models=(inputs.scaled_shape(base.models[0], vocab=512, hidden=64),))
+    _check_all(_case(cfg, seed=seed))
 
 
 def test_long_window_two_row_groups():
     """k = 16 with 8 query heads per KV head: 128 packed rows, two row groups."""
-    cfg = inputs.scaled(inputs.CONFIGS[4], B=2, ctx_lo=3000, ctx_hi=5200, pool_tokens=None,
+    cfg = inputs.scaled(inputs.WORKLOADS["long-teacher-bf16"], B=2, ctx_lo=3000, ctx_hi=5200, pool_tokens=None,
                         models=(inputs.scaled_shape(inputs.TEACHER, vocab=512, hidden=64),))
     _check_all(_case(cfg, seed=4))
 
 
 @pytest.mark.parametrize("ps", [32, 64])
 def test_other_page_sizes(ps):
-    cfg = inputs.scaled(inputs.CONFIGS[3], B=3, ctx_lo=10, ctx_hi=900, page_size=ps,
+    cfg = inputs.scaled(inputs.WORKLOADS["teacher-bf16"], B=3, ctx_lo=10, ctx_hi=900, page_size=ps,
                         models=(inputs.scaled_shape(inputs.TEACHER, vocab=512, hidden=64),))
     _check_all(_case(cfg, seed=ps))
 
 
 def test_mixed_windows_and_two_models():
-    cfg = inputs.scaled(inputs.CONFIGS[5], B=10, ctx_lo=0, ctx_hi=700,
+    cfg = inputs.scaled(inputs.WORKLOADS["dual-cache-bf16"], B=10, ctx_lo=0, ctx_hi=700,
                         models=(inputs.scaled_shape(inputs.STUDENT, vocab=512, hidden=64),
                                 inputs.scaled_shape(inputs.TEACHER, vocab=512, hidden=64)))
     b = _case(cfg, seed=5)
@@ -72,13 +75,13 @@ def test_mixed_windows_and_two_models():
 
 def test_head_dim_64_bf16():
     shape = inputs.ModelShape("d64", Hq=8, Hkv=2, D=64, hidden=64, vocab=512)
-    cfg = inputs.scaled(inputs.CONFIGS[3], B=3, ctx_lo=5, ctx_hi=400, models=(shape,))
+    cfg = inputs.scaled(inputs.WORKLOADS["teacher-bf16"], B=3, ctx_lo=5, ctx_hi=400, models=(shape,))
     _check_all(_case(cfg, seed=64))
 
 
 def test_k1_equals_sequential_decode():
     """A k-token window equals k single-token verifies with append."""
-    cfg = inputs.scaled(inputs.CONFIGS[3], B=2, ctx_lo=200, ctx_hi=700,
+    cfg = inputs.scaled(inputs.WORKLOADS["teacher-bf16"], B=2, ctx_lo=200, ctx_hi=700,
                         models=(inputs.scaled_shape(inputs.TEACHER, vocab=512, hidden=64),))
     b = _case(cfg, seed=11)
     mdl = b.models[0]
@@ -108,7 +111,7 @@ def test_k1_equals_sequential_decode():
 def test_eviction_recompute_matches_cached_verify():
     """ctx_len = 0 and the whole prefix + window as rows: the last k rows equal
     the cached verify (Section 3.2.3, preemption recompute)."""
-    cfg = inputs.scaled(inputs.CONFIGS[3], B=1, ctx_lo=150, ctx_hi=150,
+    cfg = inputs.scaled(inputs.WORKLOADS["teacher-bf16"], B=1, ctx_lo=150, ctx_hi=150,
                         models=(inputs.scaled_shape(inputs.TEACHER, vocab=512, hidden=64),))
     b = _case(cfg, seed=12)
     mdl = b.models[0]
@@ -139,7 +142,7 @@ def test_eviction_recompute_matches_cached_verify():
 def test_full_size_teacher_config_sampled():
     """The full teacher workload (64 sequences, contexts up to 8192) in the
     launch configuration the benchmark times; the oracle checks 3 sequences."""
-    b = _case(inputs.CONFIGS[3], seed=0, poison=False)
+    b = _case(inputs.WORKLOADS["teacher-bf16"], seed=0, poison=False)
     mdl = b.models[0]
     out, _, _ = parity.run_gpu_attention(mdl, b)
     seqs = [int(np.argmax(b.ctx_lens)), int(np.argmin(b.ctx_lens)), 17]

@@ -102,16 +102,16 @@ def _pipeline(cfg, seed):
 
 
 def test_tiny_fp32_config():
-    _pipeline(inputs.CONFIGS[1], 0)
+    _pipeline(inputs.WORKLOADS["tiny-f32"], 0)
 
 
 def test_student_config_scaled():
-    _pipeline(inputs.scaled(inputs.CONFIGS[2], B=6, ctx_lo=64, ctx_hi=1200), 2)
+    _pipeline(inputs.scaled(inputs.WORKLOADS["student-bf16"], B=6, ctx_lo=64, ctx_hi=1200), 2)
 
 
 def test_teacher_config_scaled():
-    _pipeline(inputs.scaled(inputs.CONFIGS[3], B=5, ctx_lo=300, ctx_hi=2000), 3)
+    _pipeline(inputs.scaled(inputs.WORKLOADS["teacher-bf16"], B=5, ctx_lo=300, ctx_hi=2000), 3)
 
 
 def test_dual_cache_config_scaled():
-    _pipeline(inputs.scaled(inputs.CONFIGS[5], B=8, ctx_lo=20, ctx_hi=1000), 5)
+    _pipeline(inputs.scaled(inputs.WORKLOADS["dual-cache-bf16"], B=8, ctx_lo=20, ctx_hi=1000), 5)

@@ -6,12 +6,12 @@ from paper_2609_36546_amd import inputs
 from tests.workload import to_np
 
 
-def small(cfg_id, **kw):
-    return inputs.scaled(inputs.CONFIGS[cfg_id], **kw)
+def small(name, **kw):
+    return inputs.scaled(inputs.WORKLOADS[name], **kw)
 
 
 def test_tiny_config_structure_and_poison():
-    b = inputs.make_batch(inputs.CONFIGS[1], seed=0)
+    b = inputs.make_batch(inputs.WORKLOADS["tiny-f32"], seed=0)
     cfg = b.cfg
     assert b.T == 8 and list(b.k) == [4, 4] and list(b.ctx_lens) == [128, 128]
     assert list(b.driver) == [inputs.DRIVER_S, inputs.DRIVER_T]
@@ -34,8 +34,8 @@ def test_tiny_config_structure_and_poison():
 
 
 def test_seeded_and_reproducible():
-    a = inputs.make_batch(small(3, B=4, ctx_lo=20, ctx_hi=90, models=(inputs.TINY,)), seed=5)
-    b = inputs.make_batch(small(3, B=4, ctx_lo=20, ctx_hi=90, models=(inputs.TINY,)), seed=5)
+    a = inputs.make_batch(small("teacher-bf16", B=4, ctx_lo=20, ctx_hi=90, models=(inputs.TINY,)), seed=5)
+    b = inputs.make_batch(small("teacher-bf16", B=4, ctx_lo=20, ctx_hi=90, models=(inputs.TINY,)), seed=5)
     assert np.array_equal(a.ctx_lens, b.ctx_lens)
     assert torch.equal(a.models[0].q, b.models[0].q)
     assert torch.equal(a.models[0].W, b.models[0].W)
@@ -43,7 +43,7 @@ def test_seeded_and_reproducible():
 
 
 def test_dual_config_split_and_row_maps():
-    cfg = small(5, B=16, ctx_lo=16, ctx_hi=64,
+    cfg = small("dual-cache-bf16", B=16, ctx_lo=16, ctx_hi=64,
                 models=(inputs.scaled_shape(inputs.STUDENT, vocab=64, hidden=32),
                         inputs.scaled_shape(inputs.TEACHER, vocab=64, hidden=32)))
     b = inputs.make_batch(cfg, seed=0)
