@@ -18,8 +18,10 @@ What it computes, each part written from the paper's definitions:
   (logit descending, index ascending).
 * ``accept_scan`` -- the verdict stage (Section 3.2.3) applying the top-K
   coverage transition of Eq. (9) over a window with the EOS and maximum
-  length rules; ``eq9_stepper`` is a second, token-by-token writing of
-  Eq. (9) used to cross-check it.
+  length rules, and the rule variants named after Eq. (9) in Section 3.2.1
+  (entropy thresholds, asymmetric rules, SKD's fixed one-token handback);
+  ``eq9_stepper`` is a second, token-by-token writing of Eq. (9) used to
+  cross-check it.
 * ``sample_takeover`` -- the teacher's replacement token at a takeover
   (Eq. (9), second case: the uncovered student draft is discarded and the
   teacher samples a replacement from its own distribution at that position,
@@ -211,24 +213,69 @@ def lmhead_logsoftmax(hidden, W, prop_tok, K, logits=None):
 # Verdict stage: top-K coverage rule of Eq. (9) over a window
 # ---------------------------------------------------------------------------
 
-def accept_scan(cu_q, prop_tok, topk_idx, K, driver, ctx_lens, seq_lens, eos_id, max_len):
+# Takeover and handback rules (Section 3.2.1, after Eq. (9): the coverage
+# rules are the paper's default; an entropy threshold can replace either, the
+# two may differ, and SKD is coverage takeover with a fixed one-token handback).
+TAKE_COVERAGE = 0     # take over when the student's draft is outside the teacher's top-K
+TAKE_ENTROPY = 1      # take over when ent[row] > tau_take
+HAND_COVERAGE = 0     # hand back when the teacher's draft is inside the student's top-K
+HAND_FIXED_ONE = 1    # the teacher emits one token, then hands back (SKD)
+HAND_ENTROPY = 2      # hand back when ent[row] <= tau_hand
+
+
+def _rule_tests(row, tok, topk_row, K, take_rule, hand_rule, ent, tau_take, tau_hand):
+    """(takeover test, handback test) for one window row.
+
+    Coverage: the draft is among the verifier's K entries.  Entropy: a
+    threshold on the caller's per-row entropy (which model's entropy it is --
+    the paper allows either -- is the caller's choice); a NaN entropy passes
+    neither test.  Fixed one-token handback: every teacher token hands back.
+    """
+    covered = K > 0 and tok in [int(t) for t in topk_row[:K]]
+    if take_rule == TAKE_COVERAGE:
+        take = not covered
+    elif take_rule == TAKE_ENTROPY:
+        take = bool(float(ent[row]) > tau_take)
+    else:
+        raise ValueError("unknown takeover rule")
+    if hand_rule == HAND_COVERAGE:
+        hand = covered
+    elif hand_rule == HAND_FIXED_ONE:
+        hand = True
+    elif hand_rule == HAND_ENTROPY:
+        hand = bool(float(ent[row]) <= tau_hand)
+    else:
+        raise ValueError("unknown handback rule")
+    return take, hand
+
+
+def accept_scan(cu_q, prop_tok, topk_idx, K, driver, ctx_lens, seq_lens, eos_id, max_len,
+                take_rule=TAKE_COVERAGE, hand_rule=HAND_COVERAGE, ent=None,
+                tau_take=0.0, tau_hand=0.0):
     """Verdict for every sequence's window (Eq. (9), Section 3.2.3).
 
     Row i of sequence b scores draft i (``prop_tok[cu_q[b]+i]``), proposed by
-    the driver; covered_i = draft in the verifier's top-K at that row.
+    the driver.  With the default rules, take_i = the draft is not in the
+    verifier's top-K at that row and hand_i = it is (top-K coverage).
 
-    * Driver S (teacher verifies): drafts are accepted (source S) while
-      covered.  The first uncovered draft is a takeover: it is rejected, the
-      teacher will emit a replacement there (sampled later), and the next
-      driver is T.
+    * Driver S (teacher verifies): drafts are accepted (source S) until the
+      first row with take_i.  That row is a takeover: the draft is rejected,
+      the teacher will emit a replacement there (sampled later), and the next
+      driver is T -- or S under the fixed one-token handback, where the
+      replacement is the teacher's only token (SKD, Section 2).
     * Driver T (student verifies): drafts are accepted (source T).  The first
-      covered draft is a handback: it is kept, later drafts are discarded and
+      row with hand_i is a handback: it is kept, later drafts are discarded and
       the next driver is S.
-    * EOS: a student EOS ends the request only if covered (else takeover); a
-      teacher EOS is accepted and ends it.  Drafts after it are discarded.
+    * EOS: a student EOS ends the request only if it passes the takeover test
+      (else takeover); a teacher EOS is accepted and ends it.  Drafts after it
+      are discarded.
     * Length cap: draft i needs seq_len + i < max_len; a request whose
       accepted drafts reach max_len ends (a takeover's replacement is checked
       by the caller when it is sampled).
+
+    Rule variants (Section 3.2.1, after Eq. (9)): ``take_rule`` and
+    ``hand_rule`` pick the tests independently (asymmetric rules), with
+    ``ent[row]`` and the thresholds for the entropy rules.
 
     Returns arrays: n_acc, event_row (-1: no transition), next_driver,
     finished, new_cache_len, and src[T] (0 S, 1 T, 255 discarded).
@@ -238,6 +285,8 @@ def accept_scan(cu_q, prop_tok, topk_idx, K, driver, ctx_lens, seq_lens, eos_id,
     cu_q = np.asarray(cu_q, np.int64)
     B = len(cu_q) - 1
     T = int(cu_q[-1])
+    if (take_rule == TAKE_ENTROPY or hand_rule == HAND_ENTROPY) and ent is None:
+        raise ValueError("an entropy rule needs ent")
     n_acc = np.zeros(B, np.int64)
     event_row = np.full(B, -1, np.int64)
     next_driver = np.asarray(driver, np.int64).copy()
@@ -254,11 +303,12 @@ def accept_scan(cu_q, prop_tok, topk_idx, K, driver, ctx_lens, seq_lens, eos_id,
                 finished[b] = 1
                 break
             tok = int(prop_tok[row])
-            covered = K > 0 and tok in [int(t) for t in topk_idx[row][:K]]
+            take, hand = _rule_tests(row, tok, topk_idx[row], K, take_rule, hand_rule, ent,
+                                     tau_take, tau_hand)
             if drv == DRIVER_S:
-                if not covered:
+                if take:
                     event_row[b] = i
-                    next_driver[b] = DRIVER_T
+                    next_driver[b] = DRIVER_S if hand_rule == HAND_FIXED_ONE else DRIVER_T
                     takeover = True
                     break
                 src[row] = SRC_S
@@ -267,10 +317,10 @@ def accept_scan(cu_q, prop_tok, topk_idx, K, driver, ctx_lens, seq_lens, eos_id,
             else:
                 src[row] = SRC_T
                 n_acc[b] = i + 1
-                if covered:
+                if hand:
                     event_row[b] = i
                     next_driver[b] = DRIVER_S
-                stop = covered or tok == eos_id
+                stop = hand or tok == eos_id
             if tok == eos_id or int(seq_lens[b]) + n_acc[b] >= int(max_len):
                 finished[b] = 1
                 stop = True
@@ -284,7 +334,8 @@ def accept_scan(cu_q, prop_tok, topk_idx, K, driver, ctx_lens, seq_lens, eos_id,
 REPLACEMENT = -1   # placeholder for the teacher's replacement token
 
 
-def eq9_stepper(drafts, verifier_topk, K, m1, eos_id, room):
+def eq9_stepper(drafts, verifier_topk, K, m1, eos_id, room, take_rule=TAKE_COVERAGE,
+                hand_rule=HAND_COVERAGE, ent=None, tau_take=0.0, tau_hand=0.0):
     """Token-by-token iteration of Eq. (9) over one window (second writing).
 
     ``drafts[t]`` is the driver's proposal at step t and ``verifier_topk[t]``
@@ -293,6 +344,13 @@ def eq9_stepper(drafts, verifier_topk, K, m1, eos_id, room):
     old driver, so the walk stops as soon as the driver changes, at an
     emitted EOS, or when ``room`` tokens have been emitted.  A takeover emits
     the placeholder REPLACEMENT (the teacher samples it later).
+
+    Rule variants (Section 3.2.1, after Eq. (9)): case 2 fires on the
+    takeover test and case 3 on the handback test of ``take_rule`` /
+    ``hand_rule`` (coverage by default; ``ent[t]`` for the entropy rules).
+    Under the fixed one-token handback (SKD), the teacher's replacement is its
+    only token: case 2 then hands control straight back (m_{t+1} = S), and a
+    teacher-driven step always takes case 3.
 
     Returns (emitted tokens, their sources, final driver, finished flag).
     """
@@ -304,17 +362,28 @@ def eq9_stepper(drafts, verifier_topk, K, m1, eos_id, room):
             finished = True
             break
         in_support = x_tilde in list(verifier_topk[t])[:K] if K > 0 else False
-        if m == DRIVER_S and in_support:           # case 1
+        if take_rule == TAKE_COVERAGE:
+            take = not in_support
+        else:
+            take = ent[t] > tau_take
+        if hand_rule == HAND_COVERAGE:
+            hand = in_support
+        elif hand_rule == HAND_FIXED_ONE:
+            hand = True
+        else:
+            hand = ent[t] <= tau_hand
+        if m == DRIVER_S and not take:             # case 1
             x, z, m_next = x_tilde, SRC_S, DRIVER_S
         elif m == DRIVER_S:                        # case 2: takeover
-            x, z, m_next = REPLACEMENT, SRC_T, DRIVER_T
-        elif in_support:                           # case 3: handback
+            x, z = REPLACEMENT, SRC_T
+            m_next = DRIVER_S if hand_rule == HAND_FIXED_ONE else DRIVER_T
+        elif hand:                                 # case 3: handback
             x, z, m_next = x_tilde, SRC_T, DRIVER_S
         else:                                      # case 4
             x, z, m_next = x_tilde, SRC_T, DRIVER_T
         xs.append(x)
         zs.append(z)
-        changed = m_next != m
+        changed = m_next != m or x == REPLACEMENT
         m = m_next
         if x == eos_id or (x != REPLACEMENT and len(xs) >= room):
             finished = True
