@@ -243,6 +243,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="teacher-bf16", choices=sorted(inputs.WORKLOADS))
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--K", type=int, default=None,
+                    help="top-K coverage width (default: the workload's, 16); the coverage-width "
+                         "ablation sweeps 4, 8, 16, 32")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only copy MIB MiB device-to-device 5 times (a kernel of known "
@@ -264,6 +267,8 @@ def main():
         sys.exit(2)
     dev = torch.device("cuda:0")
     cfg = inputs.WORKLOADS[args.workload]
+    if args.K is not None:
+        cfg = inputs.scaled(cfg, K=args.K)
     batch = inputs.make_batch(cfg, seed=args.seed, device=dev, poison=False)
     step = Step(batch, dev)
     for _ in range(args.warmup):

@@ -18,6 +18,9 @@
  *                               Eq. (9) applied as a first-event scan over each
  *                               window, with the EOS and length rules and the
  *                               rollback length shared by both caches;
+ *   accept_scan_rule         -- the same scan with the rule variants named
+ *                               after Eq. (9) (entropy thresholds, asymmetric
+ *                               rules, SKD's fixed one-token handback);
  *   sample_takeover          -- the teacher's replacement token at each
  *                               takeover (Eq. (9), second case), drawn from
  *                               the verifier's distribution at that row.
@@ -69,6 +72,16 @@ typedef enum { IPDV_F32 = 0, IPDV_BF16 = 1 } ipdv_dtype;
 /* Driver codes (accept_scan): who proposed the window. */
 #define IPDV_DRIVER_S 0   /* the student drives; the teacher verifies */
 #define IPDV_DRIVER_T 1   /* the teacher drives; the student verifies */
+
+/* Takeover and handback rules (accept_scan_rule), Section 3.2.1 after
+ * Eq. (9): top-K coverage is the paper's rule for both; an entropy threshold
+ * may replace either test, and the two may differ.  SKD is coverage takeover
+ * with a fixed one-token handback. */
+#define IPDV_TAKE_COVERAGE 0   /* take over when the draft is outside the verifier's top-K */
+#define IPDV_TAKE_ENTROPY 1    /* take over when ent[row] > tau_take */
+#define IPDV_HAND_COVERAGE 0   /* hand back when the draft is inside the verifier's top-K */
+#define IPDV_HAND_FIXED_ONE 1  /* the teacher emits one token, then hands back (SKD) */
+#define IPDV_HAND_ENTROPY 2    /* hand back when ent[row] <= tau_hand */
 
 /* Source labels (accept_scan `src`). */
 #define IPDV_SRC_S 0
@@ -223,6 +236,43 @@ int accept_scan(const int32_t* cu_q, const int32_t* prop_tok,
                 void* hip_stream);
 
 /*
+ * accept_scan_rule -- accept_scan with the rule variants named after Eq. (9)
+ * in Section 3.2.1 (SKD's behaviour as described in Section 2).
+ *
+ * take_rule (IPDV_TAKE_*) replaces the "uncovered" test of a student-driven
+ * window and hand_rule (IPDV_HAND_*) the "covered" test of a teacher-driven
+ * one; every other rule of accept_scan (first event ends the window, EOS,
+ * length cap, cache lengths, source labels) is unchanged, with "covered"
+ * read as "passes the takeover test" for a student EOS.
+ *   IPDV_TAKE_ENTROPY: row i takes over when ent[row] > tau_take.
+ *   IPDV_HAND_ENTROPY: row i hands back when ent[row] <= tau_hand.
+ *     ent [T] float32 is a per-row entropy chosen by the caller (the paper
+ *     allows the student's or the teacher's; e.g. the `entropy` output of
+ *     lmhead_logsoftmax_verify for the verifier's).  Comparisons are IEEE: a
+ *     NaN entropy passes neither test.
+ *   IPDV_HAND_FIXED_ONE: a teacher-driven window keeps its first draft and
+ *     hands back at row 0; a takeover's next driver stays S, since the
+ *     replacement is the teacher's only token (SKD: the teacher resamples the
+ *     rejected position and the student resumes).
+ * With IPDV_TAKE_COVERAGE and IPDV_HAND_COVERAGE it equals accept_scan.
+ *
+ * ent may be NULL unless an entropy rule is selected; topk_idx may be NULL
+ * when K = 0 or no coverage rule is selected.
+ *
+ * Errors: those of accept_scan, and IPDV_EINVAL for an unknown rule or a
+ * NULL ent under an entropy rule.
+ */
+int accept_scan_rule(const int32_t* cu_q, const int32_t* prop_tok,
+                     const int32_t* topk_idx, int K,
+                     const uint8_t* driver, const int32_t* ctx_lens, const int32_t* seq_lens,
+                     int32_t eos_id, int32_t max_len, int B,
+                     int take_rule, int hand_rule, const float* ent,
+                     float tau_take, float tau_hand,
+                     int32_t* n_acc, int32_t* event_row, uint8_t* next_driver,
+                     uint8_t* finished, int32_t* new_cache_len, uint8_t* src,
+                     void* hip_stream);
+
+/*
  * sample_takeover -- the teacher's replacement token at a takeover (Eq. (9),
  * second case: the uncovered student draft is discarded and the teacher
  * samples a replacement from its own distribution q(. | c_t) at that position;
@@ -273,7 +323,7 @@ int sample_takeover(const void* hidden, const void* W, int M, int Hd, int V, int
  * ipdv_trace_count() returns how many events have been recorded since the
  * hook was last set.  Kernels per call: verify_attn_paged 3 (append,
  * attention, split combine), lmhead_logsoftmax_verify 2 (GEMM + epilogue,
- * merge), accept_scan 1, sample_takeover 1.
+ * merge), accept_scan 1, accept_scan_rule 1, sample_takeover 1.
  */
 int ipdv_trace_events(void* const* events, int capacity);
 int ipdv_trace_count(void);

@@ -194,22 +194,43 @@ int sample_takeover(const void* hidden, const void* W, int M, int Hd, int V, int
   return ok();
 }
 
+int accept_scan_rule(const int32_t* cu_q, const int32_t* prop_tok, const int32_t* topk_idx,
+                     int K, const uint8_t* driver, const int32_t* ctx_lens,
+                     const int32_t* seq_lens, int32_t eos_id, int32_t max_len, int B,
+                     int take_rule, int hand_rule, const float* ent, float tau_take,
+                     float tau_hand, int32_t* n_acc, int32_t* event_row, uint8_t* next_driver,
+                     uint8_t* finished, int32_t* new_cache_len, uint8_t* src, void* hip_stream) {
+  if (B < 0) return fail(IPDV_EINVAL, "B must be >= 0 (got %d)", B);
+  if (K < 0 || K > IPDV_MAX_K) return fail(IPDV_EINVAL, "K=%d must be in [0, %d]", K, IPDV_MAX_K);
+  if (take_rule != IPDV_TAKE_COVERAGE && take_rule != IPDV_TAKE_ENTROPY)
+    return fail(IPDV_EINVAL, "unknown takeover rule %d", take_rule);
+  if (hand_rule != IPDV_HAND_COVERAGE && hand_rule != IPDV_HAND_FIXED_ONE &&
+      hand_rule != IPDV_HAND_ENTROPY)
+    return fail(IPDV_EINVAL, "unknown handback rule %d", hand_rule);
+  if (B == 0) return ok();
+  const bool uses_cov = take_rule == IPDV_TAKE_COVERAGE || hand_rule == IPDV_HAND_COVERAGE;
+  const bool uses_ent = take_rule == IPDV_TAKE_ENTROPY || hand_rule == IPDV_HAND_ENTROPY;
+  if (!cu_q || !prop_tok || (K > 0 && uses_cov && !topk_idx) || !driver || !ctx_lens ||
+      !seq_lens || !n_acc || !event_row || !next_driver || !finished || !new_cache_len || !src)
+    return fail(IPDV_EINVAL, "null required pointer");
+  if (uses_ent && !ent) return fail(IPDV_EINVAL, "an entropy rule needs ent");
+  ipdv::ScanLaunch L{cu_q, prop_tok, topk_idx, K, driver, ctx_lens, seq_lens, eos_id, max_len,
+                     B, n_acc, event_row, next_driver, finished, new_cache_len, src,
+                     take_rule, hand_rule, ent, tau_take, tau_hand};
+  hipError_t e = ipdv::launch_accept_scan(L, reinterpret_cast<hipStream_t>(hip_stream));
+  if (e != hipSuccess) return hip_fail("accept_scan launch", e);
+  return ok();
+}
+
 int accept_scan(const int32_t* cu_q, const int32_t* prop_tok, const int32_t* topk_idx, int K,
                 const uint8_t* driver, const int32_t* ctx_lens, const int32_t* seq_lens,
                 int32_t eos_id, int32_t max_len, int B, int32_t* n_acc, int32_t* event_row,
                 uint8_t* next_driver, uint8_t* finished, int32_t* new_cache_len, uint8_t* src,
                 void* hip_stream) {
-  if (B < 0) return fail(IPDV_EINVAL, "B must be >= 0 (got %d)", B);
-  if (K < 0 || K > IPDV_MAX_K) return fail(IPDV_EINVAL, "K=%d must be in [0, %d]", K, IPDV_MAX_K);
-  if (B == 0) return ok();
-  if (!cu_q || !prop_tok || (K > 0 && !topk_idx) || !driver || !ctx_lens || !seq_lens || !n_acc ||
-      !event_row || !next_driver || !finished || !new_cache_len || !src)
-    return fail(IPDV_EINVAL, "null required pointer");
-  ipdv::ScanLaunch L{cu_q, prop_tok, topk_idx, K, driver, ctx_lens, seq_lens, eos_id, max_len,
-                     B, n_acc, event_row, next_driver, finished, new_cache_len, src};
-  hipError_t e = ipdv::launch_accept_scan(L, reinterpret_cast<hipStream_t>(hip_stream));
-  if (e != hipSuccess) return hip_fail("accept_scan launch", e);
-  return ok();
+  return accept_scan_rule(cu_q, prop_tok, topk_idx, K, driver, ctx_lens, seq_lens, eos_id,
+                          max_len, B, IPDV_TAKE_COVERAGE, IPDV_HAND_COVERAGE, nullptr, 0.f, 0.f,
+                          n_acc, event_row, next_driver, finished, new_cache_len, src,
+                          hip_stream);
 }
 
 }  // extern "C"

@@ -1,5 +1,8 @@
 // Verdict stage for gfx950: the top-K coverage rule of Eq. (9) applied to each
-// sequence's window as a first-event scan (Section 3.2.3, verdict stage).
+// sequence's window as a first-event scan (Section 3.2.3, verdict stage), and
+// the rule variants named after Eq. (9) in Section 3.2.1: an entropy
+// threshold in place of either coverage test, the two chosen independently,
+// and SKD's fixed one-token handback.
 //
 // One wave per sequence.  Lane i tests row i of the window in parallel
 // (is the draft in the verifier's top-K; is it EOS; does it fit under the
@@ -27,6 +30,9 @@ struct ScanParams {
   uint8_t* finished;
   int32_t* new_cache_len;
   uint8_t* src;
+  int take_rule, hand_rule;
+  const float* ent;
+  float tau_take, tau_hand;
 };
 
 __global__ __launch_bounds__(256) void accept_scan_kernel(ScanParams p) {
@@ -43,37 +49,48 @@ __global__ __launch_bounds__(256) void accept_scan_kernel(ScanParams p) {
   for (int i0 = 0; i0 < kb; i0 += kWave) {
     const int i = i0 + lane;
     const bool valid = i < kb;
-    bool covered = false, is_eos = false;
+    bool take = false, hand = false, is_eos = false;
     if (valid) {
       const int row = r0 + i;
       const int tok = p.prop_tok[row];
-      const int32_t* tk = p.topk_idx + (size_t)row * p.K;
-      for (int kk = 0; kk < p.K; ++kk) covered |= (tk[kk] == tok);
+      // coverage: the draft among the verifier's K entries (K = 0: none)
+      bool covered = false;
+      if (p.take_rule == IPDV_TAKE_COVERAGE_DEV || p.hand_rule == IPDV_HAND_COVERAGE_DEV) {
+        const int32_t* tk = p.topk_idx + (size_t)row * p.K;
+        for (int kk = 0; kk < p.K; ++kk) covered |= (tk[kk] == tok);
+      }
+      // entropy thresholds compare as IEEE floats: a NaN passes neither test
+      const float e = (p.take_rule == IPDV_TAKE_ENTROPY_DEV || p.hand_rule == IPDV_HAND_ENTROPY_DEV)
+                          ? p.ent[row] : 0.f;
+      take = p.take_rule == IPDV_TAKE_COVERAGE_DEV ? !covered : e > p.tau_take;
+      hand = p.hand_rule == IPDV_HAND_COVERAGE_DEV ? covered
+             : p.hand_rule == IPDV_HAND_FIXED_ONE_DEV ? true : e <= p.tau_hand;
       is_eos = tok == p.eos_id;
     }
     const bool allowed = seq_len + i < max_len;
     const bool cap_after = seq_len + i + 1 >= max_len;
     bool stop;
-    if (drv == IPDV_DRIVER_S_DEV) stop = !allowed || !covered || is_eos || cap_after;
-    else stop = !allowed || covered || is_eos || cap_after;
+    if (drv == IPDV_DRIVER_S_DEV) stop = !allowed || take || is_eos || cap_after;
+    else stop = !allowed || hand || is_eos || cap_after;
     const unsigned long long mask = __ballot(valid && stop);
     if (mask == 0) continue;
     const int first = __builtin_ctzll(mask);
     const int fi = i0 + first;
     const bool f_allowed = __shfl(allowed ? 1 : 0, first, kWave);
-    const bool f_cov = __shfl(covered ? 1 : 0, first, kWave);
+    const bool f_take = __shfl(take ? 1 : 0, first, kWave);
+    const bool f_hand = __shfl(hand ? 1 : 0, first, kWave);
     const bool f_eos = __shfl(is_eos ? 1 : 0, first, kWave);
     const bool f_cap = __shfl(cap_after ? 1 : 0, first, kWave);
     if (!f_allowed) {
       n_acc = fi;
       fin = 1;
-    } else if (drv == IPDV_DRIVER_S_DEV && !f_cov) {
+    } else if (drv == IPDV_DRIVER_S_DEV && f_take) {
       n_acc = fi;
       event = fi;
       takeover = 1;
     } else {
       n_acc = fi + 1;
-      if (drv != IPDV_DRIVER_S_DEV && f_cov) event = fi;
+      if (drv != IPDV_DRIVER_S_DEV && f_hand) event = fi;
       fin = (f_eos || f_cap) ? 1 : 0;
     }
     break;
@@ -83,7 +100,10 @@ __global__ __launch_bounds__(256) void accept_scan_kernel(ScanParams p) {
   if (lane == 0) {
     p.n_acc[b] = n_acc;
     p.event_row[b] = event;
-    p.next_driver[b] = event >= 0 ? (uint8_t)(1 - drv) : (uint8_t)drv;
+    // an event flips the driver, except a takeover under the fixed one-token
+    // handback: the replacement is the teacher's only token (SKD)
+    const bool flip = event >= 0 && !(takeover && p.hand_rule == IPDV_HAND_FIXED_ONE_DEV);
+    p.next_driver[b] = flip ? (uint8_t)(1 - drv) : (uint8_t)drv;
     p.finished[b] = (uint8_t)fin;
     p.new_cache_len[b] = p.ctx_lens[b] + n_acc + takeover;
   }
@@ -95,7 +115,8 @@ hipError_t launch_accept_scan(const ScanLaunch& L, hipStream_t st) {
   if (L.B == 0) return hipSuccess;
   ScanParams p{L.cu_q, L.prop_tok, L.topk_idx, L.K, L.driver, L.ctx_lens, L.seq_lens,
                L.eos_id, L.max_len, L.B, L.n_acc, L.event_row, L.next_driver, L.finished,
-               L.new_cache_len, L.src};
+               L.new_cache_len, L.src, L.take_rule, L.hand_rule, L.ent, L.tau_take,
+               L.tau_hand};
   trace_begin(st);
   hipLaunchKernelGGL(accept_scan_kernel, dim3((L.B + 3) / 4), dim3(256), 0, st, p);
   hipError_t e = hipGetLastError();

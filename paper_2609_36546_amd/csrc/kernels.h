@@ -7,6 +7,11 @@
 
 #define IPDV_MAX_K_DEV 32
 #define IPDV_DRIVER_S_DEV 0
+#define IPDV_TAKE_COVERAGE_DEV 0
+#define IPDV_TAKE_ENTROPY_DEV 1
+#define IPDV_HAND_COVERAGE_DEV 0
+#define IPDV_HAND_FIXED_ONE_DEV 1
+#define IPDV_HAND_ENTROPY_DEV 2
 
 namespace ipdv {
 
@@ -110,6 +115,10 @@ struct ScanLaunch {
   uint8_t* finished;
   int32_t* new_cache_len;
   uint8_t* src;
+  // rule variants (IPDV_TAKE_*, IPDV_HAND_*); ent is read only by the entropy rules
+  int take_rule = 0, hand_rule = 0;
+  const float* ent = nullptr;
+  float tau_take = 0.f, tau_hand = 0.f;
 };
 
 hipError_t launch_accept_scan(const ScanLaunch& L, hipStream_t st);

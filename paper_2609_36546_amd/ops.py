@@ -55,6 +55,10 @@ def lib() -> ctypes.CDLL:
         L.accept_scan.argtypes = [i32p, i32p, i32p, ci, u8p, i32p, i32p, ctypes.c_int32,
                                   ctypes.c_int32, ci, i32p, i32p, u8p, u8p, i32p, u8p, vp]
         L.accept_scan.restype = ci
+        L.accept_scan_rule.argtypes = [i32p, i32p, i32p, ci, u8p, i32p, i32p, ctypes.c_int32,
+                                       ctypes.c_int32, ci, ci, ci, f32p, ctypes.c_float,
+                                       ctypes.c_float, i32p, i32p, u8p, u8p, i32p, u8p, vp]
+        L.accept_scan_rule.restype = ci
         L.sample_takeover.argtypes = [vp, vp, ci, ci, ci, ci, vp, cs, i32p, ci, i32p, u8p, i32p,
                                       i32p, f32p, ctypes.c_int32, i32p, u8p, ci, vp]
         L.sample_takeover.restype = ci
@@ -242,12 +246,32 @@ def accept_scan(cu_q, prop_tok, topk_idx, K: int, driver, ctx_lens, seq_lens, eo
                 max_len: int, outs=None):
     """Verdict for each sequence's window (see include/ipdv.h).  Returns dict
     n_acc, event_row, next_driver, finished, new_cache_len, src."""
+    return accept_scan_rule(cu_q, prop_tok, topk_idx, K, driver, ctx_lens, seq_lens, eos_id,
+                            max_len, outs=outs, _entry="accept_scan")
+
+
+TAKE_COVERAGE, TAKE_ENTROPY = 0, 1
+HAND_COVERAGE, HAND_FIXED_ONE, HAND_ENTROPY = 0, 1, 2
+
+
+def accept_scan_rule(cu_q, prop_tok, topk_idx, K: int, driver, ctx_lens, seq_lens, eos_id: int,
+                     max_len: int, take_rule: int = TAKE_COVERAGE, hand_rule: int = HAND_COVERAGE,
+                     ent=None, tau_take: float = 0.0, tau_hand: float = 0.0, outs=None,
+                     _entry="accept_scan_rule"):
+    """Verdict with the takeover / handback rule variants (see
+    include/ipdv.h, accept_scan_rule).  ``ent`` is a [T] float32 entropy per
+    row, needed by the entropy rules."""
     dev = cu_q.device
     _need(cu_q, "cu_q", torch.int32, dev, 1)
     B = cu_q.shape[0] - 1
     _need(prop_tok, "prop_tok", torch.int32, dev, 1)
     T = prop_tok.shape[0]
-    if K > 0:
+    uses_ent = take_rule == TAKE_ENTROPY or hand_rule == HAND_ENTROPY
+    if uses_ent:
+        _need(ent, "ent", torch.float32, dev, 1)
+        if ent.shape[0] != T:
+            raise ValueError("ent must be [T]")
+    if K > 0 and topk_idx is not None:
         _need(topk_idx, "topk_idx", torch.int32, dev, 2)
         if topk_idx.shape[0] != T or topk_idx.shape[1] != K:
             raise ValueError("topk_idx must be [T, K]")
@@ -263,12 +287,21 @@ def accept_scan(cu_q, prop_tok, topk_idx, K: int, driver, ctx_lens, seq_lens, eo
             "new_cache_len": torch.empty(B, dtype=torch.int32, device=dev),
             "src": torch.empty(T, dtype=torch.uint8, device=dev),
         }
-    st = lib().accept_scan(
-        _ptr(cu_q), _ptr(prop_tok), _ptr(topk_idx) if K > 0 else None, K, _ptr(driver),
-        _ptr(ctx_lens), _ptr(seq_lens), int(eos_id), int(max_len), B,
-        _ptr(outs["n_acc"]), _ptr(outs["event_row"]), _ptr(outs["next_driver"]),
-        _ptr(outs["finished"]), _ptr(outs["new_cache_len"]), _ptr(outs["src"]), _stream(dev))
-    _check("accept_scan", st)
+    tk = _ptr(topk_idx) if (K > 0 and topk_idx is not None) else None
+    if _entry == "accept_scan":
+        st = lib().accept_scan(
+            _ptr(cu_q), _ptr(prop_tok), tk, K, _ptr(driver), _ptr(ctx_lens), _ptr(seq_lens),
+            int(eos_id), int(max_len), B, _ptr(outs["n_acc"]), _ptr(outs["event_row"]),
+            _ptr(outs["next_driver"]), _ptr(outs["finished"]), _ptr(outs["new_cache_len"]),
+            _ptr(outs["src"]), _stream(dev))
+    else:
+        st = lib().accept_scan_rule(
+            _ptr(cu_q), _ptr(prop_tok), tk, K, _ptr(driver), _ptr(ctx_lens), _ptr(seq_lens),
+            int(eos_id), int(max_len), B, int(take_rule), int(hand_rule),
+            _ptr(ent) if uses_ent else None, float(tau_take), float(tau_hand),
+            _ptr(outs["n_acc"]), _ptr(outs["event_row"]), _ptr(outs["next_driver"]),
+            _ptr(outs["finished"]), _ptr(outs["new_cache_len"]), _ptr(outs["src"]), _stream(dev))
+    _check(_entry, st)
     return outs
 
 

@@ -19,9 +19,10 @@ def declared_functions():
                   {"sizeof", "defined", "if", "extern"})
 
 
-def test_header_declares_the_three_entry_points():
+def test_header_declares_the_entry_points():
     names = declared_functions()
-    for n in ("verify_attn_paged", "lmhead_logsoftmax_verify", "accept_scan"):
+    for n in ("verify_attn_paged", "lmhead_logsoftmax_verify", "accept_scan", "accept_scan_rule",
+              "sample_takeover"):
         assert n in names
 
 
@@ -107,6 +108,24 @@ def test_scan_argument_errors():
     empty = list(args)
     empty[9] = 0
     assert L.accept_scan(*empty) == 0
+
+
+def test_scan_rule_argument_errors():
+    L = ops.lib()
+    vp = ctypes.c_void_p
+
+    def args(take=0, hand=0, ent=vp(1), topk=vp(1), B=3):
+        return ([vp(1), vp(1), topk, 4, vp(1), vp(1), vp(1), 0, 100, B, take, hand, ent,
+                 0.5, 0.5] + [vp(1)] * 6 + [None])
+    assert L.accept_scan_rule(*args(take=2)) == -1            # unknown takeover rule
+    assert L.accept_scan_rule(*args(hand=3)) == -1            # unknown handback rule
+    assert L.accept_scan_rule(*args(take=-1)) == -1
+    assert L.accept_scan_rule(*args(take=1, ent=None)) == -1  # entropy rule without ent
+    assert L.accept_scan_rule(*args(hand=2, ent=None)) == -1
+    assert L.accept_scan_rule(*args(topk=None)) == -1         # coverage rule, K > 0, no top-K
+    # rules are validated before the empty-batch shortcut
+    assert L.accept_scan_rule(*args(take=5, B=0)) == -1
+    assert L.accept_scan_rule(*args(take=1, hand=2, B=0)) == 0
 
 
 def test_lmhead_vocab_limit():
