@@ -9,4 +9,7 @@ from .ipdv_oracle import (  # noqa: F401
     append_window, gather_sequence, attention_rows, verify_attention,
     verify_attn_paged, logits_fp64, lmhead_logsoftmax, accept_scan, eq9_stepper,
     sample_categorical, sample_takeover,
+    SUPPORT_UNION, SUPPORT_STUDENT, SUPPORT_TEACHER, SUPPORT_INTERSECTION,
+    LOSS_IPD_SPLIT, LOSS_PURE_REVERSE, LOSS_PURE_FORWARD, LOSS_INVERSE_SPLIT,
+    logp_gather, source_split_kl, source_split_kl_lists,
 )

@@ -27,6 +27,12 @@ What it computes, each part written from the paper's definitions:
   teacher samples a replacement from its own distribution at that position,
   temperature 1), drawn by inverse CDF over the vocabulary in index order
   from a caller-supplied uniform.
+* ``source_split_kl`` -- the per-position values of the source-split
+  objective (Section 3.2.2): both models renormalised on the top-K support
+  (Eqs. (5), (6)), reverse KL at student-generated positions and forward KL
+  at teacher-generated ones (Eq. (10)), the length-normalised sum per
+  trajectory (Eq. (11)), the top-K overlap ratio and the intervention ratio;
+  ``logp_gather`` gives each model's log-probs at the other's top-K indices.
 
 Readings where the paper is silent (tie-break, window/row alignment, cache
 rollback lengths, EOS inside a window, length cap) are listed in the
@@ -438,3 +444,179 @@ def sample_takeover(cu_q, driver, event_row, logits, u, eos_id):
         token[b], margin[b] = sample_categorical(logits[r], float(u[b]))
         eos[b] = token[b] == eos_id
     return {"token": token, "eos": eos, "margin": margin}
+
+
+# ---------------------------------------------------------------------------
+# Source-split KL values on the top-K support (Eqs. (5), (6), (10), (11))
+# ---------------------------------------------------------------------------
+
+# Distillation support S_t (Eq. (5) and the text after it; Appendix B.2: the
+# union is the paper's default).
+SUPPORT_UNION = 0
+SUPPORT_STUDENT = 1
+SUPPORT_TEACHER = 2
+SUPPORT_INTERSECTION = 3
+# KL direction per token source (Eq. (10) is the default; Section 4.3 ablates
+# the other three).
+LOSS_IPD_SPLIT = 0       # reverse KL where z = S, forward KL where z = T
+LOSS_PURE_REVERSE = 1
+LOSS_PURE_FORWARD = 2
+LOSS_INVERSE_SPLIT = 3   # forward KL where z = S, reverse KL where z = T
+
+
+def logp_gather(hidden, W, idx, logits=None):
+    """log-softmax of the row's logits at the given vocabulary indices.
+
+    ``idx [M, n]``; entries outside [0, V) give -inf.  Each model's log-probs
+    at the other model's top-K indices complete the union support of Eq. (6).
+    """
+    l = logits_fp64(hidden, W) if logits is None else _f64(logits)
+    M, V = l.shape
+    mx = l.max(axis=1)
+    lse = mx + np.log(np.exp(l - mx[:, None]).sum(axis=1))
+    idx = np.asarray(idx, np.int64)
+    out = np.full(idx.shape, -np.inf)
+    for m in range(M):
+        for j, v in enumerate(idx[m]):
+            if 0 <= v < V:
+                out[m, j] = l[m, v] - lse[m]
+    return out
+
+
+def _topk_set(logp_row, K):
+    """Top_K of Eq. (5): the first K of a stable sort by log-prob descending
+    (equal values: lower index first)."""
+    return [int(v) for v in np.argsort(-logp_row, kind="stable")[:K]]
+
+
+def _support(Sp, Sq, support):
+    if support == SUPPORT_UNION:
+        return Sp + [v for v in Sq if v not in Sp]
+    if support == SUPPORT_STUDENT:
+        return list(Sp)
+    if support == SUPPORT_TEACHER:
+        return list(Sq)
+    if support == SUPPORT_INTERSECTION:
+        return [v for v in Sp if v in Sq]
+    raise ValueError("unknown support")
+
+
+def _kl_pair(lp, lq):
+    """(D(pi_bar || q_bar), D(q_bar || pi_bar)) of Eq. (6)'s renormalised
+    distributions from log-probs on the support; an empty support gives 0."""
+    lp = np.asarray(lp, np.float64)
+    lq = np.asarray(lq, np.float64)
+    if lp.size == 0:
+        return 0.0, 0.0
+    a = lp - (lp.max() + np.log(np.exp(lp - lp.max()).sum()))   # log pi_bar
+    b = lq - (lq.max() + np.log(np.exp(lq - lq.max()).sum()))   # log q_bar
+    rev = float((np.exp(a) * (a - b)).sum())
+    fwd = float((np.exp(b) * (b - a)).sum())
+    return rev, fwd
+
+
+def _row_loss(rev, fwd, z, loss_mode):
+    if z == SRC_DISCARDED:
+        return 0.0
+    on = z == SRC_S
+    if loss_mode == LOSS_IPD_SPLIT:
+        return rev if on else fwd
+    if loss_mode == LOSS_PURE_REVERSE:
+        return rev
+    if loss_mode == LOSS_PURE_FORWARD:
+        return fwd
+    if loss_mode == LOSS_INVERSE_SPLIT:
+        return fwd if on else rev
+    raise ValueError("unknown loss mode")
+
+
+def _segments(rows_loss, src, cu):
+    """Eq. (11)'s inner term per trajectory segment: the mean of the row losses
+    over the emitted tokens (src S or T), and the teacher-intervention ratio
+    (the share of teacher-generated tokens, Section 4.3).  A segment with no
+    emitted token gives 0 for both."""
+    cu = np.asarray(cu, np.int64)
+    B = len(cu) - 1
+    seq_loss = np.zeros(B)
+    t_ratio = np.zeros(B)
+    for b in range(B):
+        z = np.asarray(src[cu[b]:cu[b + 1]])
+        keep = z != SRC_DISCARDED
+        n = int(keep.sum())
+        if n:
+            seq_loss[b] = float(np.asarray(rows_loss[cu[b]:cu[b + 1]])[keep].sum()) / n
+            t_ratio[b] = float((z == SRC_T).sum()) / n
+    return seq_loss, t_ratio
+
+
+def source_split_kl(logp_student, logp_teacher, K, src, support=SUPPORT_UNION,
+                    loss_mode=LOSS_IPD_SPLIT, cu=None):
+    """Per-position source-split KL values (Section 3.2.2).
+
+    ``logp_student`` / ``logp_teacher`` ``[M, V]`` are the two models' full
+    log-softmax at the same positions c_t; ``src [M]`` the token sources z_t.
+    Per row: S^pi and S^q (Eq. (5)), the support S_t, both distributions
+    renormalised on it (Eq. (6)), the reverse KL D(pi_bar || q_bar) and the
+    forward KL D(q_bar || pi_bar) (Eq. (10)), the row's loss by source
+    (``loss_mode``; discarded rows give 0) and the top-K overlap ratio
+    |S^pi n S^q| / K (Section 4.2).  With ``cu`` (segment offsets, one
+    segment per trajectory) also the length-normalised loss of Eq. (11) and
+    the intervention ratio per segment.
+    """
+    lps = _f64(logp_student)
+    lpt = _f64(logp_teacher)
+    M = lps.shape[0]
+    out = {k: np.zeros(M) for k in ("kl_rev", "kl_fwd", "loss", "overlap")}
+    for m in range(M):
+        Sp = _topk_set(lps[m], K)
+        Sq = _topk_set(lpt[m], K)
+        S = _support(Sp, Sq, support)
+        rev, fwd = _kl_pair(lps[m, S], lpt[m, S])
+        out["kl_rev"][m], out["kl_fwd"][m] = rev, fwd
+        out["loss"][m] = _row_loss(rev, fwd, int(src[m]), loss_mode)
+        out["overlap"][m] = len(set(Sp) & set(Sq)) / K
+    if cu is not None:
+        out["seq_loss"], out["t_ratio"] = _segments(out["loss"], src, cu)
+    return out
+
+
+def source_split_kl_lists(s_idx, s_logp, s_at_t, t_idx, t_logp, t_at_s, src,
+                          support=SUPPORT_UNION, loss_mode=LOSS_IPD_SPLIT, cu=None):
+    """``source_split_kl`` from what the verifier path produces instead of
+    full log-prob rows: each model's top-K indices and log-probs
+    (``s_idx, s_logp``; ``t_idx, t_logp``, each ``[M, K]``) and each model's
+    log-probs at the other's top-K indices (``s_at_t`` = student at t_idx,
+    ``t_at_s`` = teacher at s_idx).
+
+    An index in both lists takes its two log-probs from the list that defines
+    the support: the student's list (s_logp, t_at_s) for the union, S^pi and
+    the intersection; the teacher's (s_at_t, t_logp) for S^q.
+    """
+    s_idx = np.asarray(s_idx, np.int64)
+    t_idx = np.asarray(t_idx, np.int64)
+    M, K = s_idx.shape
+    out = {k: np.zeros(M) for k in ("kl_rev", "kl_fwd", "loss", "overlap")}
+    for m in range(M):
+        Sp, Sq = list(s_idx[m]), list(t_idx[m])
+        lp, lq = [], []
+        if support in (SUPPORT_UNION, SUPPORT_STUDENT, SUPPORT_INTERSECTION):
+            for j, v in enumerate(Sp):
+                if support == SUPPORT_INTERSECTION and v not in Sq:
+                    continue
+                lp.append(s_logp[m][j])
+                lq.append(t_at_s[m][j])
+        if support in (SUPPORT_UNION, SUPPORT_TEACHER):
+            for j, v in enumerate(Sq):
+                if support == SUPPORT_UNION and v in Sp:
+                    continue
+                lp.append(s_at_t[m][j])
+                lq.append(t_logp[m][j])
+        if support not in (SUPPORT_UNION, SUPPORT_STUDENT, SUPPORT_TEACHER, SUPPORT_INTERSECTION):
+            raise ValueError("unknown support")
+        rev, fwd = _kl_pair(lp, lq)
+        out["kl_rev"][m], out["kl_fwd"][m] = rev, fwd
+        out["loss"][m] = _row_loss(rev, fwd, int(src[m]), loss_mode)
+        out["overlap"][m] = len(set(Sp) & set(Sq)) / K
+    if cu is not None:
+        out["seq_loss"], out["t_ratio"] = _segments(out["loss"], src, cu)
+    return out
