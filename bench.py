@@ -133,6 +133,55 @@ class Step:
                                 seq_ids=m.seq_ids, token=self.repl)
 
 
+def time_source_split(batch, step, dev, reps):
+    """Per-kernel time of the source-split KL values (Eqs. (6), (10), (11)) at
+    the step's window rows, outside the step's timed region: the teacher's
+    outputs come from the step; the student's distribution at the same
+    positions (in the engine, from its proposing pass) from a second LM head of
+    the same shape with random weights.  Returns microseconds per launch and
+    the gather's algorithmic GB/s."""
+    m = step.per_model[0]["m"]
+    M, Hd = m.hidden.shape
+    V = m.W.shape[0]
+    K = step.K
+    g = torch.Generator(device=dev)
+    g.manual_seed(int(np.random.SeedSequence([0, batch.cfg.id, 30]).generate_state(1)[0]))
+    hs = torch.randn(M, Hd, generator=g, device=dev)
+    hs = (hs / hs.pow(2).mean(1, keepdim=True).sqrt()).to(m.hidden.dtype)
+    Ws = (torch.randn(V, Hd, generator=g, device=dev) * batch.cfg.w_std).to(m.W.dtype)
+    ws = torch.empty(ops.lmhead_workspace_size(M, Hd, V, K), dtype=torch.uint8, device=dev)
+    s = ops.lmhead_logsoftmax_verify(hs, Ws, torch.zeros(M, dtype=torch.int32, device=dev), K,
+                                     workspace=ws)
+    t = {k: step.outs[k][m.rows.long()].contiguous() for k in ("lse", "topk_idx", "topk_logp")}
+    src = step.scan_outs["src"][m.rows.long()].contiguous()
+    cu = step.cu
+    s_at_t = torch.empty(M, K, device=dev)
+    t_at_s = torch.empty(M, K, device=dev)
+
+    def once():
+        ops.lmhead_logp_gather(hs, Ws, s["lse"], t["topk_idx"], out=s_at_t)
+        ops.lmhead_logp_gather(m.hidden, m.W, t["lse"], s["topk_idx"], out=t_at_s)
+        ops.source_split_kl(s["topk_idx"], s["topk_logp"], s_at_t, t["topk_idx"], t["topk_logp"],
+                            t_at_s, src, cu=cu)
+    for _ in range(3):
+        once()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(7)] for _ in range(reps)]
+    for r in range(reps):
+        ops.trace_events(evs[r])
+        once()
+    ops.trace_events(None)
+    torch.cuda.synchronize()
+    gat = sum(e[0].elapsed_time(e[1]) + e[2].elapsed_time(e[3]) for e in evs) / (2 * reps)
+    rows = sum(e[4].elapsed_time(e[5]) for e in evs) / reps
+    seg = sum(e[5].elapsed_time(e[6]) for e in evs) / reps
+    es = m.hidden.element_size()
+    gather_bytes = M * K * Hd * es + M * Hd * es + M * K * 8 + M * 4
+    return {"logp_gather_us": round(gat * 1e3, 2), "kl_rows_us": round(rows * 1e3, 2),
+            "kl_segments_us": round(seg * 1e3, 2),
+            "logp_gather_gbs": round(gather_bytes / (gat * 1e-3) / 1e9, 1)}
+
+
 def work_per_launch(batch):
     """Algorithmic bytes and flops of the attention and LM-head GEMM kernels."""
     res = {"attention": [0.0, 0.0], "lmhead_gemm": [0.0, 0.0]}
@@ -345,6 +394,8 @@ def main():
         "attention_hbm_gbs": round(attn_bytes / (kt["attention"] * 1e-3) / 1e9, 1),
         "lmhead_tflops": round(work["lmhead_gemm"][1] / (kt["lmhead_gemm"] * 1e-3) / 1e12, 1),
     }
+    if len(step.per_model) == 1 and cfg.dtype == "bf16":
+        res["source_split_kl"] = time_source_split(batch, step, dev, 20)
     if not args.no_cpu:
         res["cpu_baseline"] = cpu_baseline(batch, step.prop.cpu().numpy().astype(np.int64))
     print(json.dumps(res), flush=True)

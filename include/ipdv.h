@@ -23,7 +23,12 @@
  *                               rules, SKD's fixed one-token handback);
  *   sample_takeover          -- the teacher's replacement token at each
  *                               takeover (Eq. (9), second case), drawn from
- *                               the verifier's distribution at that row.
+ *                               the verifier's distribution at that row;
+ *   lmhead_logp_gather       -- a model's log-probs at listed vocabulary
+ *                               indices (the other model's top-K), which
+ *                               complete the union support of Eq. (6);
+ *   source_split_kl          -- the per-position values of the source-split
+ *                               objective (Eqs. (6), (10), (11)).
  *
  * Conventions common to every entry point:
  *   - All array arguments are DEVICE pointers owned by the caller (except the
@@ -82,6 +87,23 @@ typedef enum { IPDV_F32 = 0, IPDV_BF16 = 1 } ipdv_dtype;
 #define IPDV_HAND_COVERAGE 0   /* hand back when the draft is inside the verifier's top-K */
 #define IPDV_HAND_FIXED_ONE 1  /* the teacher emits one token, then hands back (SKD) */
 #define IPDV_HAND_ENTROPY 2    /* hand back when ent[row] <= tau_hand */
+
+/* Distillation support S_t (source_split_kl), Eq. (5) and the text after
+ * it; the union is the paper's default (Appendix B.2). */
+#define IPDV_SUPPORT_UNION 0
+#define IPDV_SUPPORT_STUDENT 1
+#define IPDV_SUPPORT_TEACHER 2
+#define IPDV_SUPPORT_INTERSECTION 3
+
+/* KL direction per token source (source_split_kl): Eq. (10) is the default;
+ * Section 4.3 ablates the other three. */
+#define IPDV_LOSS_IPD_SPLIT 0      /* reverse KL where src = S, forward where src = T */
+#define IPDV_LOSS_PURE_REVERSE 1
+#define IPDV_LOSS_PURE_FORWARD 2
+#define IPDV_LOSS_INVERSE_SPLIT 3  /* forward KL where src = S, reverse where src = T */
+
+/* Largest index list per row of lmhead_logp_gather. */
+#define IPDV_MAX_GATHER 64
 
 /* Source labels (accept_scan `src`). */
 #define IPDV_SRC_S 0
@@ -295,13 +317,15 @@ int accept_scan_rule(const int32_t* cu_q, const int32_t* prop_tok,
  *
  * hidden, W, M, Hd, V, K, dtype and workspace must be those of the preceding
  * lmhead_logsoftmax_verify call over the rows of hidden, with the workspace
- * unchanged since (its group records hold each 128-entry group's mass; the
- * chosen group's 128 logits are recomputed exactly).  seq_ids [n_seq] int32
+ * unchanged since (its group records hold the mass of each 32-entry quarter
+ * of each 128-entry group; the chosen quarter's 32 logits are recomputed
+ * exactly).  seq_ids [n_seq] int32
  * or NULL; cu_q [B+1] int32, driver [B] uint8, event_row [B] int32, row_local
  * [T] int32 or NULL, u [B] float (B = the batch's sequences).  Outputs: token
  * int32 [B]; finished uint8 [B] (updated in place).
  * The draw agrees with the exact one whenever u[b] is farther than the fp32
- * rounding of the cumulative probabilities (about 1e-5) from an interval end.
+ * rounding of the cumulative probabilities from an interval end (typically
+ * about 1e-6 of the total mass; at most 1.2e-4 at V = 262144).
  *
  * Errors: IPDV_EINVAL (null pointer, n_seq < 0, the LM-head shape rules),
  * IPDV_EUNSUPPORTED, IPDV_EWORKSPACE, IPDV_EHIP.
@@ -314,6 +338,67 @@ int sample_takeover(const void* hidden, const void* W, int M, int Hd, int V, int
                     int32_t* token, uint8_t* finished, int dtype, void* hip_stream);
 
 /*
+ * lmhead_logp_gather -- log-softmax of a model's logits at listed vocabulary
+ * indices: logp[m, j] = hidden[m] . W[idx[m, j]] - lse[m].  The union support
+ * of Eq. (6) needs each model's log-probs at the other model's top-K indices
+ * (S^pi u S^q, Eq. (5)); each model's own top-K log-probs come from
+ * lmhead_logsoftmax_verify.
+ *
+ * hidden [M, Hd], W [V, Hd] (dtype), lse [M] float (that call's LSE for these
+ * rows), idx [M, n_idx] int32, n_idx <= IPDV_MAX_GATHER.  Output logp [M,
+ * n_idx] float; an index outside [0, V) gives -inf.  The dot product is
+ * accumulated in fp32 in a different order from the GEMM's, so a value can
+ * differ from the same index's top-K log-prob by fp32 rounding (about 1e-6
+ * of the logit's magnitude).
+ *
+ * Errors: IPDV_EINVAL (null pointer, n_idx out of range, the LM-head shape
+ * rules with K = 1), IPDV_EUNSUPPORTED, IPDV_EHIP.
+ */
+int lmhead_logp_gather(const void* hidden, const void* W, int M, int Hd, int V,
+                       const float* lse, const int32_t* idx, int n_idx,
+                       float* logp, int dtype, void* hip_stream);
+
+/*
+ * source_split_kl -- the per-position values of the source-split objective
+ * (Section 3.2.2).  For each row m (a position c_t seen by both models):
+ *   S^pi = s_idx[m, 0..K-1] (student top-K), S^q = t_idx[m, 0..K-1] (teacher);
+ *   S_t  = the support (IPDV_SUPPORT_*; Eq. (5));
+ *   pi_bar, q_bar = both distributions renormalised on S_t (Eq. (6));
+ *   kl_rev[m] = D(pi_bar || q_bar), kl_fwd[m] = D(q_bar || pi_bar) (Eq. (10));
+ *   loss[m]   = by src[m] and loss_mode (IPDV_LOSS_*): with the default,
+ *               kl_rev where src = IPDV_SRC_S, kl_fwd where src = IPDV_SRC_T,
+ *               0 where src = IPDV_SRC_DISCARDED;
+ *   overlap[m] = |S^pi n S^q| / K (the top-K overlap ratio, Section 4.2).
+ * An empty support (a disjoint intersection) gives 0 for both KLs.
+ * With cu (segment offsets [B+1], one segment per trajectory), also
+ *   seq_loss[b] = the mean of loss over the segment's emitted rows (src S or
+ *                 T) -- the length-normalised inner term of Eq. (11);
+ *   t_ratio[b]  = the share of teacher tokens among them (the intervention
+ *                 ratio, Section 4.3); both 0 for a segment with none.
+ *
+ * Inputs, each [M, K] (float or int32): s_idx, s_logp (the student's top-K
+ * and its log-probs, from its lmhead_logsoftmax_verify), s_at_t (the
+ * student's log-probs at t_idx, from lmhead_logp_gather), t_idx, t_logp, t_at_s
+ * (the same for the teacher); src [M] uint8.  Log-probs must be finite.  An
+ * index in both lists takes its two log-probs from the list that defines the
+ * support: the student's (s_logp, t_at_s) for the union, S^pi and the
+ * intersection, the teacher's (s_at_t, t_logp) for S^q.  Outputs kl_rev,
+ * kl_fwd, loss, overlap [M] and seq_loss, t_ratio [B] float are each
+ * optional (NULL: not written); src is required with loss or cu, and loss
+ * with cu and B > 0.  Computed in fp32.
+ *
+ * Errors: IPDV_EINVAL (null pointer, M < 0, K outside [1, IPDV_MAX_K], an
+ * unknown support or loss mode, B < 0), IPDV_EHIP.
+ */
+int source_split_kl(int M, int K,
+                    const int32_t* s_idx, const float* s_logp, const float* s_at_t,
+                    const int32_t* t_idx, const float* t_logp, const float* t_at_s,
+                    const uint8_t* src, int support, int loss_mode,
+                    float* kl_rev, float* kl_fwd, float* loss, float* overlap,
+                    const int32_t* cu, int B, float* seq_loss, float* t_ratio,
+                    void* hip_stream);
+
+/*
  * Optional timing hook for profilers and benchmarks (thread-local).  While
  * set, each kernel an entry point launches is bracketed by hipEventRecord of
  * the caller's events (hipEvent_t handles cast to void*), taken from
@@ -323,7 +408,8 @@ int sample_takeover(const void* hidden, const void* W, int M, int Hd, int V, int
  * ipdv_trace_count() returns how many events have been recorded since the
  * hook was last set.  Kernels per call: verify_attn_paged 3 (append,
  * attention, split combine), lmhead_logsoftmax_verify 2 (GEMM + epilogue,
- * merge), accept_scan 1, accept_scan_rule 1, sample_takeover 1.
+ * merge), accept_scan 1, accept_scan_rule 1, sample_takeover 1,
+ * lmhead_logp_gather 1, source_split_kl 1 (+1 with cu).
  */
 int ipdv_trace_events(void* const* events, int capacity);
 int ipdv_trace_count(void);

@@ -17,7 +17,7 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(os.path.dirname(HERE), "include")
 OUT = os.path.join(HERE, "libipdv.so")
 BUILD_DIR = os.path.join(HERE, "_build")
-SOURCES = ["verify_attn.hip", "lmhead.hip", "accept_scan.hip", "abi.cpp"]
+SOURCES = ["verify_attn.hip", "lmhead.hip", "accept_scan.hip", "kl.hip", "abi.cpp"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [

@@ -233,4 +233,43 @@ int accept_scan(const int32_t* cu_q, const int32_t* prop_tok, const int32_t* top
                           hip_stream);
 }
 
+int lmhead_logp_gather(const void* hidden, const void* W, int M, int Hd, int V,
+                       const float* lse, const int32_t* idx, int n_idx, float* logp, int dtype,
+                       void* hip_stream) {
+  int st = lm_shape_check(M, Hd, V, 1);
+  if (st != IPDV_OK) return st;
+  if (n_idx < 0 || n_idx > IPDV_MAX_GATHER)
+    return fail(IPDV_EINVAL, "n_idx=%d must be in [0, %d]", n_idx, IPDV_MAX_GATHER);
+  if (dtype != IPDV_F32 && dtype != IPDV_BF16) return fail(IPDV_EINVAL, "unknown dtype %d", dtype);
+  if (M == 0 || n_idx == 0) return ok();
+  if (!hidden || !W || !lse || !idx || !logp) return fail(IPDV_EINVAL, "null required pointer");
+  ipdv::GatherLaunch L{hidden, W, M, Hd, V, lse, idx, n_idx, logp, dtype == IPDV_BF16};
+  hipError_t e = ipdv::launch_logp_gather(L, reinterpret_cast<hipStream_t>(hip_stream));
+  if (e != hipSuccess) return hip_fail("lmhead_logp_gather launch", e);
+  return ok();
+}
+
+int source_split_kl(int M, int K, const int32_t* s_idx, const float* s_logp, const float* s_at_t,
+                    const int32_t* t_idx, const float* t_logp, const float* t_at_s,
+                    const uint8_t* src, int support, int loss_mode, float* kl_rev, float* kl_fwd,
+                    float* loss, float* overlap, const int32_t* cu, int B, float* seq_loss,
+                    float* t_ratio, void* hip_stream) {
+  if (M < 0) return fail(IPDV_EINVAL, "M must be >= 0 (got %d)", M);
+  if (K < 1 || K > IPDV_MAX_K) return fail(IPDV_EINVAL, "K=%d must be in [1, %d]", K, IPDV_MAX_K);
+  if (support < IPDV_SUPPORT_UNION || support > IPDV_SUPPORT_INTERSECTION)
+    return fail(IPDV_EINVAL, "unknown support %d", support);
+  if (loss_mode < IPDV_LOSS_IPD_SPLIT || loss_mode > IPDV_LOSS_INVERSE_SPLIT)
+    return fail(IPDV_EINVAL, "unknown loss mode %d", loss_mode);
+  if (cu && B < 0) return fail(IPDV_EINVAL, "B must be >= 0 (got %d)", B);
+  if (M > 0 && (!s_idx || !s_logp || !s_at_t || !t_idx || !t_logp || !t_at_s))
+    return fail(IPDV_EINVAL, "null required pointer");
+  if ((loss || cu) && !src) return fail(IPDV_EINVAL, "the loss needs src");
+  if (cu && B > 0 && !loss) return fail(IPDV_EINVAL, "per-segment values need the row loss");
+  ipdv::KlLaunch L{M, K, s_idx, s_logp, s_at_t, t_idx, t_logp, t_at_s, src, support, loss_mode,
+                   kl_rev, kl_fwd, loss, overlap, cu, cu ? B : 0, seq_loss, t_ratio};
+  hipError_t e = ipdv::launch_source_split_kl(L, reinterpret_cast<hipStream_t>(hip_stream));
+  if (e != hipSuccess) return hip_fail("source_split_kl launch", e);
+  return ok();
+}
+
 }  // extern "C"

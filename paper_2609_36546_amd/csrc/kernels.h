@@ -12,6 +12,16 @@
 #define IPDV_HAND_COVERAGE_DEV 0
 #define IPDV_HAND_FIXED_ONE_DEV 1
 #define IPDV_HAND_ENTROPY_DEV 2
+#define IPDV_SRC_S_DEV 0
+#define IPDV_SRC_T_DEV 1
+#define IPDV_SUPPORT_UNION_DEV 0
+#define IPDV_SUPPORT_STUDENT_DEV 1
+#define IPDV_SUPPORT_TEACHER_DEV 2
+#define IPDV_SUPPORT_INTERSECTION_DEV 3
+#define IPDV_LOSS_IPD_SPLIT_DEV 0
+#define IPDV_LOSS_PURE_REVERSE_DEV 1
+#define IPDV_LOSS_PURE_FORWARD_DEV 2
+#define IPDV_LOSS_INVERSE_SPLIT_DEV 3
 
 namespace ipdv {
 
@@ -97,6 +107,43 @@ struct SampleLaunch {
 };
 
 hipError_t launch_sample_takeover(const SampleLaunch& L, const LmPlan& pl, hipStream_t st);
+
+// ---- log-probs at given vocabulary indices ----
+struct GatherLaunch {
+  const void* hidden;
+  const void* W;
+  int M, Hd, V;
+  const float* lse;            // [M], the LM head's
+  const int32_t* idx;          // [M, n]
+  int n;
+  float* logp;                 // [M, n]
+  bool dtype_bf16;
+};
+
+hipError_t launch_logp_gather(const GatherLaunch& L, hipStream_t st);
+
+// ---- source-split KL values ----
+struct KlLaunch {
+  int M, K;
+  const int32_t* s_idx;
+  const float* s_logp;
+  const float* s_at_t;
+  const int32_t* t_idx;
+  const float* t_logp;
+  const float* t_at_s;
+  const uint8_t* src;
+  int support, loss_mode;
+  float* kl_rev;
+  float* kl_fwd;
+  float* loss;
+  float* overlap;
+  const int32_t* cu;
+  int B;
+  float* seq_loss;
+  float* t_ratio;
+};
+
+hipError_t launch_source_split_kl(const KlLaunch& L, hipStream_t st);
 
 // ---- verdict scan ----
 struct ScanLaunch {

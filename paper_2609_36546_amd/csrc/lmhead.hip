@@ -1206,6 +1206,52 @@ hipError_t launch_lmhead(const LmLaunch& L, const LmPlan& pl, hipStream_t st) {
   return launch_rb<float, 1>(p, st);
 }
 
+// log-softmax at listed vocabulary indices: one workgroup per row, the row's
+// hidden vector staged in LDS, each wave streaming 4 W rows at a time with
+// 16-byte loads across its lanes (the merge's exact recompute).
+constexpr int kMaxGather = 64;
+
+template <typename DT>
+__global__ __launch_bounds__(kMT) void logp_gather_kernel(LmParams p, const float* lse,
+                                                          const int32_t* idx, int n, float* out) {
+  const int m = blockIdx.x;
+  __shared__ float s_hid[kMaxHd];
+  __shared__ float s_v[kMaxGather];
+  __shared__ int s_i[kMaxGather];
+  const DT* hr = reinterpret_cast<const DT*>(p.hidden) + (size_t)m * p.Hd;
+  for (int k = threadIdx.x; k < p.Hd; k += kMT) s_hid[k] = to_f32(hr[k]);
+  __syncthreads();
+  const int32_t* ir = idx + (size_t)m * n;
+  // indices outside [0, V) read as V: recompute_entries gives them -inf
+  recompute_entries<DT, 4>(p, s_hid, n, [&](int e) {
+    const int v = ir[e];
+    return (v < 0 || v >= p.V) ? p.V : v;
+  }, s_v, s_i);
+  __syncthreads();
+  const float l = lse[m];
+  for (int e = threadIdx.x; e < n; e += kMT) out[(size_t)m * n + e] = s_v[e] - l;
+}
+
+hipError_t launch_logp_gather(const GatherLaunch& L, hipStream_t st) {
+  if (L.M == 0 || L.n == 0) return hipSuccess;
+  LmParams p{};
+  p.hidden = L.hidden;
+  p.W = L.W;
+  p.M = L.M;
+  p.Hd = L.Hd;
+  p.V = L.V;
+  trace_begin(st);
+  if (L.dtype_bf16)
+    hipLaunchKernelGGL((logp_gather_kernel<bf16>), dim3(L.M), dim3(kMT), 0, st, p, L.lse, L.idx,
+                       L.n, L.logp);
+  else
+    hipLaunchKernelGGL((logp_gather_kernel<float>), dim3(L.M), dim3(kMT), 0, st, p, L.lse, L.idx,
+                       L.n, L.logp);
+  const hipError_t e = hipGetLastError();
+  trace_mark(st);
+  return e;
+}
+
 hipError_t launch_sample_takeover(const SampleLaunch& L, const LmPlan& pl, hipStream_t st) {
   if (L.n_seq == 0) return hipSuccess;
   const LmParams p = lm_params(L.hidden, L.W, L.M, L.Hd, L.V, L.K, pl, const_cast<void*>(L.workspace));

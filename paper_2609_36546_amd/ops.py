@@ -59,6 +59,11 @@ def lib() -> ctypes.CDLL:
                                        ctypes.c_int32, ci, ci, ci, f32p, ctypes.c_float,
                                        ctypes.c_float, i32p, i32p, u8p, u8p, i32p, u8p, vp]
         L.accept_scan_rule.restype = ci
+        L.lmhead_logp_gather.argtypes = [vp, vp, ci, ci, ci, f32p, i32p, ci, f32p, ci, vp]
+        L.lmhead_logp_gather.restype = ci
+        L.source_split_kl.argtypes = [ci, ci, i32p, f32p, f32p, i32p, f32p, f32p, u8p, ci, ci,
+                                      f32p, f32p, f32p, f32p, i32p, ci, f32p, f32p, vp]
+        L.source_split_kl.restype = ci
         L.sample_takeover.argtypes = [vp, vp, ci, ci, ci, ci, vp, cs, i32p, ci, i32p, u8p, i32p,
                                       i32p, f32p, ctypes.c_int32, i32p, u8p, ci, vp]
         L.sample_takeover.restype = ci
@@ -343,3 +348,65 @@ def sample_takeover(hidden, W, K: int, workspace, cu_q, driver, event_row, u, eo
         _ptr(finished), _dtype_code(dt), _stream(dev))
     _check("sample_takeover", st)
     return token
+
+
+def lmhead_logp_gather(hidden, W, lse, idx, out=None):
+    """log-softmax of hidden . W^T at idx [M, n] (see include/ipdv.h);
+    lse [M] float32 from the same model's lmhead_logsoftmax_verify.  Returns
+    logp [M, n] float32 (-inf for indices outside [0, V))."""
+    dev = hidden.device
+    dt = hidden.dtype
+    _need(hidden, "hidden", dt, dev, 2)
+    _need(W, "W", dt, dev, 2)
+    M, Hd = hidden.shape
+    V = W.shape[0]
+    _need(lse, "lse", torch.float32, dev, 1)
+    _need(idx, "idx", torch.int32, dev, 2)
+    if lse.shape[0] != M or idx.shape[0] != M:
+        raise ValueError("lse and idx must have M rows")
+    n = idx.shape[1]
+    if out is None:
+        out = torch.empty(M, n, dtype=torch.float32, device=dev)
+    st = lib().lmhead_logp_gather(_ptr(hidden), _ptr(W), M, Hd, V, _ptr(lse), _ptr(idx), n,
+                                  _ptr(out), _dtype_code(dt), _stream(dev))
+    _check("lmhead_logp_gather", st)
+    return out
+
+
+SUPPORT_UNION, SUPPORT_STUDENT, SUPPORT_TEACHER, SUPPORT_INTERSECTION = 0, 1, 2, 3
+LOSS_IPD_SPLIT, LOSS_PURE_REVERSE, LOSS_PURE_FORWARD, LOSS_INVERSE_SPLIT = 0, 1, 2, 3
+
+
+def source_split_kl(s_idx, s_logp, s_at_t, t_idx, t_logp, t_at_s, src, support=SUPPORT_UNION,
+                    loss_mode=LOSS_IPD_SPLIT, cu=None):
+    """Per-position source-split KL values (see include/ipdv.h).  Inputs
+    [M, K] (int32 indices, float32 log-probs) and src [M] uint8; cu [B+1]
+    int32 segment offsets or None.  Returns dict kl_rev, kl_fwd, loss,
+    overlap [M] and, with cu, seq_loss, t_ratio [B] (float32)."""
+    dev = s_idx.device
+    for t, name, dt in ((s_idx, "s_idx", torch.int32), (t_idx, "t_idx", torch.int32),
+                        (s_logp, "s_logp", torch.float32), (s_at_t, "s_at_t", torch.float32),
+                        (t_logp, "t_logp", torch.float32), (t_at_s, "t_at_s", torch.float32)):
+        _need(t, name, dt, dev, 2)
+    M, K = s_idx.shape
+    for t in (s_logp, s_at_t, t_idx, t_logp, t_at_s):
+        if tuple(t.shape) != (M, K):
+            raise ValueError("every list input must be [M, K]")
+    _need(src, "src", torch.uint8, dev, 1)
+    if src.shape[0] != M:
+        raise ValueError("src must be [M]")
+    out = {k: torch.empty(M, dtype=torch.float32, device=dev)
+           for k in ("kl_rev", "kl_fwd", "loss", "overlap")}
+    B = 0
+    if cu is not None:
+        _need(cu, "cu", torch.int32, dev, 1)
+        B = cu.shape[0] - 1
+        out["seq_loss"] = torch.empty(B, dtype=torch.float32, device=dev)
+        out["t_ratio"] = torch.empty(B, dtype=torch.float32, device=dev)
+    st = lib().source_split_kl(
+        M, K, _ptr(s_idx), _ptr(s_logp), _ptr(s_at_t), _ptr(t_idx), _ptr(t_logp), _ptr(t_at_s),
+        _ptr(src), int(support), int(loss_mode), _ptr(out["kl_rev"]), _ptr(out["kl_fwd"]),
+        _ptr(out["loss"]), _ptr(out["overlap"]), _ptr(cu), B, _ptr(out.get("seq_loss")),
+        _ptr(out.get("t_ratio")), _stream(dev))
+    _check("source_split_kl", st)
+    return out

@@ -155,3 +155,39 @@ def test_sample_argument_errors(kw, status):
 
 def test_sample_empty_batch_is_ok_without_gpu():
     assert _sample(n_seq=0, u=None, token=None) == 0
+
+
+def test_gather_and_kl_argument_errors():
+    L = ops.lib()
+    vp = ctypes.c_void_p
+    # lmhead_logp_gather(hidden, W, M, Hd, V, lse, idx, n_idx, logp, dtype, stream)
+    g = [vp(1), vp(1), 4, 128, 1000, vp(1), vp(1), 16, vp(1), 1, None]
+    bad = list(g); bad[7] = 65
+    assert L.lmhead_logp_gather(*bad) == -1           # n_idx above IPDV_MAX_GATHER
+    bad = list(g); bad[3] = 100
+    assert L.lmhead_logp_gather(*bad) == -2           # Hd not a multiple of 64
+    bad = list(g); bad[6] = None
+    assert L.lmhead_logp_gather(*bad) == -1
+    bad = list(g); bad[9] = 7
+    assert L.lmhead_logp_gather(*bad) == -1
+    empty = list(g); empty[7] = 0
+    assert L.lmhead_logp_gather(*empty) == 0
+    # source_split_kl(M, K, s_idx, s_logp, s_at_t, t_idx, t_logp, t_at_s, src, support,
+    #                 loss_mode, kl_rev, kl_fwd, loss, overlap, cu, B, seq_loss, t_ratio, stream)
+    k = [8, 16] + [vp(1)] * 7 + [0, 0] + [vp(1)] * 4 + [vp(1), 3, vp(1), vp(1), None]
+    bad = list(k); bad[1] = 33
+    assert L.source_split_kl(*bad) == -1
+    bad = list(k); bad[1] = 0
+    assert L.source_split_kl(*bad) == -1
+    bad = list(k); bad[9] = 4
+    assert L.source_split_kl(*bad) == -1              # unknown support
+    bad = list(k); bad[10] = -1
+    assert L.source_split_kl(*bad) == -1              # unknown loss mode
+    bad = list(k); bad[8] = None
+    assert L.source_split_kl(*bad) == -1              # loss without src
+    bad = list(k); bad[13] = None
+    assert L.source_split_kl(*bad) == -1              # segments without the row loss
+    bad = list(k); bad[16] = -1
+    assert L.source_split_kl(*bad) == -1
+    empty = list(k); empty[0] = 0; empty[16] = 0
+    assert L.source_split_kl(*empty) == 0

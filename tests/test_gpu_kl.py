@@ -1,0 +1,151 @@
+"""GPU parity of lmhead_logp_gather and source_split_kl against the fp64
+oracle, through the C ABI.
+
+* The KL kernel on the same float32 inputs as the oracle's list form: every
+  support, loss mode and segment case, K from 1 to 32, rows spanning several
+  workgroups with a ragged tail.  The GPU computes in fp32 with the hardware
+  exp2/log2 (relative error about 1e-7 each): 2e-5 absolute plus 1e-4
+  relative on values of order 1.
+* The gather against the oracle's log-softmax at the listed indices.  The GPU
+  subtracts its own LM head's LSE; both are fp32 sums over 2048 channels
+  (about 1e-6 of the logit scale), so 2e-4 absolute.
+* End to end at the student/teacher LM-head shape (V = 151936, Hd = 2048):
+  two LM heads, two gathers and the KL kernel against the full-form oracle
+  on fp64 logits.  Each log-prob is within 2e-3 of the oracle's (the LM-head
+  parity bound); a KL value moves by at most about twice the largest
+  log-prob error, so 5e-3.  Only rows where both top-K sets are decided
+  (oracle set margin > 1e-3 for both models) are compared value by value;
+  the others must still hold valid supports.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2609_36546_amd import ops
+from tests.workload import to_np
+
+pytestmark = pytest.mark.gpu
+
+
+def _t(a, dt):
+    return torch.from_numpy(np.ascontiguousarray(np.asarray(a, dt))).cuda()
+
+
+def _lists(rng, M, V, K, corr):
+    """Full-row log-probs of two correlated models and the lists the GPU
+    path produces from them (float32)."""
+    ls = rng.normal(size=(M, V)) * 1.5
+    lt = corr * ls + rng.normal(size=(M, V))
+    lps = ls - np.log(np.exp(ls - ls.max(1, keepdims=True)).sum(1, keepdims=True)) - ls.max(1, keepdims=True)
+    lpt = lt - np.log(np.exp(lt - lt.max(1, keepdims=True)).sum(1, keepdims=True)) - lt.max(1, keepdims=True)
+    s_idx = np.argsort(-lps, axis=1, kind="stable")[:, :K]
+    t_idx = np.argsort(-lpt, axis=1, kind="stable")[:, :K]
+    tk = lambda a, i: np.take_along_axis(a, i, axis=1).astype(np.float32)
+    return s_idx, tk(lps, s_idx), tk(lps, t_idx), t_idx, tk(lpt, t_idx), tk(lpt, s_idx)
+
+
+def _run_kl(lists, src, support, mode, cu):
+    s_idx, s_logp, s_at_t, t_idx, t_logp, t_at_s = lists
+    g = ops.source_split_kl(_t(s_idx, np.int32), _t(s_logp, np.float32), _t(s_at_t, np.float32),
+                            _t(t_idx, np.int32), _t(t_logp, np.float32), _t(t_at_s, np.float32),
+                            _t(src, np.uint8), support=support, loss_mode=mode,
+                            cu=None if cu is None else _t(cu, np.int32))
+    torch.cuda.synchronize()
+    return {k: to_np(v).astype(np.float64) for k, v in g.items()}
+
+
+@pytest.mark.parametrize("K,corr", [(16, 0.6), (1, 0.8), (4, 0.0), (32, 0.9), (7, 1.0)])
+def test_kl_kernel_every_support_and_mode(K, corr):
+    print(f"[kl] K={K} corr={corr}", flush=True)
+    rng = np.random.default_rng(100 + K)
+    M, V = 203, max(80, 3 * K)             # 51 workgroups, the last one partial
+    lists = _lists(rng, M, V, K, corr)
+    src = rng.choice([oracle.SRC_S, oracle.SRC_T, oracle.SRC_DISCARDED], size=M, p=[0.6, 0.3, 0.1])
+    cu = np.array([0, 1, 1, 50, 60, 200, 203])     # an empty and a one-row segment
+    src[50:60] = oracle.SRC_DISCARDED               # a segment with nothing emitted
+    lists64 = [np.asarray(a, np.float64) if a.dtype != np.int64 else a for a in lists]
+    for support in (oracle.SUPPORT_UNION, oracle.SUPPORT_STUDENT, oracle.SUPPORT_TEACHER,
+                    oracle.SUPPORT_INTERSECTION):
+        for mode in (oracle.LOSS_IPD_SPLIT, oracle.LOSS_PURE_REVERSE, oracle.LOSS_PURE_FORWARD,
+                     oracle.LOSS_INVERSE_SPLIT):
+            ref = oracle.source_split_kl_lists(*lists64, src, support=support, loss_mode=mode, cu=cu)
+            g = _run_kl(lists, src, support, mode, cu)
+            for key in ref:
+                np.testing.assert_allclose(g[key], ref[key], atol=2e-5, rtol=1e-4,
+                                           err_msg=f"{key} support={support} mode={mode}")
+
+
+def test_gather_against_oracle():
+    print("[kl] gather V=5003 Hd=256 bf16 and fp32", flush=True)
+    rng = np.random.default_rng(7)
+    for dt in (torch.bfloat16, torch.float32):
+        M, Hd, V, K = 37, 256, 5003, 16
+        gen = torch.Generator(device="cuda")
+        gen.manual_seed(3)
+        h = torch.randn(M, Hd, generator=gen, device="cuda").to(dt)
+        W = (torch.randn(V, Hd, generator=gen, device="cuda") * 0.1).to(dt)
+        ws = torch.empty(ops.lmhead_workspace_size(M, Hd, V, K), dtype=torch.uint8, device="cuda")
+        outs = ops.lmhead_logsoftmax_verify(h, W, torch.zeros(M, dtype=torch.int32, device="cuda"),
+                                            K, workspace=ws)
+        idx = rng.integers(0, V, size=(M, 40))
+        idx[0, :3] = [-1, V, 2**31 - 1]               # outside [0, V): -inf
+        idx[1, :] = idx[1, 0]                          # repeats
+        g = ops.lmhead_logp_gather(h, W, outs["lse"], _t(idx, np.int32))
+        torch.cuda.synchronize()
+        ref = oracle.logp_gather(to_np(h), to_np(W), idx)
+        g = to_np(g).astype(np.float64)
+        assert np.all(np.isneginf(g[0, :3]))
+        np.testing.assert_allclose(g[np.isfinite(ref)], ref[np.isfinite(ref)], atol=2e-4)
+        # gathering a row's own top-K reproduces its top-K log-probs
+        own = ops.lmhead_logp_gather(h, W, outs["lse"], outs["topk_idx"])
+        torch.cuda.synchronize()
+        np.testing.assert_allclose(to_np(own), to_np(outs["topk_logp"]), atol=2e-5)
+
+
+def test_end_to_end_student_teacher_full_vocab():
+    """Student and teacher LM heads (V = 151936, Hd = 2048) over the same 24
+    positions; teacher weights correlated with the student's so the top-K
+    sets partly overlap."""
+    print("[kl] end to end V=151936 Hd=2048 M=24", flush=True)
+    M, Hd, V, K = 24, 2048, 151936, 16
+    dev = torch.device("cuda")
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(11)
+    hs = torch.randn(M, Hd, generator=gen, device=dev)
+    hs = (hs / hs.pow(2).mean(1, keepdim=True).sqrt())
+    ht = 0.8 * hs + 0.6 * torch.randn(M, Hd, generator=gen, device=dev)
+    ht = (ht / ht.pow(2).mean(1, keepdim=True).sqrt())
+    Ws = torch.randn(V, Hd, generator=gen, device=dev) * 0.02
+    Wt = 0.8 * Ws + 0.012 * torch.randn(V, Hd, generator=gen, device=dev)
+    hs, ht, Ws, Wt = (x.to(torch.bfloat16) for x in (hs, ht, Ws, Wt))
+    res = []
+    for h, W in ((hs, Ws), (ht, Wt)):
+        ws = torch.empty(ops.lmhead_workspace_size(M, Hd, V, K), dtype=torch.uint8, device=dev)
+        res.append(ops.lmhead_logsoftmax_verify(h, W, torch.zeros(M, dtype=torch.int32, device=dev),
+                                                K, workspace=ws))
+    s, t = res
+    s_at_t = ops.lmhead_logp_gather(hs, Ws, s["lse"], t["topk_idx"])
+    t_at_s = ops.lmhead_logp_gather(ht, Wt, t["lse"], s["topk_idx"])
+    src = np.array([oracle.SRC_S, oracle.SRC_T, oracle.SRC_S, oracle.SRC_DISCARDED] * 6, np.uint8)
+    cu = np.array([0, 8, 24])
+    g = ops.source_split_kl(s["topk_idx"], s["topk_logp"], s_at_t, t["topk_idx"], t["topk_logp"],
+                            t_at_s, _t(src, np.uint8), cu=_t(cu, np.int32))
+    torch.cuda.synchronize()
+    g = {k: to_np(v).astype(np.float64) for k, v in g.items()}
+    ls = oracle.logits_fp64(to_np(hs), to_np(Ws))
+    lt = oracle.logits_fp64(to_np(ht), to_np(Wt))
+    ref = oracle.source_split_kl(ls, lt, K, src, cu=cu)
+    ms = oracle.lmhead_logsoftmax(to_np(hs), to_np(Ws), np.zeros(M, np.int64), K, logits=ls)
+    mt = oracle.lmhead_logsoftmax(to_np(ht), to_np(Wt), np.zeros(M, np.int64), K, logits=lt)
+    decided = (ms["set_margin"] > 1e-3) & (mt["set_margin"] > 1e-3)
+    print(f"  decided rows {int(decided.sum())}/{M}, mean overlap {ref['overlap'].mean():.3f}",
+          flush=True)
+    assert decided.sum() >= M // 2
+    assert 0.0 < ref["overlap"].mean() < 1.0
+    for key in ("kl_rev", "kl_fwd", "loss", "overlap"):
+        np.testing.assert_allclose(g[key][decided], ref[key][decided], atol=5e-3, err_msg=key)
+    assert np.all(g["kl_rev"] >= -1e-5) and np.all(g["kl_fwd"] >= -1e-5)
+    if decided.all():
+        np.testing.assert_allclose(g["seq_loss"], ref["seq_loss"], atol=5e-3)
+        np.testing.assert_allclose(g["t_ratio"], ref["t_ratio"], atol=0)
