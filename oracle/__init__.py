@@ -11,5 +11,5 @@ from .ipdv_oracle import (  # noqa: F401
     sample_categorical, sample_takeover,
     SUPPORT_UNION, SUPPORT_STUDENT, SUPPORT_TEACHER, SUPPORT_INTERSECTION,
     LOSS_IPD_SPLIT, LOSS_PURE_REVERSE, LOSS_PURE_FORWARD, LOSS_INVERSE_SPLIT,
-    logp_gather, source_split_kl, source_split_kl_lists,
+    logp_gather, source_split_kl, source_split_kl_lists, propose_decode,
 )

@@ -33,6 +33,9 @@ What it computes, each part written from the paper's definitions:
   at teacher-generated ones (Eq. (10)), the length-normalised sum per
   trajectory (Eq. (11)), the top-K overlap ratio and the intervention ratio;
   ``logp_gather`` gives each model's log-probs at the other's top-K indices.
+* ``propose_decode`` -- the driver's gamma autoregressive draft steps over
+  its own paged cache (Section 3.2.3, propose stage): a one-row attention
+  window, the LM head and a temperature-1 draw per step.
 
 Readings where the paper is silent (tie-break, window/row alignment, cache
 rollback lengths, EOS inside a window, length cap) are listed in the
@@ -620,3 +623,50 @@ def source_split_kl_lists(s_idx, s_logp, s_at_t, t_idx, t_logp, t_at_s, src,
     if cu is not None:
         out["seq_loss"], out["t_ratio"] = _segments(out["loss"], src, cu)
     return out
+
+
+# ---------------------------------------------------------------------------
+# The proposer's decode steps (Section 3.2.3, propose stage)
+# ---------------------------------------------------------------------------
+
+def propose_decode(steps, k_cache, v_cache, page_table, ctx_lens, scale, W, K, seq_ids=None):
+    """The driver's draft of gamma tokens, one autoregressive step at a time
+    (Section 3.2.3: the driver proposes gamma tokens; Eq. (9): the draft is
+    drawn from the driver's own distribution at temperature 1, Appendix A).
+
+    Step j of sequence b (b over ``seq_ids``, default all) appends its input
+    token's keys/values at position L_b + j of the proposer's own paged cache,
+    attends over keys 0 .. L_b + j (a one-row window), scores the row with the
+    LM head and draws the next token by inverse CDF with the uniform u[b].
+    ``steps`` is a list of dicts with q [n,Hq,D], k_new / v_new [n,Hkv,D],
+    hidden [n,Hd] and u [n] (n = number of sequences handled, row i for the
+    i-th of the ascending ``seq_ids``): the inputs a
+    full model derives from the previous step's token through layers that
+    are not part of this path.
+
+    Returns (per-step list of dicts out / lm / token, k_cache', v_cache').
+    """
+    kc = np.array(k_cache, copy=True)
+    vc = np.array(v_cache, copy=True)
+    seqs = list(range(len(ctx_lens))) if seq_ids is None else [int(b) for b in seq_ids]
+    if seqs != sorted(set(seqs)):
+        raise ValueError("seq_ids must be ascending and distinct (row i is seq_ids[i])")
+    n = len(seqs)
+    sid = np.asarray(seqs, np.int64)
+    res = []
+    for j, st in enumerate(steps):
+        lens = np.asarray(ctx_lens, np.int64).copy()
+        lens[sid] += j
+        # cu_q indexes the handled sequences' rows: row i belongs to seqs[i]
+        cu_full = np.zeros(len(ctx_lens) + 1, np.int64)
+        for i, b in enumerate(seqs):
+            cu_full[b + 1] = 1
+        cu_full = np.cumsum(cu_full)
+        out, kc, vc = verify_attn_paged(st["q"], st["k_new"], st["v_new"], kc, vc, page_table,
+                                        lens, cu_full, scale, seq_ids=sid, n_seq=n)
+        logits = logits_fp64(st["hidden"], W)
+        lm = lmhead_logsoftmax(st["hidden"], W, np.zeros(n, np.int64), K, logits=logits)
+        draws = [sample_categorical(logits[i], float(st["u"][i])) for i in range(n)]
+        res.append({"out": out, "lm": lm, "token": np.array([d[0] for d in draws]),
+                    "margin": np.array([d[1] for d in draws]), "logits": logits})
+    return res, kc, vc
