@@ -182,6 +182,62 @@ def time_source_split(batch, step, dev, reps):
             "logp_gather_gbs": round(gather_bytes / (gat * 1e-3) / 1e9, 1)}
 
 
+def time_propose_step(dev, reps, seed=0):
+    """One decode step of the proposer (Section 3.2.3, propose stage) beside
+    the verify step: the student shape (16 query / 8 KV heads, D 128, hidden
+    2048, vocab 151936), 64 sequences with contexts U[1024, 8192], one row
+    each: append + attention over its own cache, the LM head, and one
+    temperature-1 draw per row.  Returns the step time, decode tokens/s,
+    per-kernel microseconds and the LM-head GEMM's HBM rate (W read once)."""
+    cfg = inputs.scaled(inputs.WORKLOADS["student-bf16"], B=64, ctx_lo=1024, ctx_hi=8192,
+                        k_choices=(1,))
+    b = inputs.make_batch(cfg, seed=seed, device=dev, poison=False)
+    m = b.models[0]
+    B, K = cfg.B, cfg.K
+    t = lambda a, dt: torch.from_numpy(np.asarray(a, dt)).to(dev)
+    ctx, cu = t(b.ctx_lens, np.int32), t(b.cu_q, np.int32)
+    ws_a = torch.empty(ops.attn_workspace_size(B, m.shape.Hq, m.shape.Hkv, m.shape.D, 1,
+                                               m.page_table.shape[1], cfg.page_size),
+                       dtype=torch.uint8, device=dev)
+    M = m.hidden.shape[0]
+    ws_l = torch.empty(ops.lmhead_workspace_size(M, m.shape.hidden, m.shape.vocab, K),
+                       dtype=torch.uint8, device=dev)
+    out = torch.empty_like(m.q)
+    prop = torch.zeros(M, dtype=torch.int32, device=dev)
+    lm_outs = None
+    u = t(np.minimum(np.random.default_rng(seed).random(M), 1 - 2.0 ** -24), np.float32)
+    tok = torch.empty(M, dtype=torch.int32, device=dev)
+
+    def once():
+        nonlocal lm_outs
+        ops.verify_attn_paged(m.q, m.k_new, m.v_new, m.k_pool, m.v_pool, m.page_table, ctx, cu, 1,
+                              out=out, workspace=ws_a)
+        lm_outs = ops.lmhead_logsoftmax_verify(m.hidden, m.W, prop, K, outs=lm_outs, workspace=ws_l)
+        ops.lmhead_sample(m.hidden, m.W, K, ws_l, u, token=tok)
+    for _ in range(3):
+        once()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(9)] for _ in range(reps)]
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for r in range(reps):
+        ops.trace_events(evs[r])
+        once()
+    stop.record()
+    ops.trace_events(None)
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(stop) / reps
+    names = ["append", "attention", "combine", None, "lmhead_gemm", "lmhead_merge", None, "sample"]
+    kt = {n: sum(e[i].elapsed_time(e[i + 1]) for e in evs) / reps * 1e3
+          for i, n in enumerate(names) if n}
+    w_bytes = m.shape.vocab * m.shape.hidden * m.W.element_size()
+    return {"workload": "student-bf16 decode: B=64, ctx U[1024,8192], k=1, 16q/8kv/D128, "
+                        "hidden 2048, vocab 151936, K=16",
+            "ms_per_step": round(ms, 4), "tokens_per_s": round(B / (ms * 1e-3), 1),
+            "kernels_us": {k: round(v, 2) for k, v in kt.items()},
+            "lmhead_gemm_w_gbs": round(w_bytes / (kt["lmhead_gemm"] * 1e-6) / 1e9, 1)}
+
+
 def work_per_launch(batch):
     """Algorithmic bytes and flops of the attention and LM-head GEMM kernels."""
     res = {"attention": [0.0, 0.0], "lmhead_gemm": [0.0, 0.0]}
@@ -396,6 +452,8 @@ def main():
     }
     if len(step.per_model) == 1 and cfg.dtype == "bf16":
         res["source_split_kl"] = time_source_split(batch, step, dev, 20)
+    if args.workload == "teacher-bf16":
+        res["propose_step"] = time_propose_step(dev, 20, args.seed)
     if not args.no_cpu:
         res["cpu_baseline"] = cpu_baseline(batch, step.prop.cpu().numpy().astype(np.int64))
     print(json.dumps(res), flush=True)

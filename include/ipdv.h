@@ -24,6 +24,8 @@
  *   sample_takeover          -- the teacher's replacement token at each
  *                               takeover (Eq. (9), second case), drawn from
  *                               the verifier's distribution at that row;
+ *   lmhead_sample            -- the proposer's per-row draw (temperature 1)
+ *                               from the same records;
  *   lmhead_logp_gather       -- a model's log-probs at listed vocabulary
  *                               indices (the other model's top-K), which
  *                               complete the union support of Eq. (6);
@@ -338,6 +340,30 @@ int sample_takeover(const void* hidden, const void* W, int M, int Hd, int V, int
                     int32_t* token, uint8_t* finished, int dtype, void* hip_stream);
 
 /*
+ * lmhead_sample -- one draw per row from the model's distribution at
+ * temperature 1, top-p 1 (Appendix A), reusing the preceding
+ * lmhead_logsoftmax_verify call's group records: the proposer's sampling step
+ * of the propose stage (Section 3.2.3: the driver proposes its next tokens
+ * autoregressively; Eq. (9): x~ ~ pi(. | c_t) when the student drives, q when
+ * the teacher does).
+ *
+ *   token[m] = the first vocabulary index v (index order) with
+ *              sum_{w <= v} softmax(l_m)_w > u[m]
+ * -- the inverse-CDF draw with the caller's uniform u[m] in [0, 1).
+ *
+ * hidden, W, M, Hd, V, K, dtype and workspace as in the preceding
+ * lmhead_logsoftmax_verify call over these rows, the workspace unchanged
+ * since.  u [M] float, token [M] int32.  The same rounding note as
+ * sample_takeover applies.
+ *
+ * Errors: IPDV_EINVAL (null pointer, the LM-head shape rules),
+ * IPDV_EUNSUPPORTED, IPDV_EWORKSPACE, IPDV_EHIP.
+ */
+int lmhead_sample(const void* hidden, const void* W, int M, int Hd, int V, int K,
+                  const void* workspace, size_t workspace_bytes, const float* u,
+                  int32_t* token, int dtype, void* hip_stream);
+
+/*
  * lmhead_logp_gather -- log-softmax of a model's logits at listed vocabulary
  * indices: logp[m, j] = hidden[m] . W[idx[m, j]] - lse[m].  The union support
  * of Eq. (6) needs each model's log-probs at the other model's top-K indices
@@ -409,7 +435,7 @@ int source_split_kl(int M, int K,
  * hook was last set.  Kernels per call: verify_attn_paged 3 (append,
  * attention, split combine), lmhead_logsoftmax_verify 2 (GEMM + epilogue,
  * merge), accept_scan 1, accept_scan_rule 1, sample_takeover 1,
- * lmhead_logp_gather 1, source_split_kl 1 (+1 with cu).
+ * lmhead_sample 1, lmhead_logp_gather 1, source_split_kl 1 (+1 with cu).
  */
 int ipdv_trace_events(void* const* events, int capacity);
 int ipdv_trace_count(void);

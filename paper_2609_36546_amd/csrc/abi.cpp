@@ -194,6 +194,26 @@ int sample_takeover(const void* hidden, const void* W, int M, int Hd, int V, int
   return ok();
 }
 
+int lmhead_sample(const void* hidden, const void* W, int M, int Hd, int V, int K,
+                  const void* workspace, size_t workspace_bytes, const float* u, int32_t* token,
+                  int dtype, void* hip_stream) {
+  int st = lm_shape_check(M, Hd, V, K);
+  if (st != IPDV_OK) return st;
+  if (dtype != IPDV_F32 && dtype != IPDV_BF16) return fail(IPDV_EUNSUPPORTED, "dtype %d", dtype);
+  if (M == 0) return ok();
+  if (!hidden || !W || !u || !token) return fail(IPDV_EINVAL, "null required pointer");
+  const ipdv::LmPlan pl = ipdv::lm_plan(M, Hd, V, K, dtype == IPDV_BF16);
+  const size_t need = ipdv::lm_plan(M, Hd, V, K, true).workspace_bytes;
+  if (!workspace || workspace_bytes < need)
+    return fail(IPDV_EWORKSPACE, "workspace of %zu bytes needed (got %zu)", need,
+                workspace ? workspace_bytes : (size_t)0);
+  ipdv::SampleLaunch L{hidden, W, M, Hd, V, K, workspace, nullptr, 0, nullptr, nullptr, nullptr,
+                       nullptr, u, -1, token, nullptr, dtype == IPDV_BF16};
+  hipError_t e = ipdv::launch_sample_rows(L, pl, reinterpret_cast<hipStream_t>(hip_stream));
+  if (e != hipSuccess) return hip_fail("lmhead_sample launch", e);
+  return ok();
+}
+
 int accept_scan_rule(const int32_t* cu_q, const int32_t* prop_tok, const int32_t* topk_idx,
                      int K, const uint8_t* driver, const int32_t* ctx_lens,
                      const int32_t* seq_lens, int32_t eos_id, int32_t max_len, int B,

@@ -107,6 +107,8 @@ struct SampleLaunch {
 };
 
 hipError_t launch_sample_takeover(const SampleLaunch& L, const LmPlan& pl, hipStream_t st);
+// one draw per hidden row: u [M] and token [M] (the sequence fields unused)
+hipError_t launch_sample_rows(const SampleLaunch& L, const LmPlan& pl, hipStream_t st);
 
 // ---- log-probs at given vocabulary indices ----
 struct GatherLaunch {

@@ -911,12 +911,15 @@ __global__ __launch_bounds__(kMT) void lmhead_merge_kernel(LmParams p) {
 }
 
 // ---------------------------------------------------------------------------
-// Takeover replacement draw (Eq. (9), second case): one workgroup per
-// sequence.  The inverse CDF over the vocabulary in index order is taken in
-// two levels: the group records give each 128-entry group's mass,
-// s_g exp(v1_g - max), so a block-wide prefix scan over the groups finds the
-// group the uniform falls in; that group's 128 logits are recomputed exactly
-// and the draw finishes inside it, at the same fraction of the group's mass.
+// Draws from softmax(l) at temperature 1 (Appendix A): the takeover
+// replacement (Eq. (9), second case; one workgroup per sequence) and the
+// proposer's per-row draw (one workgroup per row).  The inverse CDF over the
+// vocabulary in index order is taken in three levels: the group records give
+// each 128-entry group's mass, exp(v1_g - max) times its quarter sums, so a
+// block-wide prefix scan over the groups finds the group the uniform falls
+// in; the group's four quarter sums find the 32-entry quarter, at the same
+// fraction of the group's mass; the quarter's 32 logits are recomputed
+// exactly and the draw finishes inside it.
 // ---------------------------------------------------------------------------
 
 struct SampleParams {
@@ -952,10 +955,13 @@ __device__ float block_scan(float x, float* s_w, float* total) {
   return x + before;
 }
 
-template <typename DT>
-__global__ __launch_bounds__(kMT) void sample_takeover_kernel(LmParams p, SampleParams s) {
+// PER_ROW: one draw per hidden row m (blockIdx.x), with u[m], into token[m].
+// Otherwise: one workgroup per handled sequence b; only a student-driven
+// window with a takeover draws, at the takeover row, with u[b], into token[b]
+// (and a drawn EOS finishes the sequence).
+template <typename DT, bool PER_ROW>
+__global__ __launch_bounds__(kMT) void sample_kernel(LmParams p, SampleParams s) {
   constexpr int NW = kMT / kWave;
-  const int b = s.seq_ids ? s.seq_ids[blockIdx.x] : blockIdx.x;
   const int tid = threadIdx.x;
   __shared__ float s_red[3 * NW];
   __shared__ float s_hid[kMaxHd];
@@ -963,13 +969,19 @@ __global__ __launch_bounds__(kMT) void sample_takeover_kernel(LmParams p, Sample
   __shared__ int s_first, s_last;
   __shared__ float s_cv[32];
   __shared__ int s_ci[32];
-  const int ev = s.event_row[b];
-  const int r = ev >= 0 ? s.cu_q[b] + ev : -1;
-  const int m = r < 0 ? -1 : (s.row_local ? s.row_local[r] : r);
-  // only student-driven windows with an event (a takeover) draw
-  if (s.driver[b] != 0 || ev < 0 || m < 0 || m >= p.M) {
-    if (tid == 0) s.token[b] = -1;
-    return;
+  int b, m;
+  if (PER_ROW) {
+    b = m = blockIdx.x;
+  } else {
+    b = s.seq_ids ? s.seq_ids[blockIdx.x] : blockIdx.x;
+    const int ev = s.event_row[b];
+    const int r = ev >= 0 ? s.cu_q[b] + ev : -1;
+    m = r < 0 ? -1 : (s.row_local ? s.row_local[r] : r);
+    // only student-driven windows with an event (a takeover) draw
+    if (s.driver[b] != 0 || ev < 0 || m < 0 || m >= p.M) {
+      if (tid == 0) s.token[b] = -1;
+      return;
+    }
   }
   const int G = p.n_groups;
   const size_t base = (size_t)m * G;
@@ -1082,7 +1094,7 @@ __global__ __launch_bounds__(kMT) void sample_takeover_kernel(LmParams p, Sample
     if (tid == 0) {
       const int tok = s_ci[i];
       s.token[b] = tok;
-      if (tok == s.eos_id) s.finished[b] = 1;
+      if (!PER_ROW && tok == s.eos_id) s.finished[b] = 1;
     }
   }
 }
@@ -1252,6 +1264,22 @@ hipError_t launch_logp_gather(const GatherLaunch& L, hipStream_t st) {
   return e;
 }
 
+hipError_t launch_sample_rows(const SampleLaunch& L, const LmPlan& pl, hipStream_t st) {
+  if (L.M == 0) return hipSuccess;
+  const LmParams p = lm_params(L.hidden, L.W, L.M, L.Hd, L.V, L.K, pl, const_cast<void*>(L.workspace));
+  SampleParams s{};
+  s.u = L.u;
+  s.token = L.token;
+  trace_begin(st);
+  if (L.dtype_bf16)
+    hipLaunchKernelGGL((sample_kernel<bf16, true>), dim3(L.M), dim3(kMT), 0, st, p, s);
+  else
+    hipLaunchKernelGGL((sample_kernel<float, true>), dim3(L.M), dim3(kMT), 0, st, p, s);
+  const hipError_t e = hipGetLastError();
+  trace_mark(st);
+  return e;
+}
+
 hipError_t launch_sample_takeover(const SampleLaunch& L, const LmPlan& pl, hipStream_t st) {
   if (L.n_seq == 0) return hipSuccess;
   const LmParams p = lm_params(L.hidden, L.W, L.M, L.Hd, L.V, L.K, pl, const_cast<void*>(L.workspace));
@@ -1259,9 +1287,9 @@ hipError_t launch_sample_takeover(const SampleLaunch& L, const LmPlan& pl, hipSt
                        L.finished};
   trace_begin(st);
   if (L.dtype_bf16)
-    hipLaunchKernelGGL((sample_takeover_kernel<bf16>), dim3(L.n_seq), dim3(kMT), 0, st, p, s);
+    hipLaunchKernelGGL((sample_kernel<bf16, false>), dim3(L.n_seq), dim3(kMT), 0, st, p, s);
   else
-    hipLaunchKernelGGL((sample_takeover_kernel<float>), dim3(L.n_seq), dim3(kMT), 0, st, p, s);
+    hipLaunchKernelGGL((sample_kernel<float, false>), dim3(L.n_seq), dim3(kMT), 0, st, p, s);
   const hipError_t e = hipGetLastError();
   trace_mark(st);
   return e;

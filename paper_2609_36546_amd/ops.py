@@ -59,6 +59,8 @@ def lib() -> ctypes.CDLL:
                                        ctypes.c_int32, ci, ci, ci, f32p, ctypes.c_float,
                                        ctypes.c_float, i32p, i32p, u8p, u8p, i32p, u8p, vp]
         L.accept_scan_rule.restype = ci
+        L.lmhead_sample.argtypes = [vp, vp, ci, ci, ci, ci, vp, cs, f32p, i32p, ci, vp]
+        L.lmhead_sample.restype = ci
         L.lmhead_logp_gather.argtypes = [vp, vp, ci, ci, ci, f32p, i32p, ci, f32p, ci, vp]
         L.lmhead_logp_gather.restype = ci
         L.source_split_kl.argtypes = [ci, ci, i32p, f32p, f32p, i32p, f32p, f32p, u8p, ci, ci,
@@ -410,3 +412,25 @@ def source_split_kl(s_idx, s_logp, s_at_t, t_idx, t_logp, t_at_s, src, support=S
         _ptr(out.get("t_ratio")), _stream(dev))
     _check("source_split_kl", st)
     return out
+
+
+def lmhead_sample(hidden, W, K: int, workspace, u, token=None):
+    """One temperature-1 draw per row (see include/ipdv.h): hidden, W, K and
+    workspace as passed to the preceding lmhead_logsoftmax_verify call; u [M]
+    float32 uniforms in [0, 1).  Returns token [M] int32."""
+    dev = hidden.device
+    dt = hidden.dtype
+    _need(hidden, "hidden", dt, dev, 2)
+    _need(W, "W", dt, dev, 2)
+    M, Hd = hidden.shape
+    V = W.shape[0]
+    _need(u, "u", torch.float32, dev, 1)
+    if u.shape[0] != M:
+        raise ValueError("u must be [M]")
+    if token is None:
+        token = torch.empty(M, dtype=torch.int32, device=dev)
+    st = lib().lmhead_sample(_ptr(hidden), _ptr(W), M, Hd, V, K, _ptr(workspace),
+                             workspace.numel() * workspace.element_size(), _ptr(u), _ptr(token),
+                             _dtype_code(dt), _stream(dev))
+    _check("lmhead_sample", st)
+    return token

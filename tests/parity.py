@@ -187,3 +187,27 @@ def check_takeover_draws(tok, fin, fin0, ref, logits_of_row, cu_q, driver, event
                 (b, tok[b], u[b], lo, c[tok[b]])
         assert fin[b] == (1 if tok[b] == eos_id else fin0[b]), b
     return exact
+
+
+def check_row_draws(tok, logits, u, ref_tok, ref_margin):
+    """Per-row draws against the oracle's: equal where the oracle margin
+    exceeds DRAW_TOL, otherwise valid (u within DRAW_TOL of the drawn token's
+    cumulative interval).  Returns (exact draws, the largest distance of u
+    from the GPU token's interval in the oracle's CDF, as a fraction of the
+    total mass; 0 for a draw inside its interval)."""
+    exact = 0
+    worst = 0.0
+    for m in range(len(tok)):
+        l = logits[m]
+        p = np.exp(l - l.max())
+        p /= p.sum()
+        c = np.cumsum(p)
+        t = int(tok[m])
+        lo = c[t - 1] if t > 0 else 0.0
+        worst = max(worst, lo - u[m], u[m] - c[t])
+        if ref_margin[m] > DRAW_TOL:
+            assert tok[m] == ref_tok[m], (m, tok[m], ref_tok[m], ref_margin[m])
+            exact += 1
+        else:
+            assert p[t] > 0 and lo - DRAW_TOL <= u[m] < c[t] + DRAW_TOL, (m, t, u[m], lo, c[t])
+    return exact, worst

@@ -1,0 +1,115 @@
+"""GPU parity of the proposer's decode steps (Section 3.2.3, propose stage):
+lmhead_sample (one temperature-1 draw per row) and gamma decode steps
+(verify_attn_paged with one-row windows, lmhead_logsoftmax_verify,
+lmhead_sample) against the oracle, through the C ABI.
+
+Draws must equal the oracle's where its margin exceeds parity.DRAW_TOL (the
+fp32 rounding bound of the cumulative probabilities; see test_gpu_sample) and
+be valid elsewhere.  Beyond that worst-case bound, u must lie within
+CDF_TOL = 1e-5 of the GPU token's interval in the oracle's CDF: the expected
+error of the GPU's cumulative sums is about 1e-6 of the mass (fp32 logits
+within about 1e-6 relative, sums blocked over at most 16 levels of 2^-24
+each), so 1e-5 leaves a factor of ten; the GPU is deterministic, so the check
+does not flake.  Attention, cache and LM-head checks are those of the
+verify path.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2609_36546_amd import inputs, ops
+from tests import parity
+from tests.workload import to_np
+
+pytestmark = pytest.mark.gpu
+CDF_TOL = 1e-5
+
+
+def _say(msg):
+    print(msg, flush=True)
+
+
+def _lm(h, W, K):
+    ws = torch.empty(ops.lmhead_workspace_size(h.shape[0], h.shape[1], W.shape[0], K),
+                     dtype=torch.uint8, device=h.device)
+    outs = ops.lmhead_logsoftmax_verify(h, W, torch.zeros(h.shape[0], dtype=torch.int32,
+                                                          device=h.device), K, workspace=ws)
+    return ws, outs
+
+
+@pytest.mark.parametrize("M,Hd,V,dt,std,peaked", [(64, 2048, 151936, torch.bfloat16, 0.02, False),
+                                                  (64, 2048, 151936, torch.bfloat16, 0.12, True),
+                                                  (37, 128, 5003, torch.bfloat16, 0.6, True),
+                                                  (9, 64, 300, torch.float32, 0.1, False)])
+def test_lmhead_sample_rows(M, Hd, V, dt, std, peaked):
+    """Near-uniform rows (the workload's W scale: every token's probability is
+    below DRAW_TOL, so no draw is decided and every draw is checked for
+    validity only) and peaked rows, where most draws are decided and must
+    equal the oracle's."""
+    _say(f"[decode] lmhead_sample M={M} Hd={Hd} V={V} {dt}")
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(M + V)
+    h = torch.randn(M, Hd, generator=gen, device="cuda")
+    h = (h / h.pow(2).mean(1, keepdim=True).sqrt()).to(dt)
+    W = (torch.randn(V, Hd, generator=gen, device="cuda") * std).to(dt)
+    K = 16
+    ws, _ = _lm(h, W, K)
+    u = ((np.arange(M) + 0.5) / M).astype(np.float32)
+    u[0] = 0.0
+    tok = ops.lmhead_sample(h, W, K, ws, torch.from_numpy(u).cuda())
+    torch.cuda.synchronize()
+    l = oracle.logits_fp64(to_np(h), to_np(W))
+    ref = [oracle.sample_categorical(l[m], float(u[m])) for m in range(M)]
+    exact, worst = parity.check_row_draws(to_np(tok), l, u.astype(np.float64), [r[0] for r in ref],
+                                          [r[1] for r in ref])
+    _say(f"  exact={exact}/{M} worst CDF distance {worst:.2e}")
+    assert worst <= CDF_TOL
+    if peaked:
+        assert exact >= M // 2
+
+
+def test_gamma_decode_steps_student_shape():
+    """Six sequences of the student shape (16 query / 8 KV heads, D = 128,
+    V = 151936), gamma = 4 steps over the proposer's own pages."""
+    gamma = 4
+    cfg = inputs.scaled(inputs.WORKLOADS["student-bf16"], B=6, ctx_lo=40, ctx_hi=1300,
+                        k_choices=(gamma,))
+    _say(f"[decode] gamma={gamma} B={cfg.B} student shape")
+    b = inputs.make_batch(cfg, seed=4, device="cuda")
+    m = b.models[0]
+    B, K, dev = cfg.B, cfg.K, torch.device("cuda")
+    rng = np.random.default_rng(9)
+    us = rng.random((gamma, B)).astype(np.float32)
+    kc, vc = m.k_pool.clone(), m.v_pool.clone()
+    cu1 = torch.arange(B + 1, dtype=torch.int32, device=dev)
+    scale = 1.0 / np.sqrt(m.shape.D)
+    steps, gpu = [], []
+    for j in range(gamma):
+        rows = torch.from_numpy(b.cu_q[:-1] + j).long().to(dev)
+        q, kn, vn, hid = (x.index_select(0, rows).contiguous() for x in (m.q, m.k_new, m.v_new, m.hidden))
+        ctx = torch.from_numpy((b.ctx_lens + j).astype(np.int32)).to(dev)
+        out = ops.verify_attn_paged(q, kn, vn, kc, vc, m.page_table, ctx, cu1, max_q=1)
+        ws, lm = _lm(hid, m.W, K)
+        tok = ops.lmhead_sample(hid, m.W, K, ws, torch.from_numpy(us[j]).to(dev))
+        torch.cuda.synchronize()
+        gpu.append(dict(out=out, lm={k: v.clone() for k, v in lm.items()}, tok=to_np(tok)))
+        steps.append(dict(q=to_np(q), k_new=to_np(kn), v_new=to_np(vn), hidden=to_np(hid),
+                          u=us[j].astype(np.float64)))
+    res, kref, vref = oracle.propose_decode(steps, to_np(m.k_pool), to_np(m.v_pool),
+                                            to_np(m.page_table), b.ctx_lens, scale,
+                                            to_np(m.W), K)
+    # the proposer's cache after gamma appends, bit for bit (poisoned slots stay NaN)
+    for g, r in ((kc, kref), (vc, vref)):
+        g = to_np(g).astype(np.float64)
+        np.testing.assert_array_equal(np.isnan(g), np.isnan(r))
+        np.testing.assert_array_equal(g[~np.isnan(g)], r[~np.isnan(r)])
+    total_exact = 0
+    for j in range(gamma):
+        parity.check_attention_rows(gpu[j]["out"], res[j]["out"], np.arange(B), m.q.dtype)
+        parity.check_lmhead(gpu[j]["lm"], res[j]["lm"], res[j]["logits"], K)
+        ex, worst = parity.check_row_draws(gpu[j]["tok"], res[j]["logits"], steps[j]["u"],
+                                           res[j]["token"], res[j]["margin"])
+        total_exact += ex
+        _say(f"  step {j}: exact {ex}/{B}, worst CDF distance {worst:.2e}")
+        assert worst <= CDF_TOL
