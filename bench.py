@@ -348,6 +348,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="teacher-bf16", choices=sorted(inputs.WORKLOADS))
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--launch", choices=["graph", "eager"], default="eager",
+                    help="timed steps as eager launches (default) or as replays of one "
+                         "captured HIP graph")
     ap.add_argument("--K", type=int, default=None,
                     help="top-K coverage width (default: the workload's, 16); the coverage-width "
                          "ablation sweeps 4, 8, 16, 32")
@@ -380,20 +383,49 @@ def main():
         step.run()
     torch.cuda.synchronize()
 
-    # per-kernel timing: the library records these events around its kernels
-    n_models = len(step.per_model)
-    per_step = 9 * n_models + 2
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(per_step)] for _ in range(args.steps)]
+    # the timed region: K steps, no per-kernel events inside it
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    graph = None
+    if args.launch == "graph":
+        # one step captured as a HIP graph (the step allocates nothing and
+        # records no memset), replayed K times
+        graph = torch.cuda.CUDAGraph()
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            step.run()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(graph):
+            step.run()
+        for _ in range(args.warmup):
+            graph.replay()
     torch.cuda.synchronize()
     start.record()
     for s in range(args.steps):
-        ops.trace_events(evs[s])
-        step.run()
+        if graph is not None:
+            graph.replay()
+        else:
+            step.run()
     stop.record()
-    ops.trace_events(None)
     torch.cuda.synchronize()
     ms = start.elapsed_time(stop) / args.steps
+
+    # per-kernel timing, in a separate eager pass: the library records these
+    # events around its kernels
+    n_models = len(step.per_model)
+    per_step = 9 * n_models + 2
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(per_step)] for _ in range(args.steps)]
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0.record()
+    for s in range(args.steps):
+        ops.trace_events(evs[s])
+        step.run()
+    t1.record()
+    ops.trace_events(None)
+    torch.cuda.synchronize()
+    ms_traced = t0.elapsed_time(t1) / args.steps
 
     kt = {k: 0.0 for k in KERNELS}
     for s in range(args.steps):
@@ -446,6 +478,8 @@ def main():
                                f"hidden {cfg.models[0].hidden}, vocab {cfg.models[0].vocab}, K={cfg.K}",
                    "window_rows": batch.T, "parallelism": "single GPU"},
         "roofline": roof,
+        "launch": "hip graph" if args.launch == "graph" else "eager",
+        "ms_per_step_eager_traced": round(ms_traced, 4),
         "kernels_us": {k: round(v * 1e3, 2) for k, v in kt.items()},
         "attention_hbm_gbs": round(attn_bytes / (kt["attention"] * 1e-3) / 1e9, 1),
         "lmhead_tflops": round(work["lmhead_gemm"][1] / (kt["lmhead_gemm"] * 1e-3) / 1e12, 1),
