@@ -41,7 +41,8 @@ def _lm(h, W, K):
 @pytest.mark.parametrize("M,Hd,V,dt,std,peaked", [(64, 2048, 151936, torch.bfloat16, 0.02, False),
                                                   (64, 2048, 151936, torch.bfloat16, 0.12, True),
                                                   (37, 128, 5003, torch.bfloat16, 0.6, True),
-                                                  (9, 64, 300, torch.float32, 0.1, False)])
+                                                  (9, 64, 300, torch.float32, 0.1, False),
+                                                  (5, 4096, 262143, torch.bfloat16, 0.05, False)])
 def test_lmhead_sample_rows(M, Hd, V, dt, std, peaked):
     """Near-uniform rows (the workload's W scale: every token's probability is
     below DRAW_TOL, so no draw is decided and every draw is checked for
