@@ -115,3 +115,48 @@ def test_teacher_config_scaled():
 
 def test_dual_cache_config_scaled():
     _pipeline(inputs.scaled(inputs.WORKLOADS["dual-cache-bf16"], B=8, ctx_lo=20, ctx_hi=1000), 5)
+
+
+def test_rule_variants_on_verifier_outputs():
+    """The rule variants fed by the verifier itself: the LM head's entropy at
+    each row drives the entropy takeover (and, for teacher-driven windows, the
+    entropy handback), and its top-K drives SKD's coverage takeover.  Both
+    sides take the same float32 entropies and the same top-K lists, so the
+    verdicts must be bit-exact."""
+    cfg = inputs.scaled(inputs.WORKLOADS["dual-cache-bf16"], B=10, ctx_lo=20, ctx_hi=900)
+    _say(f"[pipeline] rule variants on {cfg.name} B={cfg.B}")
+    b = inputs.make_batch(cfg, seed=8, device="cuda")
+    K, T, dev = cfg.K, b.T, torch.device("cuda")
+    prop = batch_proposals(b)
+    prop_t = torch.from_numpy(prop.astype(np.int32)).to(dev)
+    outs = {"lse": torch.empty(T, device=dev), "logp_prop": torch.empty(T, device=dev),
+            "argmax": torch.empty(T, dtype=torch.int32, device=dev),
+            "topk_idx": torch.empty(T, K, dtype=torch.int32, device=dev),
+            "topk_logp": torch.empty(T, K, device=dev), "entropy": torch.empty(T, device=dev)}
+    for m in b.models:
+        if m.hidden.shape[0] == 0:
+            continue
+        ops.lmhead_logsoftmax_verify(m.hidden, m.W, prop_t[m.rows.long()].contiguous(), K,
+                                     out_rows=m.rows, n_out_rows=T, outs=outs)
+    torch.cuda.synchronize()
+    ent = to_np(outs["entropy"]).astype(np.float32)
+    topk = to_np(outs["topk_idx"]).astype(np.int64)
+    tau = np.float32(np.median(ent))          # about half the rows on each side
+    t = lambda a, dt: torch.from_numpy(np.asarray(a, dt)).to(dev)
+    for take, hand in [(oracle.TAKE_ENTROPY, oracle.HAND_ENTROPY),
+                       (oracle.TAKE_COVERAGE, oracle.HAND_FIXED_ONE),
+                       (oracle.TAKE_ENTROPY, oracle.HAND_COVERAGE)]:
+        g = ops.accept_scan_rule(t(b.cu_q, np.int32), prop_t, outs["topk_idx"], K,
+                                 t(b.driver, np.uint8), t(b.ctx_lens, np.int32),
+                                 t(b.seq_lens, np.int32), b.eos_id, b.max_len, take_rule=take,
+                                 hand_rule=hand, ent=outs["entropy"], tau_take=float(tau),
+                                 tau_hand=float(tau))
+        torch.cuda.synchronize()
+        ref = oracle.accept_scan(b.cu_q, prop, topk, K, b.driver, b.ctx_lens, b.seq_lens,
+                                 b.eos_id, b.max_len, take_rule=take, hand_rule=hand,
+                                 ent=ent.astype(np.float64), tau_take=float(tau),
+                                 tau_hand=float(tau))
+        parity.compare_scan(g, ref)
+        np.testing.assert_array_equal(to_np(g["src"]).astype(np.int64), ref["src"])
+        _say(f"  take={take} hand={hand}: events {int((ref['event_row'] >= 0).sum())}/{cfg.B}, "
+             f"accepted {int(ref['n_acc'].sum())}/{T}")
