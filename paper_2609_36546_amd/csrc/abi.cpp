@@ -11,6 +11,26 @@
 #include "../../include/ipdv.h"
 #include "kernels.h"
 
+// The kernels see their own copies of the public constants (kernels.h does not
+// include the C header); these keep the two in step.
+static_assert(IPDV_MAX_K == IPDV_MAX_K_DEV, "top-K limit");
+static_assert(IPDV_MAX_GATHER == IPDV_MAX_GATHER_DEV, "gather limit");
+static_assert(IPDV_DRIVER_S == IPDV_DRIVER_S_DEV, "driver code");
+static_assert(IPDV_SRC_S == IPDV_SRC_S_DEV && IPDV_SRC_T == IPDV_SRC_T_DEV, "source labels");
+static_assert(IPDV_TAKE_COVERAGE == IPDV_TAKE_COVERAGE_DEV &&
+                  IPDV_TAKE_ENTROPY == IPDV_TAKE_ENTROPY_DEV, "takeover rules");
+static_assert(IPDV_HAND_COVERAGE == IPDV_HAND_COVERAGE_DEV &&
+                  IPDV_HAND_FIXED_ONE == IPDV_HAND_FIXED_ONE_DEV &&
+                  IPDV_HAND_ENTROPY == IPDV_HAND_ENTROPY_DEV, "handback rules");
+static_assert(IPDV_SUPPORT_UNION == IPDV_SUPPORT_UNION_DEV &&
+                  IPDV_SUPPORT_STUDENT == IPDV_SUPPORT_STUDENT_DEV &&
+                  IPDV_SUPPORT_TEACHER == IPDV_SUPPORT_TEACHER_DEV &&
+                  IPDV_SUPPORT_INTERSECTION == IPDV_SUPPORT_INTERSECTION_DEV, "supports");
+static_assert(IPDV_LOSS_IPD_SPLIT == IPDV_LOSS_IPD_SPLIT_DEV &&
+                  IPDV_LOSS_PURE_REVERSE == IPDV_LOSS_PURE_REVERSE_DEV &&
+                  IPDV_LOSS_PURE_FORWARD == IPDV_LOSS_PURE_FORWARD_DEV &&
+                  IPDV_LOSS_INVERSE_SPLIT == IPDV_LOSS_INVERSE_SPLIT_DEV, "loss modes");
+
 namespace {
 
 thread_local char g_err[512] = "";

@@ -6,6 +6,7 @@
 #include <stdint.h>
 
 #define IPDV_MAX_K_DEV 32
+#define IPDV_MAX_GATHER_DEV 64
 #define IPDV_DRIVER_S_DEV 0
 #define IPDV_TAKE_COVERAGE_DEV 0
 #define IPDV_TAKE_ENTROPY_DEV 1

@@ -1218,10 +1218,12 @@ hipError_t launch_lmhead(const LmLaunch& L, const LmPlan& pl, hipStream_t st) {
   return launch_rb<float, 1>(p, st);
 }
 
+namespace {
+
 // log-softmax at listed vocabulary indices: one workgroup per row, the row's
 // hidden vector staged in LDS, each wave streaming 4 W rows at a time with
 // 16-byte loads across its lanes (the merge's exact recompute).
-constexpr int kMaxGather = 64;
+constexpr int kMaxGather = IPDV_MAX_GATHER_DEV;
 
 template <typename DT>
 __global__ __launch_bounds__(kMT) void logp_gather_kernel(LmParams p, const float* lse,
@@ -1243,6 +1245,8 @@ __global__ __launch_bounds__(kMT) void logp_gather_kernel(LmParams p, const floa
   const float l = lse[m];
   for (int e = threadIdx.x; e < n; e += kMT) out[(size_t)m * n + e] = s_v[e] - l;
 }
+
+}  // namespace
 
 hipError_t launch_logp_gather(const GatherLaunch& L, hipStream_t st) {
   if (L.M == 0 || L.n == 0) return hipSuccess;

@@ -249,31 +249,17 @@ def lmhead_logsoftmax_verify(hidden, W, prop_tok, K: int, out_rows=None, n_out_r
     return outs
 
 
-def accept_scan(cu_q, prop_tok, topk_idx, K: int, driver, ctx_lens, seq_lens, eos_id: int,
-                max_len: int, outs=None):
-    """Verdict for each sequence's window (see include/ipdv.h).  Returns dict
-    n_acc, event_row, next_driver, finished, new_cache_len, src."""
-    return accept_scan_rule(cu_q, prop_tok, topk_idx, K, driver, ctx_lens, seq_lens, eos_id,
-                            max_len, outs=outs, _entry="accept_scan")
-
-
 TAKE_COVERAGE, TAKE_ENTROPY = 0, 1
 HAND_COVERAGE, HAND_FIXED_ONE, HAND_ENTROPY = 0, 1, 2
 
 
-def accept_scan_rule(cu_q, prop_tok, topk_idx, K: int, driver, ctx_lens, seq_lens, eos_id: int,
-                     max_len: int, take_rule: int = TAKE_COVERAGE, hand_rule: int = HAND_COVERAGE,
-                     ent=None, tau_take: float = 0.0, tau_hand: float = 0.0, outs=None,
-                     _entry="accept_scan_rule"):
-    """Verdict with the takeover / handback rule variants (see
-    include/ipdv.h, accept_scan_rule).  ``ent`` is a [T] float32 entropy per
-    row, needed by the entropy rules."""
+def _scan_args(cu_q, prop_tok, topk_idx, K, driver, ctx_lens, seq_lens, ent, uses_ent, outs):
+    """Checks the verdict inputs and allocates the outputs when none are given."""
     dev = cu_q.device
     _need(cu_q, "cu_q", torch.int32, dev, 1)
     B = cu_q.shape[0] - 1
     _need(prop_tok, "prop_tok", torch.int32, dev, 1)
     T = prop_tok.shape[0]
-    uses_ent = take_rule == TAKE_ENTROPY or hand_rule == HAND_ENTROPY
     if uses_ent:
         _need(ent, "ent", torch.float32, dev, 1)
         if ent.shape[0] != T:
@@ -295,20 +281,42 @@ def accept_scan_rule(cu_q, prop_tok, topk_idx, K: int, driver, ctx_lens, seq_len
             "src": torch.empty(T, dtype=torch.uint8, device=dev),
         }
     tk = _ptr(topk_idx) if (K > 0 and topk_idx is not None) else None
-    if _entry == "accept_scan":
-        st = lib().accept_scan(
-            _ptr(cu_q), _ptr(prop_tok), tk, K, _ptr(driver), _ptr(ctx_lens), _ptr(seq_lens),
-            int(eos_id), int(max_len), B, _ptr(outs["n_acc"]), _ptr(outs["event_row"]),
-            _ptr(outs["next_driver"]), _ptr(outs["finished"]), _ptr(outs["new_cache_len"]),
-            _ptr(outs["src"]), _stream(dev))
-    else:
-        st = lib().accept_scan_rule(
-            _ptr(cu_q), _ptr(prop_tok), tk, K, _ptr(driver), _ptr(ctx_lens), _ptr(seq_lens),
-            int(eos_id), int(max_len), B, int(take_rule), int(hand_rule),
-            _ptr(ent) if uses_ent else None, float(tau_take), float(tau_hand),
-            _ptr(outs["n_acc"]), _ptr(outs["event_row"]), _ptr(outs["next_driver"]),
-            _ptr(outs["finished"]), _ptr(outs["new_cache_len"]), _ptr(outs["src"]), _stream(dev))
-    _check(_entry, st)
+    return dev, B, tk, outs
+
+
+def _scan_outs(outs):
+    return (_ptr(outs["n_acc"]), _ptr(outs["event_row"]), _ptr(outs["next_driver"]),
+            _ptr(outs["finished"]), _ptr(outs["new_cache_len"]), _ptr(outs["src"]))
+
+
+def accept_scan(cu_q, prop_tok, topk_idx, K: int, driver, ctx_lens, seq_lens, eos_id: int,
+                max_len: int, outs=None):
+    """Verdict for each sequence's window (see include/ipdv.h).  Returns dict
+    n_acc, event_row, next_driver, finished, new_cache_len, src."""
+    dev, B, tk, outs = _scan_args(cu_q, prop_tok, topk_idx, K, driver, ctx_lens, seq_lens, None,
+                                  False, outs)
+    st = lib().accept_scan(_ptr(cu_q), _ptr(prop_tok), tk, K, _ptr(driver), _ptr(ctx_lens),
+                           _ptr(seq_lens), int(eos_id), int(max_len), B, *_scan_outs(outs),
+                           _stream(dev))
+    _check("accept_scan", st)
+    return outs
+
+
+def accept_scan_rule(cu_q, prop_tok, topk_idx, K: int, driver, ctx_lens, seq_lens, eos_id: int,
+                     max_len: int, take_rule: int = TAKE_COVERAGE, hand_rule: int = HAND_COVERAGE,
+                     ent=None, tau_take: float = 0.0, tau_hand: float = 0.0, outs=None):
+    """Verdict with the takeover / handback rule variants (see
+    include/ipdv.h, accept_scan_rule).  ``ent`` is a [T] float32 entropy per
+    row, needed by the entropy rules."""
+    uses_ent = take_rule == TAKE_ENTROPY or hand_rule == HAND_ENTROPY
+    dev, B, tk, outs = _scan_args(cu_q, prop_tok, topk_idx, K, driver, ctx_lens, seq_lens, ent,
+                                  uses_ent, outs)
+    st = lib().accept_scan_rule(
+        _ptr(cu_q), _ptr(prop_tok), tk, K, _ptr(driver), _ptr(ctx_lens), _ptr(seq_lens),
+        int(eos_id), int(max_len), B, int(take_rule), int(hand_rule),
+        _ptr(ent) if uses_ent else None, float(tau_take), float(tau_hand), *_scan_outs(outs),
+        _stream(dev))
+    _check("accept_scan_rule", st)
     return outs
 
 

@@ -191,3 +191,24 @@ def test_gather_and_kl_argument_errors():
     assert L.source_split_kl(*bad) == -1
     empty = list(k); empty[0] = 0; empty[16] = 0
     assert L.source_split_kl(*empty) == 0
+
+
+def test_binding_and_oracle_constants_match_the_header():
+    import oracle
+    defs = dict((m.group(1), int(m.group(2))) for m in
+                re.finditer(r"#define\s+(IPDV_\w+)\s+(-?\d+)", open(HEADER).read()))
+    pairs = {"TAKE_COVERAGE": "IPDV_TAKE_COVERAGE", "TAKE_ENTROPY": "IPDV_TAKE_ENTROPY",
+             "HAND_COVERAGE": "IPDV_HAND_COVERAGE", "HAND_FIXED_ONE": "IPDV_HAND_FIXED_ONE",
+             "HAND_ENTROPY": "IPDV_HAND_ENTROPY", "SUPPORT_UNION": "IPDV_SUPPORT_UNION",
+             "SUPPORT_STUDENT": "IPDV_SUPPORT_STUDENT", "SUPPORT_TEACHER": "IPDV_SUPPORT_TEACHER",
+             "SUPPORT_INTERSECTION": "IPDV_SUPPORT_INTERSECTION",
+             "LOSS_IPD_SPLIT": "IPDV_LOSS_IPD_SPLIT", "LOSS_PURE_REVERSE": "IPDV_LOSS_PURE_REVERSE",
+             "LOSS_PURE_FORWARD": "IPDV_LOSS_PURE_FORWARD",
+             "LOSS_INVERSE_SPLIT": "IPDV_LOSS_INVERSE_SPLIT"}
+    for name, macro in pairs.items():
+        assert getattr(ops, name) == defs[macro], name
+        assert getattr(oracle, name) == defs[macro], name
+    for name, macro in (("DRIVER_S", "IPDV_DRIVER_S"), ("DRIVER_T", "IPDV_DRIVER_T"),
+                        ("SRC_S", "IPDV_SRC_S"), ("SRC_T", "IPDV_SRC_T"),
+                        ("SRC_DISCARDED", "IPDV_SRC_DISCARDED")):
+        assert getattr(oracle, name) == defs[macro], name
