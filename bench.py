@@ -101,7 +101,10 @@ class Step:
                                                          m.shape.vocab, K), dtype=torch.uint8, device=dev)
             row_local = torch.full((T,), -1, dtype=torch.int32, device=dev)
             row_local[m.rows.long()] = torch.arange(m.rows.shape[0], dtype=torch.int32, device=dev)
-            self.per_model.append(dict(m=m, ws_a=ws_a, ws_l=ws_l, prop=p.contiguous(),
+            # bf16 weights are repacked once into the tiled layout (setup, as an
+            # engine does at load time); fp32 keeps the row-major W
+            W = ops.lmhead_pack_w(m.W) if m.W.dtype == torch.bfloat16 else m.W
+            self.per_model.append(dict(m=m, W=W, ws_a=ws_a, ws_l=ws_l, prop=p.contiguous(),
                                        out=torch.empty_like(m.q), row_local=row_local))
         self.outs = {
             "lse": torch.empty(T, device=dev), "logp_prop": torch.empty(T, device=dev),
@@ -118,7 +121,7 @@ class Step:
             ops.verify_attn_paged(m.q, m.k_new, m.v_new, m.k_pool, m.v_pool, m.page_table,
                                   self.ctx, self.cu, self.max_q, seq_ids=m.seq_ids,
                                   out=pm["out"], workspace=pm["ws_a"])
-            ops.lmhead_logsoftmax_verify(m.hidden, m.W, pm["prop"], self.K, out_rows=m.rows,
+            ops.lmhead_logsoftmax_verify(m.hidden, pm["W"], pm["prop"], self.K, out_rows=m.rows,
                                          n_out_rows=self.b.T, outs=self.outs, workspace=pm["ws_l"])
         self.scan_outs = ops.accept_scan(self.cu, self.prop, self.outs["topk_idx"], self.K,
                                          self.driver, self.ctx, self.seq_lens, self.b.eos_id,
@@ -127,7 +130,7 @@ class Step:
         # from its own LM-head records
         for pm in self.per_model:
             m = pm["m"]
-            ops.sample_takeover(m.hidden, m.W, self.K, pm["ws_l"], self.cu, self.driver,
+            ops.sample_takeover(m.hidden, pm["W"], self.K, pm["ws_l"], self.cu, self.driver,
                                 self.scan_outs["event_row"], self.u_repl, self.b.eos_id,
                                 self.scan_outs["finished"], row_local=pm["row_local"],
                                 seq_ids=m.seq_ids, token=self.repl)
@@ -148,7 +151,11 @@ def time_source_split(batch, step, dev, reps):
     g.manual_seed(int(np.random.SeedSequence([0, batch.cfg.id, 30]).generate_state(1)[0]))
     hs = torch.randn(M, Hd, generator=g, device=dev)
     hs = (hs / hs.pow(2).mean(1, keepdim=True).sqrt()).to(m.hidden.dtype)
-    Ws = (torch.randn(V, Hd, generator=g, device=dev) * batch.cfg.w_std).to(m.W.dtype)
+    # the LM heads read the tiled copies; the gathers, which read single
+    # random rows, read the row-major ones (half of every line of a tiled row
+    # belongs to its neighbour row)
+    Ws_rm = (torch.randn(V, Hd, generator=g, device=dev) * batch.cfg.w_std).to(m.W.dtype)
+    Ws = ops.lmhead_pack_w(Ws_rm)
     ws = torch.empty(ops.lmhead_workspace_size(M, Hd, V, K), dtype=torch.uint8, device=dev)
     s = ops.lmhead_logsoftmax_verify(hs, Ws, torch.zeros(M, dtype=torch.int32, device=dev), K,
                                      workspace=ws)
@@ -159,7 +166,7 @@ def time_source_split(batch, step, dev, reps):
     t_at_s = torch.empty(M, K, device=dev)
 
     def once():
-        ops.lmhead_logp_gather(hs, Ws, s["lse"], t["topk_idx"], out=s_at_t)
+        ops.lmhead_logp_gather(hs, Ws_rm, s["lse"], t["topk_idx"], out=s_at_t)
         ops.lmhead_logp_gather(m.hidden, m.W, t["lse"], s["topk_idx"], out=t_at_s)
         ops.source_split_kl(s["topk_idx"], s["topk_logp"], s_at_t, t["topk_idx"], t["topk_logp"],
                             t_at_s, src, cu=cu)
@@ -207,13 +214,14 @@ def time_propose_step(dev, reps, seed=0):
     lm_outs = None
     u = t(np.minimum(np.random.default_rng(seed).random(M), 1 - 2.0 ** -24), np.float32)
     tok = torch.empty(M, dtype=torch.int32, device=dev)
+    Wp = ops.lmhead_pack_w(m.W)
 
     def once():
         nonlocal lm_outs
         ops.verify_attn_paged(m.q, m.k_new, m.v_new, m.k_pool, m.v_pool, m.page_table, ctx, cu, 1,
                               out=out, workspace=ws_a)
-        lm_outs = ops.lmhead_logsoftmax_verify(m.hidden, m.W, prop, K, outs=lm_outs, workspace=ws_l)
-        ops.lmhead_sample(m.hidden, m.W, K, ws_l, u, token=tok)
+        lm_outs = ops.lmhead_logsoftmax_verify(m.hidden, Wp, prop, K, outs=lm_outs, workspace=ws_l)
+        ops.lmhead_sample(m.hidden, Wp, K, ws_l, u, token=tok)
     for _ in range(3):
         once()
     torch.cuda.synchronize()

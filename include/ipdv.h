@@ -26,6 +26,8 @@
  *                               the verifier's distribution at that row;
  *   lmhead_sample            -- the proposer's per-row draw (temperature 1)
  *                               from the same records;
+ *   lmhead_pack_w            -- W repacked once into 1 KB blocks (optional
+ *                               layout for the calls that read W);
  *   lmhead_logp_gather       -- a model's log-probs at listed vocabulary
  *                               indices (the other model's top-K), which
  *                               complete the union support of Eq. (6);
@@ -75,6 +77,13 @@ typedef enum {
 } ipdv_status;
 
 typedef enum { IPDV_F32 = 0, IPDV_BF16 = 1 } ipdv_dtype;
+
+/* OR'ed into the `dtype` argument of the calls that read the LM-head weight
+ * W (lmhead_logsoftmax_verify, sample_takeover, lmhead_sample,
+ * lmhead_logp_gather): W is in the tiled layout written by lmhead_pack_w
+ * instead of row-major [V, Hd].  bf16 only.  Results are bit-identical to the
+ * row-major call; the GEMM's operand loads then read whole cache lines. */
+#define IPDV_W_TILED 0x10
 
 /* Driver codes (accept_scan): who proposed the window. */
 #define IPDV_DRIVER_S 0   /* the student drives; the teacher verifies */
@@ -364,6 +373,24 @@ int lmhead_sample(const void* hidden, const void* W, int M, int Hd, int V, int K
                   int32_t* token, int dtype, void* hip_stream);
 
 /*
+ * lmhead_pack_w -- W [V, Hd] row-major bf16 -> the tiled layout of IPDV_W_TILED:
+ * [ceil(V/16)][Hd/32][16][32], i.e. element (v, c) at
+ * ((v/16) * (Hd/32) + c/32) * 512 + (v%16) * 32 + c%32, with rows V..16*ceil(V/16)-1
+ * zero.  Each 16-row x 32-channel block is 1 KB contiguous, one pipeline
+ * stage of the LM-head GEMM for 16 vocabulary rows.  Done once per weight
+ * (at load time in an engine); the packed copy then replaces W in the calls
+ * above with dtype IPDV_BF16 | IPDV_W_TILED.
+ *
+ * W_tiled: device buffer of ipdv_lmhead_packed_w_size(V, Hd) bytes, not
+ * aliasing W.  V and Hd follow the LM-head shape rules.
+ *
+ * Errors: IPDV_EINVAL (null or aliasing pointers, shape rules),
+ * IPDV_EUNSUPPORTED (dtype other than IPDV_BF16), IPDV_EHIP.
+ */
+size_t ipdv_lmhead_packed_w_size(int V, int Hd);
+int lmhead_pack_w(const void* W, int V, int Hd, void* W_tiled, int dtype, void* hip_stream);
+
+/*
  * lmhead_logp_gather -- log-softmax of a model's logits at listed vocabulary
  * indices: logp[m, j] = hidden[m] . W[idx[m, j]] - lse[m].  The union support
  * of Eq. (6) needs each model's log-probs at the other model's top-K indices
@@ -435,7 +462,8 @@ int source_split_kl(int M, int K,
  * hook was last set.  Kernels per call: verify_attn_paged 3 (append,
  * attention, split combine), lmhead_logsoftmax_verify 2 (GEMM + epilogue,
  * merge), accept_scan 1, accept_scan_rule 1, sample_takeover 1,
- * lmhead_sample 1, lmhead_logp_gather 1, source_split_kl 1 (+1 with cu).
+ * lmhead_sample 1, lmhead_pack_w 1, lmhead_logp_gather 1, source_split_kl 1
+ * (+1 with cu).
  */
 int ipdv_trace_events(void* const* events, int capacity);
 int ipdv_trace_count(void);

@@ -161,6 +161,17 @@ static int lm_shape_check(int M, int Hd, int V, int K) {
   return IPDV_OK;
 }
 
+// The `dtype` argument of the calls that read W: IPDV_F32 or IPDV_BF16, with
+// IPDV_W_TILED set when W was packed by lmhead_pack_w (bf16 only).
+static int w_dtype(int dtype, bool* bf16, bool* tiled) {
+  const int base = dtype & ~IPDV_W_TILED;
+  *tiled = (dtype & IPDV_W_TILED) != 0;
+  if (base != IPDV_F32 && base != IPDV_BF16) return fail(IPDV_EUNSUPPORTED, "dtype %d", dtype);
+  if (*tiled && base != IPDV_BF16) return fail(IPDV_EUNSUPPORTED, "tiled W is bf16 only");
+  *bf16 = base == IPDV_BF16;
+  return IPDV_OK;
+}
+
 size_t ipdv_lmhead_workspace_size(int M, int Hd, int V, int K) {
   if (lm_shape_check(M, Hd, V, K) != IPDV_OK) return 0;
   return ipdv::lm_plan(M, Hd, V, K, true).workspace_bytes;
@@ -173,17 +184,18 @@ int lmhead_logsoftmax_verify(const void* hidden, const void* W, const int32_t* p
                              size_t workspace_bytes, void* hip_stream) {
   int st = lm_shape_check(M, Hd, V, K);
   if (st != IPDV_OK) return st;
-  if (dtype != IPDV_F32 && dtype != IPDV_BF16) return fail(IPDV_EUNSUPPORTED, "dtype %d", dtype);
+  bool bf16, tiled;
+  if ((st = w_dtype(dtype, &bf16, &tiled)) != IPDV_OK) return st;
   if (M == 0) return ok();
   if (!hidden || !W || !prop_tok || !lse || !logp_prop || !argmax || !topk_idx || !topk_logp)
     return fail(IPDV_EINVAL, "null required pointer");
-  const ipdv::LmPlan pl = ipdv::lm_plan(M, Hd, V, K, dtype == IPDV_BF16);
+  const ipdv::LmPlan pl = ipdv::lm_plan(M, Hd, V, K, bf16);
   const size_t need = ipdv::lm_plan(M, Hd, V, K, true).workspace_bytes;
   if (!workspace || workspace_bytes < need)
     return fail(IPDV_EWORKSPACE, "workspace of %zu bytes needed (got %zu)", need,
                 workspace ? workspace_bytes : (size_t)0);
   ipdv::LmLaunch L{hidden, W, prop_tok, out_rows, M, Hd, V, K, lse, logp_prop, argmax,
-                   topk_idx, topk_logp, entropy, dtype == IPDV_BF16, workspace};
+                   topk_idx, topk_logp, entropy, bf16, workspace, tiled};
   hipError_t e = ipdv::launch_lmhead(L, pl, reinterpret_cast<hipStream_t>(hip_stream));
   if (e != hipSuccess) return hip_fail("lmhead_logsoftmax_verify launch", e);
   return ok();
@@ -196,19 +208,20 @@ int sample_takeover(const void* hidden, const void* W, int M, int Hd, int V, int
                     uint8_t* finished, int dtype, void* hip_stream) {
   int st = lm_shape_check(M, Hd, V, K);
   if (st != IPDV_OK) return st;
-  if (dtype != IPDV_F32 && dtype != IPDV_BF16) return fail(IPDV_EUNSUPPORTED, "dtype %d", dtype);
+  bool bf16, tiled;
+  if ((st = w_dtype(dtype, &bf16, &tiled)) != IPDV_OK) return st;
   if (n_seq < 0) return fail(IPDV_EINVAL, "n_seq must be >= 0 (got %d)", n_seq);
   if (n_seq > 65535 * 32) return fail(IPDV_EUNSUPPORTED, "n_seq too large");
   if (n_seq == 0) return ok();
   if (!hidden || !W || !cu_q || !driver || !event_row || !u || !token || !finished)
     return fail(IPDV_EINVAL, "null required pointer");
-  const ipdv::LmPlan pl = ipdv::lm_plan(M, Hd, V, K, dtype == IPDV_BF16);
+  const ipdv::LmPlan pl = ipdv::lm_plan(M, Hd, V, K, bf16);
   const size_t need = ipdv::lm_plan(M, Hd, V, K, true).workspace_bytes;
   if (!workspace || workspace_bytes < need)
     return fail(IPDV_EWORKSPACE, "workspace of %zu bytes needed (got %zu)", need,
                 workspace ? workspace_bytes : (size_t)0);
   ipdv::SampleLaunch L{hidden, W, M, Hd, V, K, workspace, seq_ids, n_seq, cu_q, driver, event_row,
-                       row_local, u, eos_id, token, finished, dtype == IPDV_BF16};
+                       row_local, u, eos_id, token, finished, bf16, tiled};
   hipError_t e = ipdv::launch_sample_takeover(L, pl, reinterpret_cast<hipStream_t>(hip_stream));
   if (e != hipSuccess) return hip_fail("sample_takeover launch", e);
   return ok();
@@ -219,16 +232,17 @@ int lmhead_sample(const void* hidden, const void* W, int M, int Hd, int V, int K
                   int dtype, void* hip_stream) {
   int st = lm_shape_check(M, Hd, V, K);
   if (st != IPDV_OK) return st;
-  if (dtype != IPDV_F32 && dtype != IPDV_BF16) return fail(IPDV_EUNSUPPORTED, "dtype %d", dtype);
+  bool bf16, tiled;
+  if ((st = w_dtype(dtype, &bf16, &tiled)) != IPDV_OK) return st;
   if (M == 0) return ok();
   if (!hidden || !W || !u || !token) return fail(IPDV_EINVAL, "null required pointer");
-  const ipdv::LmPlan pl = ipdv::lm_plan(M, Hd, V, K, dtype == IPDV_BF16);
+  const ipdv::LmPlan pl = ipdv::lm_plan(M, Hd, V, K, bf16);
   const size_t need = ipdv::lm_plan(M, Hd, V, K, true).workspace_bytes;
   if (!workspace || workspace_bytes < need)
     return fail(IPDV_EWORKSPACE, "workspace of %zu bytes needed (got %zu)", need,
                 workspace ? workspace_bytes : (size_t)0);
   ipdv::SampleLaunch L{hidden, W, M, Hd, V, K, workspace, nullptr, 0, nullptr, nullptr, nullptr,
-                       nullptr, u, -1, token, nullptr, dtype == IPDV_BF16};
+                       nullptr, u, -1, token, nullptr, bf16, tiled};
   hipError_t e = ipdv::launch_sample_rows(L, pl, reinterpret_cast<hipStream_t>(hip_stream));
   if (e != hipSuccess) return hip_fail("lmhead_sample launch", e);
   return ok();
@@ -280,12 +294,29 @@ int lmhead_logp_gather(const void* hidden, const void* W, int M, int Hd, int V,
   if (st != IPDV_OK) return st;
   if (n_idx < 0 || n_idx > IPDV_MAX_GATHER)
     return fail(IPDV_EINVAL, "n_idx=%d must be in [0, %d]", n_idx, IPDV_MAX_GATHER);
-  if (dtype != IPDV_F32 && dtype != IPDV_BF16) return fail(IPDV_EINVAL, "unknown dtype %d", dtype);
+  bool bf16, tiled;
+  if ((st = w_dtype(dtype, &bf16, &tiled)) != IPDV_OK) return st;
   if (M == 0 || n_idx == 0) return ok();
   if (!hidden || !W || !lse || !idx || !logp) return fail(IPDV_EINVAL, "null required pointer");
-  ipdv::GatherLaunch L{hidden, W, M, Hd, V, lse, idx, n_idx, logp, dtype == IPDV_BF16};
+  ipdv::GatherLaunch L{hidden, W, M, Hd, V, lse, idx, n_idx, logp, bf16, tiled};
   hipError_t e = ipdv::launch_logp_gather(L, reinterpret_cast<hipStream_t>(hip_stream));
   if (e != hipSuccess) return hip_fail("lmhead_logp_gather launch", e);
+  return ok();
+}
+
+size_t ipdv_lmhead_packed_w_size(int V, int Hd) {
+  if (lm_shape_check(0, Hd, V, 1) != IPDV_OK) return 0;
+  return (size_t)((V + 15) / 16) * 16 * Hd * 2;
+}
+
+int lmhead_pack_w(const void* W, int V, int Hd, void* W_tiled, int dtype, void* hip_stream) {
+  int st = lm_shape_check(0, Hd, V, 1);
+  if (st != IPDV_OK) return st;
+  if (dtype != IPDV_BF16) return fail(IPDV_EUNSUPPORTED, "tiled W is bf16 only (dtype %d)", dtype);
+  if (!W || !W_tiled) return fail(IPDV_EINVAL, "null required pointer");
+  if (W == W_tiled) return fail(IPDV_EINVAL, "W_tiled must not alias W");
+  hipError_t e = ipdv::launch_pack_w(W, V, Hd, W_tiled, reinterpret_cast<hipStream_t>(hip_stream));
+  if (e != hipSuccess) return hip_fail("lmhead_pack_w launch", e);
   return ok();
 }
 

@@ -84,6 +84,7 @@ struct LmLaunch {
   float* entropy;
   bool dtype_bf16;
   void* workspace;
+  bool w_tiled = false;        // W packed by lmhead_pack_w
 };
 
 LmPlan lm_plan(int M, int Hd, int V, int K, bool bf16);
@@ -105,6 +106,7 @@ struct SampleLaunch {
   int32_t* token;
   uint8_t* finished;
   bool dtype_bf16;
+  bool w_tiled = false;
 };
 
 hipError_t launch_sample_takeover(const SampleLaunch& L, const LmPlan& pl, hipStream_t st);
@@ -121,7 +123,11 @@ struct GatherLaunch {
   int n;
   float* logp;                 // [M, n]
   bool dtype_bf16;
+  bool w_tiled = false;
 };
+
+// ---- W in 16-row x 32-channel blocks (bf16) ----
+hipError_t launch_pack_w(const void* W, int V, int Hd, void* W_tiled, hipStream_t st);
 
 hipError_t launch_logp_gather(const GatherLaunch& L, hipStream_t st);
 

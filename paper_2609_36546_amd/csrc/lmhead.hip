@@ -44,6 +44,7 @@ struct LmParams {
   const int32_t* prop_tok;
   const int32_t* out_rows;
   int M, Hd, V, K;
+  int w_tiled;        // W in 16-row x 32-channel blocks (lmhead_pack_w), else [V][Hd]
   int n_groups, n_rt, n_vt;
   // Group records, [M][n_groups] each: the three largest logits of the group
   // with their indices, the fourth largest value, sum exp(l - v1) over each
@@ -65,6 +66,14 @@ struct LmParams {
   float* topk_logp;
   float* entropy;
 };
+
+// Element offset of W[v][c]: row-major [V][Hd], or tiled in 1 KB blocks of
+// 16 rows x 32 channels, [ceil(V/16)][Hd/32][16][32] (lmhead_pack_w).  A
+// 16-byte chunk (8 channels from a multiple of 8) is contiguous either way.
+__device__ __forceinline__ size_t w_off(const LmParams& p, int v, int c) {
+  return p.w_tiled ? ((size_t)(v >> 4) * (p.Hd >> 5) + (c >> 5)) * 512 + (v & 15) * 32 + (c & 31)
+                   : (size_t)v * p.Hd + c;
+}
 
 // MFMA flavour per input type.  STAGE = hidden channels per pipeline stage;
 // a lane supplies its k-step operand from channels koff(ks, h) of the stage
@@ -386,8 +395,16 @@ __global__ __launch_bounds__(256) void lmhead_gemm_dlds_kernel(LmParams p) {
     const int r = (u < kVT / 16 ? 16 * u : 16 * (u - kVT / 16)) + (lane >> 2);
     const int c = (lane & 3) ^ ((r >> 2) & 3);
     if (u < kVT / 16) {
-      const int v = min(v0 + r, p.V - 1);       // rows past V: any valid row, masked later
-      src[j] = Wp + (size_t)v * p.Hd + 8 * c;
+      if (p.w_tiled) {
+        // the stage's 16 rows x 32 channels are one 1 KB block; the lane takes
+        // the same row and (swizzled) chunk as in the row-major case, so the
+        // LDS image is identical.  Blocks past V: any valid block, masked later.
+        const int vb = min((v0 >> 4) + u, ((p.V + 15) >> 4) - 1);
+        src[j] = Wp + (size_t)vb * (p.Hd >> 5) * 512 + (lane >> 2) * 32 + 8 * c;
+      } else {
+        const int v = min(v0 + r, p.V - 1);     // rows past V: any valid row, masked later
+        src[j] = Wp + (size_t)v * p.Hd + 8 * c;
+      }
     } else {
       const int m = min(m0 + r, p.M - 1);       // rows past M: any valid row, never stored
       src[j] = Hp + (size_t)m * p.Hd + 8 * c;
@@ -397,11 +414,14 @@ __global__ __launch_bounds__(256) void lmhead_gemm_dlds_kernel(LmParams p) {
   // one into a free buffer, so that every wave has the same number of loads
   // in flight at every boundary.  dma(st, j0, j1): this wave's load blocks
   // [j0, j1) of stage st.
+  // Load blocks j < kVT / 64 are W (for every wave); a stage advances a tiled
+  // W block by 512 elements per 32 channels.
+  const int wk = p.w_tiled ? 16 : 1;
   auto dma = [&](int st, int j0, int j1) {
     char* buf = s_ring + (st % NBUF) * SB;
     const int k0 = min(st, nst - 1) * kDStage;
 #pragma unroll
-    for (int j = j0; j < j1; ++j) dma16(src[j] + k0, buf + 1024 * (w + 4 * j));
+    for (int j = j0; j < j1; ++j) dma16(src[j] + (j < kVT / 64 ? wk * k0 : k0), buf + 1024 * (w + 4 * j));
   };
   // Operand offsets of this lane within a stage.  Chunk 2 ks + h of a row sits
   // at 16 ((2 ks + h) ^ q), q = row bits 2-3, which is the ks = 0 offset xor
@@ -643,7 +663,7 @@ __device__ void recompute_entries(const LmParams& p, const float* s_hid, int n, 
         for (int i = 0; i < NP; ++i) {
           // out-of-range rows and channels load a valid chunk; it is masked below
           const int c = min(c0 + EPL * (lane + kWave * i), p.Hd - EPL);
-          w[b][i] = ld16<frag>(Wp + (size_t)min(vv[b], p.V - 1) * p.Hd + c);
+          w[b][i] = ld16<frag>(Wp + w_off(p, min(vv[b], p.V - 1), c));
         }
 #pragma unroll
       for (int i = 0; i < NP; ++i) {
@@ -717,12 +737,12 @@ __global__ __launch_bounds__(kMT) void lmhead_merge_kernel(LmParams p) {
   frag ph[NPC], pw[NPC];
   {
     const DT* hr = reinterpret_cast<const DT*>(p.hidden) + (size_t)m * p.Hd;
-    const DT* wr = reinterpret_cast<const DT*>(p.W) + (size_t)(pok ? pv : 0) * p.Hd;
+    const DT* wr = reinterpret_cast<const DT*>(p.W);
 #pragma unroll
     for (int u = 0; u < NPC; ++u) {
       const int k = min(EPL * (tid + kMT * u), p.Hd - EPL);   // past Hd: masked below
       ph[u] = ld16<frag>(hr + k);
-      pw[u] = ld16<frag>(wr + k);
+      pw[u] = ld16<frag>(wr + w_off(p, pok ? pv : 0, k));
     }
   }
 
@@ -1199,6 +1219,7 @@ LmParams lm_params(const void* hidden, const void* W, int M, int Hd, int V, int 
 hipError_t launch_lmhead(const LmLaunch& L, const LmPlan& pl, hipStream_t st) {
   if (L.M == 0) return hipSuccess;
   LmParams p = lm_params(L.hidden, L.W, L.M, L.Hd, L.V, L.K, pl, L.workspace);
+  p.w_tiled = L.w_tiled ? 1 : 0;
   p.prop_tok = L.prop_tok;
   p.out_rows = L.out_rows;
   p.lse = L.lse;
@@ -1256,6 +1277,7 @@ hipError_t launch_logp_gather(const GatherLaunch& L, hipStream_t st) {
   p.M = L.M;
   p.Hd = L.Hd;
   p.V = L.V;
+  p.w_tiled = L.w_tiled ? 1 : 0;
   trace_begin(st);
   if (L.dtype_bf16)
     hipLaunchKernelGGL((logp_gather_kernel<bf16>), dim3(L.M), dim3(kMT), 0, st, p, L.lse, L.idx,
@@ -1270,7 +1292,8 @@ hipError_t launch_logp_gather(const GatherLaunch& L, hipStream_t st) {
 
 hipError_t launch_sample_rows(const SampleLaunch& L, const LmPlan& pl, hipStream_t st) {
   if (L.M == 0) return hipSuccess;
-  const LmParams p = lm_params(L.hidden, L.W, L.M, L.Hd, L.V, L.K, pl, const_cast<void*>(L.workspace));
+  LmParams p = lm_params(L.hidden, L.W, L.M, L.Hd, L.V, L.K, pl, const_cast<void*>(L.workspace));
+  p.w_tiled = L.w_tiled ? 1 : 0;
   SampleParams s{};
   s.u = L.u;
   s.token = L.token;
@@ -1286,7 +1309,8 @@ hipError_t launch_sample_rows(const SampleLaunch& L, const LmPlan& pl, hipStream
 
 hipError_t launch_sample_takeover(const SampleLaunch& L, const LmPlan& pl, hipStream_t st) {
   if (L.n_seq == 0) return hipSuccess;
-  const LmParams p = lm_params(L.hidden, L.W, L.M, L.Hd, L.V, L.K, pl, const_cast<void*>(L.workspace));
+  LmParams p = lm_params(L.hidden, L.W, L.M, L.Hd, L.V, L.K, pl, const_cast<void*>(L.workspace));
+  p.w_tiled = L.w_tiled ? 1 : 0;
   const SampleParams s{L.seq_ids, L.cu_q, L.driver, L.event_row, L.row_local, L.u, L.eos_id, L.token,
                        L.finished};
   trace_begin(st);
@@ -1294,6 +1318,39 @@ hipError_t launch_sample_takeover(const SampleLaunch& L, const LmPlan& pl, hipSt
     hipLaunchKernelGGL((sample_kernel<bf16, false>), dim3(L.n_seq), dim3(kMT), 0, st, p, s);
   else
     hipLaunchKernelGGL((sample_kernel<float, false>), dim3(L.n_seq), dim3(kMT), 0, st, p, s);
+  const hipError_t e = hipGetLastError();
+  trace_mark(st);
+  return e;
+}
+
+namespace {
+
+// W [V][Hd] -> [ceil(V/16)][Hd/32][16][32]: one thread per 16-byte chunk of
+// the output, in output order (rows past V are zero).
+__global__ __launch_bounds__(256) void pack_w_kernel(const bf16* W, int V, int Hd, bf16* Wt,
+                                                     size_t n_chunks) {
+  const size_t t = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (t >= n_chunks) return;
+  const size_t blk = t >> 6;                 // 64 chunks per 1 KB block
+  const int within = (int)(t & 63);
+  const int nb_c = Hd >> 5;
+  const int v = (int)(blk / nb_c) * 16 + (within >> 2);
+  const int c = (int)(blk % nb_c) * 32 + (within & 3) * 8;
+  typedef __attribute__((__vector_size__(16))) int i32x4;
+  i32x4 x = {0, 0, 0, 0};
+  if (v < V) x = ld16<i32x4>(W + (size_t)v * Hd + c);
+  *reinterpret_cast<i32x4*>(Wt + t * 8) = x;
+}
+
+}  // namespace
+
+hipError_t launch_pack_w(const void* W, int V, int Hd, void* W_tiled, hipStream_t st) {
+  const size_t n_chunks = (size_t)((V + 15) / 16) * 16 * Hd / 8;
+  if (n_chunks == 0) return hipSuccess;
+  trace_begin(st);
+  hipLaunchKernelGGL(pack_w_kernel, dim3((unsigned)((n_chunks + 255) / 256)), dim3(256), 0, st,
+                     reinterpret_cast<const bf16*>(W), V, Hd, reinterpret_cast<bf16*>(W_tiled),
+                     n_chunks);
   const hipError_t e = hipGetLastError();
   trace_mark(st);
   return e;

@@ -61,6 +61,10 @@ def lib() -> ctypes.CDLL:
         L.accept_scan_rule.restype = ci
         L.lmhead_sample.argtypes = [vp, vp, ci, ci, ci, ci, vp, cs, f32p, i32p, ci, vp]
         L.lmhead_sample.restype = ci
+        L.ipdv_lmhead_packed_w_size.argtypes = [ci, ci]
+        L.ipdv_lmhead_packed_w_size.restype = cs
+        L.lmhead_pack_w.argtypes = [vp, ci, ci, vp, ci, vp]
+        L.lmhead_pack_w.restype = ci
         L.lmhead_logp_gather.argtypes = [vp, vp, ci, ci, ci, f32p, i32p, ci, f32p, ci, vp]
         L.lmhead_logp_gather.restype = ci
         L.source_split_kl.argtypes = [ci, ci, i32p, f32p, f32p, i32p, f32p, f32p, u8p, ci, ci,
@@ -204,6 +208,56 @@ def lmhead_workspace_size(M, Hd, V, K) -> int:
     return int(lib().ipdv_lmhead_workspace_size(M, Hd, V, K))
 
 
+W_TILED = 0x10
+
+
+class PackedW:
+    """The LM-head weight in the tiled layout written by lmhead_pack_w (see
+    include/ipdv.h): ``data`` is the flat bf16 buffer; ``V`` and ``Hd`` the
+    logical shape.  Accepted wherever a row-major W is."""
+
+    def __init__(self, data, V: int, Hd: int):
+        self.data, self.V, self.Hd = data, int(V), int(Hd)
+
+    @property
+    def device(self):
+        return self.data.device
+
+    @property
+    def dtype(self):
+        return self.data.dtype
+
+
+def lmhead_pack_w(W) -> PackedW:
+    """Repack a row-major bf16 W [V, Hd] into the tiled layout (one launch)."""
+    dev = W.device
+    _need(W, "W", torch.bfloat16, dev, 2)
+    V, Hd = W.shape
+    n = int(lib().ipdv_lmhead_packed_w_size(V, Hd))
+    if n == 0:
+        raise ValueError(f"unsupported LM-head shape V={V} Hd={Hd}")
+    data = torch.empty(n // 2, dtype=torch.bfloat16, device=dev)
+    st = lib().lmhead_pack_w(_ptr(W), V, Hd, _ptr(data), _dtype_code(torch.bfloat16), _stream(dev))
+    _check("lmhead_pack_w", st)
+    return PackedW(data, V, Hd)
+
+
+def _w_arg(W, dt, dev, Hd):
+    """(pointer, V, dtype code) for a row-major W [V, Hd] or a PackedW."""
+    if isinstance(W, PackedW):
+        if W.dtype != torch.bfloat16 or dt != torch.bfloat16:
+            raise ValueError("a packed W needs bf16 hidden rows and weights")
+        if W.device != dev:
+            raise ValueError(f"W must be on {dev}")
+        if W.Hd != Hd:
+            raise ValueError("packed W has another hidden size")
+        return _ptr(W.data), W.V, _dtype_code(dt) | W_TILED
+    _need(W, "W", dt, dev, 2)
+    if W.shape[1] != Hd:
+        raise ValueError("W must be [V, Hd]")
+    return _ptr(W), W.shape[0], _dtype_code(dt)
+
+
 def lmhead_logsoftmax_verify(hidden, W, prop_tok, K: int, out_rows=None, n_out_rows=None,
                              with_entropy: bool = True, outs=None, workspace=None):
     """Verifier log-softmax outputs for each row (see include/ipdv.h).
@@ -215,11 +269,8 @@ def lmhead_logsoftmax_verify(hidden, W, prop_tok, K: int, out_rows=None, n_out_r
     dev = hidden.device
     dt = hidden.dtype
     _need(hidden, "hidden", dt, dev, 2)
-    _need(W, "W", dt, dev, 2)
     M, Hd = hidden.shape
-    V = W.shape[0]
-    if W.shape[1] != Hd:
-        raise ValueError("W must be [V, Hd]")
+    w_ptr, V, code = _w_arg(W, dt, dev, Hd)
     _need(prop_tok, "prop_tok", torch.int32, dev, 1)
     if prop_tok.shape[0] != M:
         raise ValueError("prop_tok must be [M]")
@@ -241,9 +292,9 @@ def lmhead_logsoftmax_verify(hidden, W, prop_tok, K: int, out_rows=None, n_out_r
     if workspace is None:
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
     st = lib().lmhead_logsoftmax_verify(
-        _ptr(hidden), _ptr(W), _ptr(prop_tok), _ptr(out_rows), M, Hd, V, K,
+        _ptr(hidden), w_ptr, _ptr(prop_tok), _ptr(out_rows), M, Hd, V, K,
         _ptr(outs["lse"]), _ptr(outs["logp_prop"]), _ptr(outs["argmax"]), _ptr(outs["topk_idx"]),
-        _ptr(outs["topk_logp"]), _ptr(outs["entropy"]), _dtype_code(dt), _ptr(workspace),
+        _ptr(outs["topk_logp"]), _ptr(outs["entropy"]), code, _ptr(workspace),
         workspace.numel() * workspace.element_size(), _stream(dev))
     _check("lmhead_logsoftmax_verify", st)
     return outs
@@ -334,9 +385,8 @@ def sample_takeover(hidden, W, K: int, workspace, cu_q, driver, event_row, u, eo
     dev = hidden.device
     dt = hidden.dtype
     _need(hidden, "hidden", dt, dev, 2)
-    _need(W, "W", dt, dev, 2)
     M, Hd = hidden.shape
-    V = W.shape[0]
+    w_ptr, V, code = _w_arg(W, dt, dev, Hd)
     _need(cu_q, "cu_q", torch.int32, dev, 1)
     B = cu_q.shape[0] - 1
     _need(driver, "driver", torch.uint8, dev, 1)
@@ -352,10 +402,10 @@ def sample_takeover(hidden, W, K: int, workspace, cu_q, driver, event_row, u, eo
     if token is None:
         token = torch.full((B,), -1, dtype=torch.int32, device=dev)
     st = lib().sample_takeover(
-        _ptr(hidden), _ptr(W), M, Hd, V, K, _ptr(workspace),
+        _ptr(hidden), w_ptr, M, Hd, V, K, _ptr(workspace),
         workspace.numel() * workspace.element_size(), _ptr(seq_ids), n_seq, _ptr(cu_q),
         _ptr(driver), _ptr(event_row), _ptr(row_local), _ptr(u), int(eos_id), _ptr(token),
-        _ptr(finished), _dtype_code(dt), _stream(dev))
+        _ptr(finished), code, _stream(dev))
     _check("sample_takeover", st)
     return token
 
@@ -367,9 +417,8 @@ def lmhead_logp_gather(hidden, W, lse, idx, out=None):
     dev = hidden.device
     dt = hidden.dtype
     _need(hidden, "hidden", dt, dev, 2)
-    _need(W, "W", dt, dev, 2)
     M, Hd = hidden.shape
-    V = W.shape[0]
+    w_ptr, V, code = _w_arg(W, dt, dev, Hd)
     _need(lse, "lse", torch.float32, dev, 1)
     _need(idx, "idx", torch.int32, dev, 2)
     if lse.shape[0] != M or idx.shape[0] != M:
@@ -377,8 +426,8 @@ def lmhead_logp_gather(hidden, W, lse, idx, out=None):
     n = idx.shape[1]
     if out is None:
         out = torch.empty(M, n, dtype=torch.float32, device=dev)
-    st = lib().lmhead_logp_gather(_ptr(hidden), _ptr(W), M, Hd, V, _ptr(lse), _ptr(idx), n,
-                                  _ptr(out), _dtype_code(dt), _stream(dev))
+    st = lib().lmhead_logp_gather(_ptr(hidden), w_ptr, M, Hd, V, _ptr(lse), _ptr(idx), n,
+                                  _ptr(out), code, _stream(dev))
     _check("lmhead_logp_gather", st)
     return out
 
@@ -429,16 +478,15 @@ def lmhead_sample(hidden, W, K: int, workspace, u, token=None):
     dev = hidden.device
     dt = hidden.dtype
     _need(hidden, "hidden", dt, dev, 2)
-    _need(W, "W", dt, dev, 2)
     M, Hd = hidden.shape
-    V = W.shape[0]
+    w_ptr, V, code = _w_arg(W, dt, dev, Hd)
     _need(u, "u", torch.float32, dev, 1)
     if u.shape[0] != M:
         raise ValueError("u must be [M]")
     if token is None:
         token = torch.empty(M, dtype=torch.int32, device=dev)
-    st = lib().lmhead_sample(_ptr(hidden), _ptr(W), M, Hd, V, K, _ptr(workspace),
+    st = lib().lmhead_sample(_ptr(hidden), w_ptr, M, Hd, V, K, _ptr(workspace),
                              workspace.numel() * workspace.element_size(), _ptr(u), _ptr(token),
-                             _dtype_code(dt), _stream(dev))
+                             code, _stream(dev))
     _check("lmhead_sample", st)
     return token

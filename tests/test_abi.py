@@ -169,7 +169,9 @@ def test_gather_and_kl_argument_errors():
     bad = list(g); bad[6] = None
     assert L.lmhead_logp_gather(*bad) == -1
     bad = list(g); bad[9] = 7
-    assert L.lmhead_logp_gather(*bad) == -1
+    assert L.lmhead_logp_gather(*bad) == -2          # unknown dtype
+    bad = list(g); bad[9] = 0x10
+    assert L.lmhead_logp_gather(*bad) == -2          # tiled W is bf16 only
     empty = list(g); empty[7] = 0
     assert L.lmhead_logp_gather(*empty) == 0
     # source_split_kl(M, K, s_idx, s_logp, s_at_t, t_idx, t_logp, t_at_s, src, support,
@@ -212,3 +214,24 @@ def test_binding_and_oracle_constants_match_the_header():
                         ("SRC_S", "IPDV_SRC_S"), ("SRC_T", "IPDV_SRC_T"),
                         ("SRC_DISCARDED", "IPDV_SRC_DISCARDED")):
         assert getattr(oracle, name) == defs[macro], name
+
+
+def test_tiled_w_argument_errors():
+    L = ops.lib()
+    vp = ctypes.c_void_p
+    L.ipdv_lmhead_packed_w_size.argtypes = [ctypes.c_int, ctypes.c_int]
+    L.ipdv_lmhead_packed_w_size.restype = ctypes.c_size_t
+    assert L.ipdv_lmhead_packed_w_size(151936, 2048) == 151936 * 2048 * 2
+    assert L.ipdv_lmhead_packed_w_size(100, 64) == 112 * 64 * 2     # rows padded to 16
+    assert L.ipdv_lmhead_packed_w_size(100, 100) == 0                # Hd not a multiple of 64
+    assert L.lmhead_pack_w(vp(1), 100, 64, vp(2), 0, None) == -2     # fp32: unsupported
+    assert L.lmhead_pack_w(None, 100, 64, vp(2), 1, None) == -1
+    assert L.lmhead_pack_w(vp(1), 100, 64, vp(1), 1, None) == -1     # aliasing
+    assert L.lmhead_pack_w(vp(1), 0, 64, vp(2), 1, None) == -1       # V < 1
+    # fp32 with the tiled flag is refused by every call that reads W
+    args = dict(M=4, Hd=64, V=100, K=4)
+    st = L.lmhead_logsoftmax_verify(vp(1), vp(1), vp(1), None, 4, 64, 100, 4, vp(1), vp(1),
+                                    vp(1), vp(1), vp(1), None, 0x10, vp(1), 1 << 30, None)
+    assert st == -2
+    st = L.lmhead_sample(vp(1), vp(1), 4, 64, 100, 4, vp(1), 1 << 30, vp(1), vp(1), 0x10, None)
+    assert st == -2
