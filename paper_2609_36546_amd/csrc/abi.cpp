@@ -7,6 +7,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstdlib>
+#include <cstring>
 
 #include "../../include/ipdv.h"
 #include "kernels.h"
@@ -69,6 +70,17 @@ int attn_sub_tokens() {
     int x = s ? atoi(s) : 0;
     if (x < 32 || x > 1024 || x % 32 != 0) x = 0;
     return x;
+  }();
+  return v;
+}
+
+// IPDV_ATTN_KERNEL=regs keeps full 64-row groups on the register kernel
+// (A/B timing sweeps only); by default they take the persistent stream-K
+// kernel.
+bool attn_sk_enabled() {
+  static bool v = [] {
+    const char* s = getenv("IPDV_ATTN_KERNEL");
+    return !(s && strcmp(s, "regs") == 0);
   }();
   return v;
 }

@@ -36,4 +36,17 @@ template <typename T> __device__ __forceinline__ T from_f32(float x);
 template <> __device__ __forceinline__ float from_f32<float>(float x) { return x; }
 template <> __device__ __forceinline__ bf16 from_f32<bf16>(float x) { return static_cast<bf16>(x); }
 
+// One 16-byte direct-to-LDS load: lane i's bytes land at lds + 16 i (M0 holds
+// the wave-uniform LDS address).  Written as inline assembly so the compiler
+// does not add its own whole-queue waits before every LDS read: the ring's
+// explicit vmcnt wait + barrier order the accesses.  Compiler-generated waits
+// for its own loads stay correct, as vmcnt retires loads in issue order.
+__device__ __forceinline__ void dma16(const void* src, char* lds) {
+  const unsigned lds_addr = (unsigned)(uintptr_t)(__attribute__((address_space(3))) void*)lds;
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off"
+               :
+               : "s"(__builtin_amdgcn_readfirstlane(lds_addr)), "v"(src)
+               : "memory", "m0");
+}
+
 }  // namespace ipdv

@@ -38,7 +38,9 @@ struct AttnPlan {
   int sub;             // keys per wave
   int chunk;           // keys per workgroup
   int max_chunks;      // chunk slots per group (padded to a multiple of 8)
+  int sk;              // full 64-row groups of 16-slot D = 128 pages: persistent stream-K kernel (bf16)
   size_t part_o_bytes, part_lse_bytes, workspace_bytes;
+  size_t sk_o_bytes, sk_lse_bytes;   // stream-K partial layout (when sk)
 };
 
 struct AttnLaunch {
@@ -61,6 +63,7 @@ struct AttnLaunch {
 };
 
 int attn_sub_tokens();
+bool attn_sk_enabled();
 AttnPlan attn_plan(int n_seq, int Hq, int Hkv, int D, int max_q, int max_pages, int page_size);
 hipError_t launch_verify_attn(const AttnLaunch& L, const AttnPlan& pl, hipStream_t st);
 

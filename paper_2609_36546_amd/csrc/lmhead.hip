@@ -348,19 +348,6 @@ constexpr int kDStage = 32;   // hidden channels per stage (64 bytes per row)
 
 __device__ __forceinline__ int dl_off(int r, int c) { return 64 * r + 16 * (c ^ ((r >> 2) & 3)); }
 
-// One 16-byte direct-to-LDS load: lane i's bytes land at lds + 16 i (M0 holds
-// the wave-uniform LDS address).  Written as inline assembly so the compiler
-// does not add its own whole-queue waits before every LDS read: the ring's
-// explicit vmcnt wait + barrier order the accesses.  Compiler-generated waits
-// for its own loads stay correct, as vmcnt retires loads in issue order.
-__device__ __forceinline__ void dma16(const void* src, char* lds) {
-  const unsigned lds_addr = (unsigned)(uintptr_t)(__attribute__((address_space(3))) void*)lds;
-  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off"
-               :
-               : "s"(__builtin_amdgcn_readfirstlane(lds_addr)), "v"(src)
-               : "memory", "m0");
-}
-
 template <int RB, int NBUF>
 __global__ __launch_bounds__(256) void lmhead_gemm_dlds_kernel(LmParams p) {
   static_assert(NBUF >= 3 && NBUF <= 5, "ring depth");

@@ -36,6 +36,15 @@
 // chunks of one (sequence, head group) are merged by a combine kernel in
 // log-sum-exp form, unless the sequence fits in one chunk (then the
 // workgroup writes the output itself).
+//
+// Full 64-row groups of bf16 D = 128 heads in 16-token pages (the teacher
+// shapes) take a second kernel, verify_attn_sk_kernel below: persistent
+// workgroups, one 16-row tile per wave, keys streamed through an LDS ring
+// with direct-to-LDS loads, and the key blocks of all groups split evenly
+// between workgroups (stream-K).  Both kernels share the block arithmetic
+// (attend_block) and the pool layouts.
+#include <algorithm>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -67,6 +76,8 @@ struct AttnParams {
   int chunk, sub;     // keys per workgroup chunk / per wave
   int max_chunks, n_qg, n_seq;
   float scale_log2;   // softmax scale * log2(e)
+  int32_t* sk_start;  // stream-K: first block of every item (written by the attention kernel)
+  int sk_grid;        // stream-K: persistent workgroups
 };
 
 template <typename DT, int D> struct Frags;
@@ -158,9 +169,32 @@ __device__ __forceinline__ void load_block(const AttnParams& a, Frags<DT, D>& f,
 // One 32-key block for every query tile: S^T = K Q^T for all tiles first
 // (independent MFMA chains), then the online softmax in exp2 units with the
 // scale folded into one FMA per score, then O^T += V^T P^T.
-template <typename DT, int D, int QT, bool TAIL>
+// Query fragments: the B operand of the QK product for tile t, k-step ks.
+// LdsQ reads them from the group's rows staged in LDS; RegQ holds one tile's
+// fragments in registers.
+template <typename DT, int D> struct LdsQ;
+template <int D> struct LdsQ<bf16, D> {
+  const bf16* s_q;
+  __device__ __forceinline__ bf16x8 get(int t, int ks) const {
+    const int lane = lane_id();
+    return *reinterpret_cast<const bf16x8*>(s_q + (16 * t + (lane & 15)) * (D + kQPad) + 8 * (lane >> 4) + 32 * ks);
+  }
+};
+template <int D> struct LdsQ<float, D> {
+  const float* s_q;
+  __device__ __forceinline__ float get(int t, int ks) const {
+    const int lane = lane_id();
+    return s_q[(16 * t + (lane & 15)) * (D + kQPad) + (lane >> 4) * (D / 4) + ks];
+  }
+};
+template <int D> struct RegQ {
+  bf16x8 q[D / 32];
+  __device__ __forceinline__ bf16x8 get(int, int ks) const { return q[ks]; }
+};
+
+template <typename DT, int D, int QT, bool TAIL, class QS>
 __device__ __forceinline__ void attend_block(const AttnParams& a, const Frags<DT, D>& f,
-                                             const DT* s_q, const int (&qlimit)[QT],
+                                             const QS& qs, const int (&qlimit)[QT],
                                              int t0, floatx4 (&acc)[QT][D / 16],
                                              float (&m_run)[QT], float (&l_run)[QT]) {
   const int lane = lane_id();
@@ -173,7 +207,7 @@ __device__ __forceinline__ void attend_block(const AttnParams& a, const Frags<DT
     for (int ks = 0; ks < D / 32; ++ks)
 #pragma unroll
       for (int t = 0; t < QT; ++t) {
-        const bf16x8 qv = *reinterpret_cast<const bf16x8*>(s_q + (16 * t + c16) * (D + kQPad) + 8 * j + 32 * ks);
+        const bf16x8 qv = qs.get(t, ks);
 #pragma unroll
         for (int st = 0; st < 2; ++st)
           s[t][st] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f.k[st][ks], qv, s[t][st], 0, 0, 0);
@@ -183,7 +217,7 @@ __device__ __forceinline__ void attend_block(const AttnParams& a, const Frags<DT
     for (int ks = 0; ks < D / 4; ++ks)
 #pragma unroll
       for (int t = 0; t < QT; ++t) {
-        const float qv = s_q[(16 * t + c16) * (D + kQPad) + j * (D / 4) + ks];
+        const float qv = qs.get(t, ks);
 #pragma unroll
         for (int st = 0; st < 2; ++st)
           s[t][st] = __builtin_amdgcn_mfma_f32_16x16x4f32(f.k[st][ks], qv, s[t][st], 0, 0, 0);
@@ -329,6 +363,7 @@ __global__ __launch_bounds__(256) void verify_attn_kernel(AttnParams a) {
       *reinterpret_cast<i32x4*>(s_q + r * (D + kQPad) + EPL * cc) = v;
     }
   }
+  const LdsQ<DT, D> qsrc{s_q};
   int qlimit[QT];   // keys < qlimit are visible to the lane's row of tile t
 #pragma unroll
   for (int t = 0; t < QT; ++t) qlimit[t] = L + min(pr0 + 16 * t + c16, pr_last) / G + 1;
@@ -360,17 +395,17 @@ __global__ __launch_bounds__(256) void verify_attn_kernel(AttnParams a) {
       load_block<DT, D, false>(a, fa, t_begin, n_keys, g, my_page, pbase);
       for (int n = 0; n < nb; n += 2) {
         load_block<DT, D, false>(a, fb, t_begin + kBlk * min(n + 1, nb - 1), n_keys, g, my_page, pbase);
-        attend_block<DT, D, QT, false>(a, fa, s_q, qlimit, t_begin + kBlk * n, acc, m_run, l_run);
+        attend_block<DT, D, QT, false>(a, fa, qsrc, qlimit, t_begin + kBlk * n, acc, m_run, l_run);
         load_block<DT, D, false>(a, fa, t_begin + kBlk * min(n + 2, nb - 1), n_keys, g, my_page, pbase);
         if (n + 1 < nb)
-          attend_block<DT, D, QT, false>(a, fb, s_q, qlimit, t_begin + kBlk * (n + 1), acc, m_run, l_run);
+          attend_block<DT, D, QT, false>(a, fb, qsrc, qlimit, t_begin + kBlk * (n + 1), acc, m_run, l_run);
       }
     }
     // The block that reaches past the last visible key, or needs the causal mask.
     for (int t0 = t_begin + kBlk * nb; t0 < t_end; t0 += kBlk) {
       Frags<DT, D> ft;
       load_block<DT, D, true>(a, ft, t0, n_keys, g, my_page, pbase);
-      attend_block<DT, D, QT, true>(a, ft, s_q, qlimit, t0, acc, m_run, l_run);
+      attend_block<DT, D, QT, true>(a, ft, qsrc, qlimit, t0, acc, m_run, l_run);
     }
   }
 
@@ -469,6 +504,394 @@ __global__ __launch_bounds__(256) void verify_attn_kernel(AttnParams a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Persistent stream-K variant for full 64-row groups (bf16, D = 128, 16-token
+// pages).
+//
+// The register kernel above holds all four 16-row tiles of a group in every
+// wave, so one wave fits per SIMD; and like any kernel of one workgroup per
+// key chunk it leaves a CU's load queue idle while a workgroup starts (page
+// table, query rows, first block) and finishes (partials), and at the ragged
+// end of the grid.  A read-only kernel of the same access pattern (random 4 KB
+// pieces) reaches about 5.4-5.7 TB/s; the chunked kernels stay near 4.4.
+//
+// Here 2 workgroups per CU stay resident.  The 32-key blocks of all items --
+// (sequence, KV head, 64-row group) -- are laid end to end, and workgroup w
+// takes the w-th equal share of them, whatever items it spans.  Its 4 waves
+// each own one 16-row tile (query fragments in registers).  Everything the
+// workgroup reads in its loop arrives through a 3-deep LDS ring of 16 KB
+// units with direct-to-LDS loads: an item's query rows (one unit), then its
+// key/value blocks, then the next item's query rows, and so on.  Each wave
+// issues a quarter of every unit.  The items' lengths and the page ids of the
+// workgroup's blocks are read into LDS before the loop, so the loop issues no
+// other loads and the ring never drains.  An item split between workgroups
+// leaves one partial per piece, at slot item + workgroup, and the combine
+// kernel merges them.
+//
+// LDS image of a key/value unit: [K page 0][K page 1][V page 0][V page 1],
+// each a 4 KB page of the pool in its own layout (keys [D/32][slot][32],
+// values [D][slot]); of a query unit: 64 rows of 256 bytes.  Within every
+// 1 KB piece the 16-byte units are permuted so that the fragment reads of
+// eight consecutive lanes hit eight distinct bank groups: unit (slot, q) of a
+// key piece sits at 4 slot + (q ^ f(slot)), unit (channel, half) of a value
+// piece at 2 channel + (half ^ bit 2 of the channel), unit u of query row r
+// at u ^ (r % 8).  A direct-to-LDS load writes lane l's 16 bytes to unit l,
+// so the loading lane fetches the global unit that belongs there.
+// ---------------------------------------------------------------------------
+constexpr int kSkBuf = 3;              // ring depth (units)
+constexpr int kSkUnit = 16384;         // bytes per unit
+constexpr int kSkMeta = 7680;          // ints of LDS for item tables, sequence data, page ids, unit records
+constexpr int kSkGrid = 512;           // persistent workgroups: 2 per CU
+
+__device__ __forceinline__ int kpiece_unit(int slot, int q) {
+  return 4 * slot + (q ^ (((slot >> 1) & 1) | ((slot >> 2) & 2)));
+}
+__device__ __forceinline__ int vpiece_unit(int ch, int h) { return 2 * ch + (h ^ ((ch >> 2) & 1)); }
+__device__ __forceinline__ int uni(int x) { return __builtin_amdgcn_readfirstlane(x); }
+
+// Item `it` = (sequence slot, KV head g, row group qg), it = (slot Hkv + g) n_qg + qg:
+// the row groups of one (sequence, head) are neighbours, so the shares that
+// read the same keys for them run at the same time and the second read is a
+// cache hit.
+struct SkItem {
+  int slot, g, b, L, r0, pr0, pr_last, n_keys, nb;
+};
+
+__device__ __forceinline__ SkItem sk_item(const AttnParams& a, const int* s_seq, int it, int maxblk) {
+  SkItem m;
+  const int qg = it % a.n_qg;
+  const int sg = it / a.n_qg;
+  m.g = sg % a.Hkv;
+  m.slot = sg / a.Hkv;
+  m.b = s_seq[4 * m.slot];
+  m.L = s_seq[4 * m.slot + 1];
+  m.r0 = s_seq[4 * m.slot + 2];
+  const int rows_total = s_seq[4 * m.slot + 3] * a.G;
+  m.pr0 = qg * kRows;
+  m.pr_last = min(rows_total, m.pr0 + kRows) - 1;
+  m.n_keys = m.L + m.pr_last / a.G + 1;
+  m.nb = m.pr0 < rows_total ? min((m.n_keys + kBlk - 1) / kBlk, maxblk) : 0;
+  return m;
+}
+
+__global__ __launch_bounds__(256, 2) void verify_attn_sk_kernel(AttnParams a) {
+  constexpr int D = 128;
+  constexpr int PS = 16;
+  const int tid = threadIdx.x;
+  const int t = tid / kWave;           // row tile
+  const int lane = lane_id();
+  const int c16 = lane & 15, j = lane >> 4;
+  const int n_it = a.n_seq * a.Hkv * a.n_qg;
+  const int maxblk = (a.max_pages * PS + kBlk - 1) / kBlk;
+
+  __shared__ __attribute__((aligned(1024))) char s_ring[kSkBuf * kSkUnit];
+  __shared__ int s_meta[kSkMeta];
+  __shared__ int s_part[2][256];
+  if (2 * (n_it + 1) + 4 * a.n_seq > kSkMeta) return;   // the host sizes every launch to fit
+  int* s_start = s_meta;                    // [n_it + 1] first block of each item
+  int* s_ne = s_start + n_it + 1;           // [n_it + 1] non-empty items before each item
+  int* s_seq = s_ne + n_it + 1;             // [n_seq][4]: b, L, r0, rows
+  int* s_pg = s_seq + 4 * a.n_seq;          // [2 per block]: page ids of this workgroup's blocks
+
+  // Sequence data, then every item's block count, and the exclusive scans of
+  // the block counts and of the non-empty flags.
+  for (int sl = tid; sl < a.n_seq; sl += 256) {
+    const int b = a.seq_ids ? a.seq_ids[sl] : sl;
+    const int r0 = a.cu_q[b];
+    s_seq[4 * sl] = b;
+    s_seq[4 * sl + 1] = max(a.ctx_lens[b], 0);
+    s_seq[4 * sl + 2] = r0;
+    s_seq[4 * sl + 3] = a.cu_q[b + 1] - r0;
+  }
+  __syncthreads();
+  const int per = (n_it + 255) / 256;
+  const int i_lo = min(n_it, tid * per), i_hi = min(n_it, (tid + 1) * per);
+  {
+    int run = 0, cnt = 0;
+    for (int i = i_lo; i < i_hi; ++i) {
+      const int nb = sk_item(a, s_seq, i, maxblk).nb;
+      run += nb;
+      cnt += nb > 0;
+    }
+    s_part[0][tid] = run;
+    s_part[1][tid] = cnt;
+  }
+  __syncthreads();
+  if (t < 2) {
+    // 256 partial sums, 4 per lane: exclusive scan across the wave
+    int v[4], tot = 0;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) { v[e] = s_part[t][4 * lane + e]; tot += v[e]; }
+    int inc = tot;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+      const int y = __shfl_up(inc, o, kWave);
+      if (lane >= o) inc += y;
+    }
+    int ex = inc - tot;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) { s_part[t][4 * lane + e] = ex; ex += v[e]; }
+  }
+  __syncthreads();
+  {
+    int bs = s_part[0][tid], ns = s_part[1][tid];
+    for (int i = i_lo; i < i_hi; ++i) {
+      s_start[i] = bs;
+      s_ne[i] = ns;
+      const int nb = sk_item(a, s_seq, i, maxblk).nb;
+      bs += nb;
+      ns += nb > 0;
+    }
+    if (tid == 255) { s_start[n_it] = bs; s_ne[n_it] = ns; }   // thread 255 ends at n_it or owns no items
+  }
+  __syncthreads();
+  const int B_tot = s_start[n_it];
+  if (blockIdx.x == 0)
+    for (int i = tid; i <= n_it; i += 256) a.sk_start[i] = s_start[i];
+  const int W = min((int)gridDim.x, B_tot);
+  const int w = blockIdx.x;
+  if (w >= W) return;
+  const int lo = (int)((long)B_tot * w / W), hi = (int)((long)B_tot * (w + 1) / W);
+  // Item of block x: s_start[i] <= x < s_start[i + 1] (empty items never qualify).
+  auto item_of = [&](int x) {
+    int l0 = 0, l1 = n_it - 1;
+    while (l0 < l1) {
+      const int mid = (l0 + l1 + 1) >> 1;
+      if (s_start[mid] <= x) l0 = mid; else l1 = mid - 1;
+    }
+    return l0;
+  };
+  const int i_first = uni(item_of(lo)), i_last = uni(item_of(hi - 1));
+  const int n_units = (hi - lo) + s_ne[i_last + 1] - s_ne[i_first];
+  if (2 * (n_it + 1) + 4 * a.n_seq + 2 * (hi - lo) + n_units > kSkMeta) return;
+  int* s_uq = s_pg + 2 * (hi - lo);          // [n_units] the workgroup's units, in order
+  // Unit records: a query unit holds 4 item + 1; a key/value unit holds
+  // 4 x + 2 (last block of the item's piece) with x the block's offset in the
+  // share.  Block x of item i is unit (x - lo) + (non-empty items from
+  // i_first through i); the unit before an item's first block is its query.
+  for (int x = lo + tid; x < hi; x += 256) {
+    const int i = item_of(x);
+    const int u = (x - lo) + s_ne[i + 1] - s_ne[i_first];
+    const int last = (x + 1 == s_start[i + 1] || x + 1 == hi) ? 2 : 0;
+    s_uq[u] = 4 * (x - lo) + last;
+    if (x == max(lo, s_start[i])) s_uq[u - 1] = 4 * i + 1;
+    const SkItem m = sk_item(a, s_seq, i, maxblk);
+    const int* pt_row = a.page_table + (size_t)m.b * a.max_pages;
+    const int pl = 2 * (x - s_start[i]);
+    s_pg[2 * (x - lo)] = clampi(pt_row[min(pl, a.max_pages - 1)], 0, a.num_pages - 1);
+    s_pg[2 * (x - lo) + 1] = clampi(pt_row[min(pl + 1, a.max_pages - 1)], 0, a.num_pages - 1);
+  }
+  __syncthreads();
+
+  // Lane-fixed parts of this wave's loads: key slice t and value channels
+  // 32t .. 32t+31 of each page; query rows 16t .. 16t+15, four per load.
+  const int ksl = lane >> 2;
+  const int k_src = t * (PS * 32) + ksl * 32 + 8 * ((lane & 3) ^ (((ksl >> 1) & 1) | ((ksl >> 2) & 2)));
+  const int vch = lane >> 1;
+  const int v_src = (32 * t + vch) * PS + 8 * ((lane & 1) ^ ((vch >> 2) & 1));
+  const bf16* kc = reinterpret_cast<const bf16*>(a.k_cache);
+  const bf16* vc = reinterpret_cast<const bf16*>(a.v_cache);
+  const bf16* qp = reinterpret_cast<const bf16*>(a.q);
+
+  // Load side: unit m goes to buffer m % kSkBuf; past the last unit the last
+  // one is loaded again, so that every wait below has the same count.  The
+  // next unit's record and page ids are read one issue ahead.
+  int d_g = 0;                               // KV head of the load side's current item
+  int d_rec = uni(s_uq[0]), d_pg0 = 0, d_pg1 = 0;
+  auto dma_unit = [&](int m) {
+    char* buf = s_ring + (m % kSkBuf) * kSkUnit;
+    if (d_rec & 1) {
+      const SkItem it = sk_item(a, s_seq, d_rec >> 2, maxblk);
+      d_g = it.g;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int r = 16 * t + 4 * u + (lane >> 4);
+        const int pr = min(it.pr0 + r, it.pr_last);
+        const bf16* row = qp + ((size_t)(it.r0 + pr / a.G) * a.Hq + it.g * a.G + pr % a.G) * D;
+        dma16(row + 8 * ((lane & 15) ^ (r & 7)), buf + 1024 * (4 * t + u));
+      }
+    } else {
+      const size_t b0 = (size_t)(d_pg0 * a.Hkv + d_g) * PS * D;
+      const size_t b1 = (size_t)(d_pg1 * a.Hkv + d_g) * PS * D;
+      dma16(kc + b0 + k_src, buf + 1024 * t);
+      dma16(vc + b0 + v_src, buf + 1024 * (8 + t));
+      dma16(kc + b1 + k_src, buf + 1024 * (4 + t));
+      dma16(vc + b1 + v_src, buf + 1024 * (12 + t));
+    }
+    d_rec = uni(s_uq[min(m + 1, n_units - 1)]);
+    if (!(d_rec & 1)) {
+      d_pg0 = uni(s_pg[(d_rec >> 2) * 2]);
+      d_pg1 = uni(s_pg[(d_rec >> 2) * 2 + 1]);
+    }
+  };
+
+  // Per-lane LDS offsets of the MFMA operands within a unit.
+  int k_off[2], v_off[D / 16];
+#pragma unroll
+  for (int st = 0; st < 2; ++st) {
+    const int kk = 8 * (c16 >> 2) + 4 * st + (c16 & 3);
+    k_off[st] = 4096 * (kk >> 4) + 16 * kpiece_unit(kk & 15, j);
+  }
+#pragma unroll
+  for (int dt = 0; dt < D / 16; ++dt) {
+    const int ch = 16 * dt + c16;
+    v_off[dt] = 8192 + 4096 * (j >> 1) + 1024 * (ch >> 5) + 16 * vpiece_unit(ch & 31, j & 1);
+  }
+
+  for (int m = 0; m < kSkBuf - 1; ++m) dma_unit(m);
+
+  // Compute side: the current item's data, set at its query unit.
+  SkItem it{};
+  int c_item = 0;
+  int x0 = 0;          // offset in the share of the item's block 0 (may be negative)
+  bool full = false;   // the whole item lies in this share
+  RegQ<D> qf;
+  int qlimit[1] = {0};
+  int prq = 0;
+  bool has_rows = false;
+  floatx4 acc[1][D / 16];
+  float m_run[1], l_run[1];
+  int c_rec = uni(s_uq[0]);
+  for (int n = 0; n < n_units; ++n) {
+    // Unit n of this wave's loads has landed (the next one may still be in
+    // flight); after the barrier every wave's pieces of it are visible, and
+    // every wave is done with unit n - 1, whose buffer the next issue refills.
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(4 * (kSkBuf - 2)) : "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    dma_unit(n + kSkBuf - 1);
+    const int rec = c_rec;
+    c_rec = uni(s_uq[min(n + 1, n_units - 1)]);
+    const char* buf = s_ring + (n % kSkBuf) * kSkUnit;
+    if (rec & 1) {
+      const int i = rec >> 2;
+      c_item = i;
+      it = sk_item(a, s_seq, i, maxblk);
+      x0 = s_start[i] - lo;
+      full = s_start[i] >= lo && s_start[i + 1] <= hi;
+      prq = it.pr0 + 16 * t + c16;
+      qlimit[0] = it.L + min(prq, it.pr_last) / a.G + 1;
+      has_rows = it.pr0 + 16 * t <= it.pr_last;
+      const int r = 16 * t + c16;
+#pragma unroll
+      for (int ks = 0; ks < D / 32; ++ks) {
+        qf.q[ks] = *reinterpret_cast<const bf16x8*>(buf + 256 * r + 16 * ((j + 4 * ks) ^ (r & 7)));
+        if (prq > it.pr_last) qf.q[ks] = bf16x8{};
+      }
+      m_run[0] = -INFINITY;
+      l_run[0] = 0.f;
+#pragma unroll
+      for (int dt = 0; dt < D / 16; ++dt) acc[0][dt] = floatx4{0.f, 0.f, 0.f, 0.f};
+      continue;
+    }
+    if (!has_rows) continue;
+    const int t0 = kBlk * ((rec >> 2) - x0);
+    const int main_end = min(it.n_keys, it.L & ~(kBlk - 1));
+    Frags<bf16, D> f;
+#pragma unroll
+    for (int st = 0; st < 2; ++st)
+#pragma unroll
+      for (int ks = 0; ks < D / 32; ++ks)
+        f.k[st][ks] = *reinterpret_cast<const bf16x8*>(buf + k_off[st] + 1024 * ks);
+#pragma unroll
+    for (int dt = 0; dt < D / 16; ++dt) f.v[dt] = *reinterpret_cast<const bf16x8*>(buf + v_off[dt]);
+    if (t0 + kBlk <= main_end) {
+      attend_block<bf16, D, 1, false>(a, f, qf, qlimit, t0, acc, m_run, l_run);
+    } else {
+      // Past the last visible key the pages are clamped stand-ins: zero
+      // those value lanes so masked probabilities never meet them.
+      const int vpos = t0 + 8 * j;
+#pragma unroll
+      for (int dt = 0; dt < D / 16; ++dt)
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if (vpos + e >= it.n_keys) f.v[dt][e] = static_cast<bf16>(0.f);
+      attend_block<bf16, D, 1, true>(a, f, qf, qlimit, t0, acc, m_run, l_run);
+    }
+    if (!(rec & 2)) continue;
+    // The item's piece ends here.  A whole item is written out; a piece
+    // leaves a partial at slot item + workgroup.
+    float l_tot = l_run[0] + __shfl_xor(l_run[0], 16, kWave);
+    l_tot += __shfl_xor(l_tot, 32, kWave);
+    const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+    if (prq <= it.pr_last && full) {
+      const int i = prq / a.G, hl = prq % a.G;
+      bf16* orow = reinterpret_cast<bf16*>(a.out) + ((size_t)(it.r0 + i) * a.Hq + it.g * a.G + hl) * D;
+#pragma unroll
+      for (int dt = 0; dt < D / 16; ++dt) {
+        bf16x4 v;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = static_cast<bf16>(acc[0][dt][e] * inv);
+        *reinterpret_cast<bf16x4*>(orow + 16 * dt + 4 * j) = v;
+      }
+    } else if (prq <= it.pr_last) {
+      const size_t ps = (size_t)c_item + w;
+      float* po = a.part_o + (ps * kRows + (16 * t + c16)) * D;
+#pragma unroll
+      for (int dt = 0; dt < D / 16; ++dt) *reinterpret_cast<floatx4*>(po + 16 * dt + 4 * j) = acc[0][dt] * inv;
+      if (j == 0)
+        a.part_lse[ps * kRows + 16 * t + c16] = l_tot > 0.f ? m_run[0] + fast_log2(l_tot) : -INFINITY;
+    }
+  }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // reloads past the end
+}
+
+// Merge the pieces of every item that the stream-K kernel split between
+// workgroups: piece w of item it sits at slot it + w, for the workgroups w
+// whose share of blocks meets the item.
+__global__ __launch_bounds__(256) void attn_combine_sk_kernel(AttnParams a) {
+  constexpr int D = 128;
+  const int qg = blockIdx.x;
+  const int slot = blockIdx.y / a.Hkv, g = blockIdx.y % a.Hkv;
+  const int it = (slot * a.Hkv + g) * a.n_qg + qg;
+  const int n_it = a.n_seq * a.Hkv * a.n_qg;
+  const int B_tot = a.sk_start[n_it];
+  const int s0 = a.sk_start[it], s1 = a.sk_start[it + 1];
+  if (s1 <= s0) return;
+  const int W = min(a.sk_grid, B_tot);
+  // Workgroup whose share [B w / W, B (w+1) / W) holds block x.
+  auto wg_of = [&](int x) { return min(W - 1, (int)(((long)(x + 1) * W - 1) / B_tot)); };
+  const int w0 = wg_of(s0), w1 = wg_of(s1 - 1);
+  if (w0 == w1) return;   // written whole by one workgroup
+  const int b = a.seq_ids ? a.seq_ids[slot] : slot;
+  const int L = max(a.ctx_lens[b], 0);
+  const int r0 = a.cu_q[b];
+  const int kb = a.cu_q[b + 1] - r0;
+  const int G = a.G;
+  const int pr0 = qg * kRows;
+  const int pr_last = min(kb * G, pr0 + kRows) - 1;
+  (void)L;
+  const int r = threadIdx.x / 4;            // packed row within the group
+  const int dq = (threadIdx.x % 4) * (D / 4);
+  const int pr = pr0 + r;
+  if (pr > pr_last) return;
+  float M = -INFINITY;
+  for (int w = w0; w <= w1; ++w) M = fmaxf(M, a.part_lse[((size_t)it + w) * kRows + r]);
+  const float Mu = (M == -INFINITY) ? 0.f : M;
+  float o[D / 4];
+#pragma unroll
+  for (int e = 0; e < D / 4; ++e) o[e] = 0.f;
+  float wsum = 0.f;
+  for (int w = w0; w <= w1; ++w) {
+    const float wgt = fast_exp2(a.part_lse[((size_t)it + w) * kRows + r] - Mu);
+    wsum += wgt;
+    const float* po = a.part_o + (((size_t)it + w) * kRows + r) * D + dq;
+#pragma unroll
+    for (int e = 0; e < D / 4; e += 4) {
+      floatx4 v = ld16<floatx4>(po + e);
+      o[e] += wgt * v[0];
+      o[e + 1] += wgt * v[1];
+      o[e + 2] += wgt * v[2];
+      o[e + 3] += wgt * v[3];
+    }
+  }
+  const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
+  const int i = pr / G, hl = pr % G;
+  bf16* orow = reinterpret_cast<bf16*>(a.out) + ((size_t)(r0 + i) * a.Hq + g * G + hl) * D + dq;
+#pragma unroll
+  for (int e = 0; e < D / 4; ++e) orow[e] = static_cast<bf16>(o[e] * inv);
+}
+
 // Merge the chunk partials of every (sequence, KV head, row group) that spans
 // more than one chunk: out = sum_c 2^(lse_c - M) o_c / sum_c 2^(lse_c - M).
 template <typename DT, int D>
@@ -535,6 +958,22 @@ hipError_t launch_t(const AttnParams& p, dim3 grid, dim3 cgrid, hipStream_t st) 
   return e;
 }
 
+hipError_t launch_sk(const AttnParams& p, dim3 cgrid, hipStream_t st) {
+  trace_begin(st);
+  hipLaunchKernelGGL((append_window_kernel<bf16, 128>), dim3(cgrid.y), dim3(256), 0, st, p);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  trace_mark(st);
+  hipLaunchKernelGGL(verify_attn_sk_kernel, dim3(p.sk_grid), dim3(256), 0, st, p);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  trace_mark(st);
+  hipLaunchKernelGGL(attn_combine_sk_kernel, cgrid, dim3(256), 0, st, p);
+  e = hipGetLastError();
+  trace_mark(st);
+  return e;
+}
+
 template <typename DT, int D>
 hipError_t launch_d(const AttnParams& p, int qt, dim3 grid, dim3 cgrid, hipStream_t st) {
   switch (qt) {
@@ -575,6 +1014,22 @@ AttnPlan attn_plan(int n_seq, int Hq, int Hkv, int D, int max_q, int max_pages, 
   pl.part_o_bytes = slots * kRows * D * sizeof(float);
   pl.part_lse_bytes = slots * kRows * sizeof(float);
   pl.workspace_bytes = pl.part_o_bytes + pl.part_lse_bytes + 256;
+  // Full 64-row groups of 16-slot D = 128 pages take the persistent stream-K
+  // kernel (bf16; the launch checks the type) when its LDS tables fit: item
+  // starts and non-empty counts, sequence data, and per workgroup two page
+  // ids per block and one record per unit (a share is at most every item at
+  // its largest block count over the grid; its units add one per item).
+  const long n_it = (long)n_seq * Hkv * pl.n_qg;
+  const long maxblk = (max_keys + kBlk - 1) / kBlk;
+  const long share = (n_it * maxblk + kSkGrid - 1) / kSkGrid;
+  pl.sk = D == 128 && page_size == 16 && pl.qt == 4 && attn_sk_enabled() &&
+          2 * (n_it + 1) + 4L * n_seq + 3 * share + n_it <= kSkMeta;
+  if (pl.sk) {
+    const size_t sk_slots = (size_t)n_it + kSkGrid;
+    pl.sk_o_bytes = std::max(pl.part_o_bytes, sk_slots * kRows * D * sizeof(float));
+    pl.sk_lse_bytes = std::max(pl.part_lse_bytes, sk_slots * kRows * sizeof(float));
+    pl.workspace_bytes = pl.sk_o_bytes + pl.sk_lse_bytes + (n_it + 1) * sizeof(int32_t) + 256;
+  }
   return pl;
 }
 
@@ -607,6 +1062,12 @@ hipError_t launch_verify_attn(const AttnLaunch& L, const AttnPlan& pl, hipStream
   p.scale_log2 = L.scale * 1.4426950408889634f;
   dim3 grid((L.n_seq * L.Hkv + 7) / 8 * 8, pl.n_qg, pl.max_chunks);
   dim3 cgrid(pl.n_qg, L.n_seq * L.Hkv);
+  if (pl.sk && L.dtype_bf16 && L.D == 128 && L.page_size == 16) {
+    p.part_lse = reinterpret_cast<float*>(reinterpret_cast<char*>(L.workspace) + pl.sk_o_bytes);
+    p.sk_start = reinterpret_cast<int32_t*>(reinterpret_cast<char*>(L.workspace) + pl.sk_o_bytes + pl.sk_lse_bytes);
+    p.sk_grid = kSkGrid;
+    return launch_sk(p, cgrid, st);
+  }
   if (L.dtype_bf16) {
     return L.D == 64 ? launch_d<bf16, 64>(p, pl.qt, grid, cgrid, st)
                      : launch_d<bf16, 128>(p, pl.qt, grid, cgrid, st);

@@ -57,6 +57,18 @@ def test_long_window_two_row_groups():
     _check_all(_case(cfg, seed=4))
 
 
+@pytest.mark.parametrize("B,ks,lo,hi,seed", [(12, (0, 1, 8, 16), 0, 300, 7),
+                                              (60, (0, 4, 16), 0, 40, 8)])
+def test_empty_windows_and_row_groups(B, ks, lo, hi, seed):
+    """Teacher heads with windows of 0 rows and empty contexts in the batch: the
+    (sequence, head, row group) items with no rows, or no second row group,
+    sit between non-empty ones; with contexts of at most 40 keys there are
+    fewer key blocks than persistent workgroups."""
+    cfg = inputs.scaled(inputs.WORKLOADS["teacher-bf16"], B=B, ctx_lo=lo, ctx_hi=hi, k_choices=ks,
+                        models=(inputs.scaled_shape(inputs.TEACHER, vocab=512, hidden=64),))
+    _check_all(_case(cfg, seed=seed))
+
+
 @pytest.mark.parametrize("ps", [32, 64])
 def test_other_page_sizes(ps):
     cfg = inputs.scaled(inputs.WORKLOADS["teacher-bf16"], B=3, ctx_lo=10, ctx_hi=900, page_size=ps,
