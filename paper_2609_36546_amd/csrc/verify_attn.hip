@@ -86,6 +86,8 @@ template <int D> struct Frags<bf16, D> {
   static constexpr int KS = D / 32;   // k-steps of the QK product
   bf16x8 k[2][KS];                    // A operand: key rows of sub-tiles 0/1
   bf16x8 v[D / 16];                   // A operand: channel rows, 8 keys each
+  __device__ __forceinline__ bf16x8 kf(int st, int ks) const { return k[st][ks]; }
+  __device__ __forceinline__ bf16x8 vf(int dt) const { return v[dt]; }
 };
 
 template <int D> struct Frags<float, D> {
@@ -192,8 +194,8 @@ template <int D> struct RegQ {
   __device__ __forceinline__ bf16x8 get(int, int ks) const { return q[ks]; }
 };
 
-template <typename DT, int D, int QT, bool TAIL, class QS>
-__device__ __forceinline__ void attend_block(const AttnParams& a, const Frags<DT, D>& f,
+template <typename DT, int D, int QT, bool TAIL, class QS, class FS>
+__device__ __forceinline__ void attend_block(const AttnParams& a, const FS& f,
                                              const QS& qs, const int (&qlimit)[QT],
                                              int t0, floatx4 (&acc)[QT][D / 16],
                                              float (&m_run)[QT], float (&l_run)[QT]) {
@@ -210,7 +212,7 @@ __device__ __forceinline__ void attend_block(const AttnParams& a, const Frags<DT
         const bf16x8 qv = qs.get(t, ks);
 #pragma unroll
         for (int st = 0; st < 2; ++st)
-          s[t][st] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f.k[st][ks], qv, s[t][st], 0, 0, 0);
+          s[t][st] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f.kf(st, ks), qv, s[t][st], 0, 0, 0);
       }
   } else {
 #pragma unroll
@@ -276,7 +278,7 @@ __device__ __forceinline__ void attend_block(const AttnParams& a, const Frags<DT
       for (int e = 0; e < 8; ++e) pf[e] = static_cast<bf16>(p[e]);
 #pragma unroll
       for (int dt = 0; dt < D / 16; ++dt)
-        acc[t][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f.v[dt], pf, acc[t][dt], 0, 0, 0);
+        acc[t][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f.vf(dt), pf, acc[t][dt], 0, 0, 0);
     } else {
 #pragma unroll
       for (int dt = 0; dt < D / 16; ++dt)
@@ -549,6 +551,26 @@ __device__ __forceinline__ int kpiece_unit(int slot, int q) {
 __device__ __forceinline__ int vpiece_unit(int ch, int h) { return 2 * ch + (h ^ ((ch >> 2) & 1)); }
 __device__ __forceinline__ int uni(int x) { return __builtin_amdgcn_readfirstlane(x); }
 
+// MFMA operands read from a key/value unit in LDS where they are used, so
+// that no full register copy of the block is live.  TAIL: value lanes of keys
+// at or past n_keys are zeroed (their pages are clamped stand-ins).
+template <bool TAIL> struct LdsFrags {
+  const char* buf;
+  int k_off0, k_off1, v_off0, vpos, n_keys;
+  __device__ __forceinline__ bf16x8 kf(int st, int ks) const {
+    return *reinterpret_cast<const bf16x8*>(buf + (st ? k_off1 : k_off0) + 1024 * ks);
+  }
+  __device__ __forceinline__ bf16x8 vf(int dt) const {
+    bf16x8 v = *reinterpret_cast<const bf16x8*>(buf + v_off0 + 512 * dt);
+    if constexpr (TAIL) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        if (vpos + e >= n_keys) v[e] = static_cast<bf16>(0.f);
+    }
+    return v;
+  }
+};
+
 // Item `it` = (sequence slot, KV head g, row group qg), it = (slot Hkv + g) n_qg + qg:
 // the row groups of one (sequence, head) are neighbours, so the shares that
 // read the same keys for them run at the same time and the second read is a
@@ -725,18 +747,16 @@ __global__ __launch_bounds__(256, 2) void verify_attn_sk_kernel(AttnParams a) {
     }
   };
 
-  // Per-lane LDS offsets of the MFMA operands within a unit.
-  int k_off[2], v_off[D / 16];
+  // Per-lane LDS offsets of the MFMA operands within a unit.  Channel
+  // 16 dt + c16 lies in value piece dt / 2 at unit 2 (16 (dt % 2) + c16) + h',
+  // and h' does not depend on dt, so the value offsets step by 512 bytes.
+  int k_off[2];
 #pragma unroll
   for (int st = 0; st < 2; ++st) {
     const int kk = 8 * (c16 >> 2) + 4 * st + (c16 & 3);
     k_off[st] = 4096 * (kk >> 4) + 16 * kpiece_unit(kk & 15, j);
   }
-#pragma unroll
-  for (int dt = 0; dt < D / 16; ++dt) {
-    const int ch = 16 * dt + c16;
-    v_off[dt] = 8192 + 4096 * (j >> 1) + 1024 * (ch >> 5) + 16 * vpiece_unit(ch & 31, j & 1);
-  }
+  const int v_off0 = 8192 + 4096 * (j >> 1) + 16 * vpiece_unit(c16, j & 1);
 
   for (int m = 0; m < kSkBuf - 1; ++m) dma_unit(m);
 
@@ -767,8 +787,14 @@ __global__ __launch_bounds__(256, 2) void verify_attn_sk_kernel(AttnParams a) {
       const int i = rec >> 2;
       c_item = i;
       it = sk_item(a, s_seq, i, maxblk);
-      x0 = s_start[i] - lo;
-      full = s_start[i] >= lo && s_start[i + 1] <= hi;
+      it.g = uni(it.g);
+      it.L = uni(it.L);
+      it.r0 = uni(it.r0);
+      it.pr0 = uni(it.pr0);
+      it.pr_last = uni(it.pr_last);
+      it.n_keys = uni(it.n_keys);
+      x0 = uni(s_start[i] - lo);
+      full = uni(s_start[i] >= lo && s_start[i + 1] <= hi);
       prq = it.pr0 + 16 * t + c16;
       qlimit[0] = it.L + min(prq, it.pr_last) / a.G + 1;
       has_rows = it.pr0 + 16 * t <= it.pr_last;
@@ -787,25 +813,11 @@ __global__ __launch_bounds__(256, 2) void verify_attn_sk_kernel(AttnParams a) {
     if (!has_rows) continue;
     const int t0 = kBlk * ((rec >> 2) - x0);
     const int main_end = min(it.n_keys, it.L & ~(kBlk - 1));
-    Frags<bf16, D> f;
-#pragma unroll
-    for (int st = 0; st < 2; ++st)
-#pragma unroll
-      for (int ks = 0; ks < D / 32; ++ks)
-        f.k[st][ks] = *reinterpret_cast<const bf16x8*>(buf + k_off[st] + 1024 * ks);
-#pragma unroll
-    for (int dt = 0; dt < D / 16; ++dt) f.v[dt] = *reinterpret_cast<const bf16x8*>(buf + v_off[dt]);
     if (t0 + kBlk <= main_end) {
+      const LdsFrags<false> f{buf, k_off[0], k_off[1], v_off0, 0, 0};
       attend_block<bf16, D, 1, false>(a, f, qf, qlimit, t0, acc, m_run, l_run);
     } else {
-      // Past the last visible key the pages are clamped stand-ins: zero
-      // those value lanes so masked probabilities never meet them.
-      const int vpos = t0 + 8 * j;
-#pragma unroll
-      for (int dt = 0; dt < D / 16; ++dt)
-#pragma unroll
-        for (int e = 0; e < 8; ++e)
-          if (vpos + e >= it.n_keys) f.v[dt][e] = static_cast<bf16>(0.f);
+      const LdsFrags<true> f{buf, k_off[0], k_off[1], v_off0, t0 + 8 * j, it.n_keys};
       attend_block<bf16, D, 1, true>(a, f, qf, qlimit, t0, acc, m_run, l_run);
     }
     if (!(rec & 2)) continue;
