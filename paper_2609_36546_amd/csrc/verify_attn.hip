@@ -866,13 +866,11 @@ __global__ __launch_bounds__(256) void attn_combine_sk_kernel(AttnParams a) {
   const int w0 = wg_of(s0), w1 = wg_of(s1 - 1);
   if (w0 == w1) return;   // written whole by one workgroup
   const int b = a.seq_ids ? a.seq_ids[slot] : slot;
-  const int L = max(a.ctx_lens[b], 0);
   const int r0 = a.cu_q[b];
   const int kb = a.cu_q[b + 1] - r0;
   const int G = a.G;
   const int pr0 = qg * kRows;
   const int pr_last = min(kb * G, pr0 + kRows) - 1;
-  (void)L;
   const int r = threadIdx.x / 4;            // packed row within the group
   const int dq = (threadIdx.x % 4) * (D / 4);
   const int pr = pr0 + r;
