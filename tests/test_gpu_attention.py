@@ -161,3 +161,36 @@ def test_full_size_teacher_config_sampled():
     ref, rows = parity.oracle_attention_subset(mdl, b, seqs, mdl.shape.D)
     worst = parity.check_attention_rows(out, ref, rows, mdl.q.dtype)
     _say(f"  full teacher config: worst rel err {worst:.2e}")
+
+
+def test_full_size_long_teacher_config_sampled():
+    """The full long-trajectory workload (16 sequences, contexts up to 32768,
+    pages shuffled over a 2M-token pool, 16-token windows: two 64-row groups
+    per KV head) in the launch configuration the benchmark times; the oracle
+    checks the longest and the shortest sequence."""
+    b = _case(inputs.WORKLOADS["long-teacher-bf16"], seed=0, poison=False)
+    mdl = b.models[0]
+    out, _, _ = parity.run_gpu_attention(mdl, b)
+    seqs = [int(np.argmax(b.ctx_lens)), int(np.argmin(b.ctx_lens))]
+    ref, rows = parity.oracle_attention_subset(mdl, b, seqs, mdl.shape.D)
+    worst = parity.check_attention_rows(out, ref, rows, mdl.q.dtype)
+    _say(f"  full long-teacher config: worst rel err {worst:.2e}")
+
+
+def test_full_size_dual_cache_teacher_sampled():
+    """The full interleaved dual-cache batch (128 sequences, windows of 1, 4,
+    8 or 16, contexts up to 16384): the teacher verifier's call, sampled on
+    its longest sequence and on one sequence of each window length."""
+    b = _case(inputs.WORKLOADS["dual-cache-bf16"], seed=0, poison=False)
+    mdl = b.models[1]
+    mine = to_np(mdl.seq_ids).astype(np.int64)
+    out, _, _ = parity.run_gpu_attention(mdl, b, seq_ids=mdl.seq_ids)
+    seqs = {int(mine[np.argmax(b.ctx_lens[mine])])}
+    for k in (1, 4, 8, 16):
+        with_k = mine[b.k[mine] == k]
+        if len(with_k):
+            seqs.add(int(with_k[0]))
+    seqs = sorted(seqs)
+    ref, rows = parity.oracle_attention_subset(mdl, b, seqs, mdl.shape.D)
+    worst = parity.check_attention_rows(out, ref, rows, mdl.q.dtype)
+    _say(f"  full dual-cache teacher call, sequences {seqs}: worst rel err {worst:.2e}")
