@@ -613,6 +613,33 @@ __device__ __forceinline__ void wave_topk(const float (&cv)[N], const int (&ci)[
   }
 }
 
+// wave_topk for at most 128 candidates with distinct indices, held two per
+// lane in registers: each round takes the wave's best remaining candidate and
+// its lane drops it, so no round re-reads LDS.  The picks come out in the same
+// order as wave_topk's.  A NaN value is never picked there, so it is dropped
+// on loading here.
+__device__ __forceinline__ void wave_topk_regs(const float* xv, const int* xi, int nx, int K,
+                                               float* out_v, int* out_i) {
+  const int lane = lane_id();
+  float v0 = -INFINITY, v1 = -INFINITY;
+  int i0 = 0x7fffffff, i1 = 0x7fffffff;
+  if (lane < nx) { v0 = xv[lane]; i0 = xi[lane]; }
+  if (lane + kWave < nx) { v1 = xv[lane + kWave]; i1 = xi[lane + kWave]; }
+  if (!(v0 >= -INFINITY)) { v0 = -INFINITY; i0 = 0x7fffffff; }
+  if (!(v1 >= -INFINITY)) { v1 = -INFINITY; i1 = 0x7fffffff; }
+  for (int k = 0; k < K; ++k) {
+    float bv = v0;
+    int bi = i0;
+    if (before(v1, i1, bv, bi)) { bv = v1; bi = i1; }
+    wave_best(bv, bi);
+    if (lane == 0) { out_v[k] = bv; out_i[k] = bi; }
+    if (bi != 0x7fffffff) {
+      if (i0 == bi) { v0 = -INFINITY; i0 = 0x7fffffff; }
+      if (i1 == bi) { v1 = -INFINITY; i1 = 0x7fffffff; }
+    }
+  }
+}
+
 constexpr int kCap = 2048;     // survivor list capacity (candidates >= theta)
 constexpr int kMaxHd = 4096;   // hidden sizes the merge can stage in LDS for recomputes
 
@@ -828,6 +855,8 @@ __global__ __launch_bounds__(kMT) void lmhead_merge_kernel(LmParams p) {
         const int fi[2] = {xi0, xi1};
         wave_topk(fv, fi, s_cv, s_ci, 0, K, s_top_v, s_top_i);
       }
+    } else if (wv == 0 && n_list <= 2 * kWave) {
+      wave_topk_regs(s_lv, s_li, n_list, K, s_top_v, s_top_i);
     } else if (wv == 0) {
       const float none[1] = {-INFINITY};
       const int nonei[1] = {0x7fffffff};
