@@ -852,8 +852,10 @@ __global__ __launch_bounds__(256, 2) void verify_attn_sk_kernel(AttnParams a) {
 // workgroups: piece w of item it sits at slot it + w, for the workgroups w
 // whose share of blocks meets the item.
 __global__ __launch_bounds__(256) void attn_combine_sk_kernel(AttnParams a) {
+  // Grid x = 4 row quarters per row group: 16 packed rows per workgroup,
+  // 16 threads per row, 8 channels per thread.
   constexpr int D = 128;
-  const int qg = blockIdx.x;
+  const int qg = blockIdx.x / 4, rq = blockIdx.x % 4;
   const int slot = blockIdx.y / a.Hkv, g = blockIdx.y % a.Hkv;
   const int it = (slot * a.Hkv + g) * a.n_qg + qg;
   const int n_it = a.n_seq * a.Hkv * a.n_qg;
@@ -869,37 +871,31 @@ __global__ __launch_bounds__(256) void attn_combine_sk_kernel(AttnParams a) {
   const int r0 = a.cu_q[b];
   const int kb = a.cu_q[b + 1] - r0;
   const int G = a.G;
-  const int pr0 = qg * kRows;
-  const int pr_last = min(kb * G, pr0 + kRows) - 1;
-  const int r = threadIdx.x / 4;            // packed row within the group
-  const int dq = (threadIdx.x % 4) * (D / 4);
-  const int pr = pr0 + r;
-  if (pr > pr_last) return;
+  const int r = 16 * rq + threadIdx.x / 16;           // packed row within the group
+  const int dq = (threadIdx.x % 16) * (D / 16);
+  const int pr = qg * kRows + r;
+  if (pr >= min(kb * G, (qg + 1) * kRows)) return;
   float M = -INFINITY;
   for (int w = w0; w <= w1; ++w) M = fmaxf(M, a.part_lse[((size_t)it + w) * kRows + r]);
   const float Mu = (M == -INFINITY) ? 0.f : M;
-  float o[D / 4];
-#pragma unroll
-  for (int e = 0; e < D / 4; ++e) o[e] = 0.f;
+  floatx4 o0 = {0.f, 0.f, 0.f, 0.f}, o1 = {0.f, 0.f, 0.f, 0.f};
   float wsum = 0.f;
   for (int w = w0; w <= w1; ++w) {
     const float wgt = fast_exp2(a.part_lse[((size_t)it + w) * kRows + r] - Mu);
     wsum += wgt;
     const float* po = a.part_o + (((size_t)it + w) * kRows + r) * D + dq;
-#pragma unroll
-    for (int e = 0; e < D / 4; e += 4) {
-      floatx4 v = ld16<floatx4>(po + e);
-      o[e] += wgt * v[0];
-      o[e + 1] += wgt * v[1];
-      o[e + 2] += wgt * v[2];
-      o[e + 3] += wgt * v[3];
-    }
+    o0 += wgt * ld16<floatx4>(po);
+    o1 += wgt * ld16<floatx4>(po + 4);
   }
   const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
   const int i = pr / G, hl = pr % G;
-  bf16* orow = reinterpret_cast<bf16*>(a.out) + ((size_t)(r0 + i) * a.Hq + g * G + hl) * D + dq;
+  bf16x8 v;
 #pragma unroll
-  for (int e = 0; e < D / 4; ++e) orow[e] = static_cast<bf16>(o[e] * inv);
+  for (int e = 0; e < 4; ++e) {
+    v[e] = static_cast<bf16>(o0[e] * inv);
+    v[4 + e] = static_cast<bf16>(o1[e] * inv);
+  }
+  *reinterpret_cast<bf16x8*>(reinterpret_cast<bf16*>(a.out) + ((size_t)(r0 + i) * a.Hq + g * G + hl) * D + dq) = v;
 }
 
 // Merge the chunk partials of every (sequence, KV head, row group) that spans
@@ -978,7 +974,7 @@ hipError_t launch_sk(const AttnParams& p, dim3 cgrid, hipStream_t st) {
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   trace_mark(st);
-  hipLaunchKernelGGL(attn_combine_sk_kernel, cgrid, dim3(256), 0, st, p);
+  hipLaunchKernelGGL(attn_combine_sk_kernel, dim3(4 * cgrid.x, cgrid.y), dim3(256), 0, st, p);
   e = hipGetLastError();
   trace_mark(st);
   return e;
