@@ -194,3 +194,12 @@ def test_full_size_dual_cache_teacher_sampled():
     ref, rows = parity.oracle_attention_subset(mdl, b, seqs, mdl.shape.D)
     worst = parity.check_attention_rows(out, ref, rows, mdl.q.dtype)
     _say(f"  full dual-cache teacher call, sequences {seqs}: worst rel err {worst:.2e}")
+
+
+def test_many_sequences_beyond_stream_k_tables():
+    """1000 teacher-head sequences: the (sequence, head) items no longer fit
+    the stream-K kernel's LDS tables, so the planner takes the register
+    kernel for full 64-row groups; both must agree with the oracle."""
+    cfg = inputs.scaled(inputs.WORKLOADS["teacher-bf16"], B=1000, ctx_lo=0, ctx_hi=40, pool_tokens=None,
+                        models=(inputs.scaled_shape(inputs.TEACHER, vocab=512, hidden=64),))
+    _check_all(_case(cfg, seed=11))
