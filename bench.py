@@ -490,6 +490,13 @@ def main():
         "ms_per_step_eager_traced": round(ms_traced, 4),
         "kernels_us": {k: round(v * 1e3, 2) for k, v in kt.items()},
         "attention_hbm_gbs": round(attn_bytes / (kt["attention"] * 1e-3) / 1e9, 1),
+        # the HBM-bound verify attention against the HBM peak, beside the
+        # dominant kernel's roofline above
+        "attention_roofline": {
+            "bound": "hbm", "achieved": round(attn_bytes / (kt["attention"] * 1e-3) / 1e9, 1),
+            "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(attn_bytes / (kt["attention"] * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+            "traffic": measured_traffic("attention", workload)},
         "lmhead_tflops": round(work["lmhead_gemm"][1] / (kt["lmhead_gemm"] * 1e-3) / 1e12, 1),
     }
     if len(step.per_model) == 1 and cfg.dtype == "bf16":
