@@ -194,8 +194,47 @@ int verify_attn_paged(const void* q, const void* k_new, const void* v_new,
                       int dtype, void* workspace, size_t workspace_bytes,
                       void* hip_stream);
 
+/*
+ * ipdv_check_page_table -- host-side check of the device-data contract of
+ * verify_attn_paged (the kernels clamp every index they read, so a table
+ * that breaks the contract gives wrong outputs, not faults).  Takes HOST
+ * copies of the call's arrays (page_table [B, max_pages_per_seq], ctx_lens
+ * [B], cu_q [B+1], seq_ids [n_seq] or NULL) and checks, for every handled
+ * sequence b:
+ *   - L_b >= 0 and k_b = cu_q[b+1] - cu_q[b] >= 0, with cu_q[0] = 0 and cu_q
+ *     non-decreasing;
+ *   - k_b <= max_q, and L_b + k_b <= max_pages_per_seq * page_size;
+ *   - every page id that holds a position 0 .. L_b + k_b - 1 lies in
+ *     [0, num_pages);
+ *   - no page the window writes (positions L_b .. L_b + k_b - 1) is also
+ *     visible to another handled sequence (a shared prefix page must be
+ *     copied before a sequence appends to it);
+ *   - seq_ids entries lie in [0, B) and are distinct.
+ * B is the number of rows of page_table / entries of ctx_lens.  Returns
+ * IPDV_OK, or IPDV_EINVAL with ipdv_last_error() naming the first violation
+ * and *bad_seq (if not NULL) set to its sequence (-1 when none applies).
+ * Allocates host memory for the page-ownership map; launches nothing.
+ */
+int ipdv_check_page_table(const int32_t* page_table, int B, int max_pages_per_seq,
+                          const int32_t* ctx_lens, const int32_t* cu_q,
+                          const int32_t* seq_ids, int n_seq, int max_q,
+                          int page_size, int num_pages, int32_t* bad_seq);
+
 /* Workspace bytes lmhead_logsoftmax_verify needs (0 if invalid). */
 size_t ipdv_lmhead_workspace_size(int M, int Hd, int V, int K);
+
+/*
+ * One query for both workspaces, dispatching to the two typed queries above:
+ *   which = IPDV_WS_ATTN:   host_shape_args = {n_seq, Hq, Hkv, D, max_q,
+ *                           max_pages_per_seq, page_size}, n = 7;
+ *   which = IPDV_WS_LMHEAD: host_shape_args = {M, Hd, V, K}, n = 4.
+ * host_shape_args is a HOST array.  Returns 0 for an unknown `which`, a NULL
+ * array, a count other than the one listed, or shape values the typed query
+ * rejects (ipdv_last_error() then says which).
+ */
+#define IPDV_WS_ATTN 0
+#define IPDV_WS_LMHEAD 1
+size_t ipdv_workspace_size(int which, const int32_t* host_shape_args, int n);
 
 /*
  * lmhead_logsoftmax_verify -- the verifier's next-token distribution at each

@@ -8,6 +8,8 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <unordered_map>
+#include <vector>
 
 #include "../../include/ipdv.h"
 #include "kernels.h"
@@ -61,29 +63,6 @@ bool is_pow2(int x) { return x > 0 && (x & (x - 1)) == 0; }
 }  // namespace
 
 namespace ipdv {
-
-// Keys streamed by one wave per split, from IPDV_ATTN_SUB (a multiple of 32
-// in [32, 1024]) for tuning sweeps; 0 = the planner's choice.
-int attn_sub_tokens() {
-  static int v = [] {
-    const char* s = getenv("IPDV_ATTN_SUB");
-    int x = s ? atoi(s) : 0;
-    if (x < 32 || x > 1024 || x % 32 != 0) x = 0;
-    return x;
-  }();
-  return v;
-}
-
-// IPDV_ATTN_KERNEL=regs keeps full 64-row groups on the register kernel
-// (A/B timing sweeps only); by default they take the persistent stream-K
-// kernel.
-bool attn_sk_enabled() {
-  static bool v = [] {
-    const char* s = getenv("IPDV_ATTN_KERNEL");
-    return !(s && strcmp(s, "regs") == 0);
-  }();
-  return v;
-}
 
 void trace_begin(hipStream_t st) { trace_mark(st); }
 
@@ -161,6 +140,71 @@ int verify_attn_paged(const void* q, const void* k_new, const void* v_new, void*
   return ok();
 }
 
+int ipdv_check_page_table(const int32_t* page_table, int B, int max_pages, const int32_t* ctx_lens,
+                          const int32_t* cu_q, const int32_t* seq_ids, int n_seq, int max_q,
+                          int page_size, int num_pages, int32_t* bad_seq) {
+  if (bad_seq) *bad_seq = -1;
+  if (!page_table || !ctx_lens || !cu_q) return fail(IPDV_EINVAL, "null required pointer");
+  if (B < 0 || n_seq < 0 || max_pages < 1 || page_size < 1 || num_pages < 1)
+    return fail(IPDV_EINVAL, "bad sizes (B %d, n_seq %d, max_pages %d, page_size %d, num_pages %d)",
+                B, n_seq, max_pages, page_size, num_pages);
+  if (!seq_ids && n_seq > B) return fail(IPDV_EINVAL, "n_seq %d exceeds B %d", n_seq, B);
+  auto bad = [&](int b, const char* fmt, ...) {
+    if (bad_seq) *bad_seq = b;
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof(g_err), fmt, ap);
+    va_end(ap);
+    return IPDV_EINVAL;
+  };
+  if (B > 0 && cu_q[0] != 0) return bad(0, "cu_q[0] = %d, must be 0", cu_q[0]);
+  for (int b = 0; b < B; ++b)
+    if (cu_q[b + 1] < cu_q[b]) return bad(b, "cu_q decreases at sequence %d", b);
+  // page -> the handled sequence that writes it (window pages), and the
+  // handled sequences that see each page
+  std::unordered_map<int32_t, int> writer;
+  std::vector<char> handled(B, 0);
+  for (int i = 0; i < n_seq; ++i) {
+    const int b = seq_ids ? seq_ids[i] : i;
+    if (b < 0 || b >= B) return bad(-1, "seq_ids[%d] = %d is not in [0, %d)", i, b, B);
+    if (handled[b]) return bad(b, "sequence %d is listed twice in seq_ids", b);
+    handled[b] = 1;
+    const long L = ctx_lens[b], k = (long)cu_q[b + 1] - cu_q[b];
+    if (L < 0) return bad(b, "sequence %d: ctx_len %ld < 0", b, L);
+    if (k > max_q) return bad(b, "sequence %d: window of %ld rows exceeds max_q %d", b, k, max_q);
+    if (L + k > (long)max_pages * page_size)
+      return bad(b, "sequence %d: %ld positions do not fit %d pages of %d", b, L + k, max_pages,
+                 page_size);
+    const long n_pages = (L + k + page_size - 1) / page_size;
+    for (long j = 0; j < n_pages; ++j) {
+      const int32_t pg = page_table[(size_t)b * max_pages + j];
+      if (pg < 0 || pg >= num_pages)
+        return bad(b, "sequence %d: page_table[%d][%ld] = %d is not in [0, %d)", b, b, j, pg,
+                   num_pages);
+    }
+    for (long j = L / page_size; k > 0 && j < n_pages; ++j) {
+      const int32_t pg = page_table[(size_t)b * max_pages + j];
+      auto it = writer.find(pg);
+      if (it != writer.end() && it->second != b)
+        return bad(b, "page %d is written by the windows of sequences %d and %d", pg, it->second, b);
+      writer[pg] = b;
+    }
+  }
+  for (int i = 0; i < n_seq && !writer.empty(); ++i) {
+    const int b = seq_ids ? seq_ids[i] : i;
+    const long L = ctx_lens[b], k = (long)cu_q[b + 1] - cu_q[b];
+    const long n_pages = (L + k + page_size - 1) / page_size;
+    for (long j = 0; j < n_pages; ++j) {
+      const int32_t pg = page_table[(size_t)b * max_pages + j];
+      auto it = writer.find(pg);
+      if (it != writer.end() && it->second != b)
+        return bad(b, "page %d is written by sequence %d's window and read by sequence %d", pg,
+                   it->second, b);
+    }
+  }
+  return ok();
+}
+
 static int lm_shape_check(int M, int Hd, int V, int K) {
   if (M < 0) return fail(IPDV_EINVAL, "M must be >= 0 (got %d)", M);
   if (V < 1) return fail(IPDV_EINVAL, "V must be >= 1 (got %d)", V);
@@ -187,6 +231,29 @@ static int w_dtype(int dtype, bool* bf16, bool* tiled) {
 size_t ipdv_lmhead_workspace_size(int M, int Hd, int V, int K) {
   if (lm_shape_check(M, Hd, V, K) != IPDV_OK) return 0;
   return ipdv::lm_plan(M, Hd, V, K, true).workspace_bytes;
+}
+
+size_t ipdv_workspace_size(int which, const int32_t* a, int n) {
+  if (!a) {
+    fail(IPDV_EINVAL, "host_shape_args is NULL");
+    return 0;
+  }
+  if (which == IPDV_WS_ATTN) {
+    if (n != 7) {
+      fail(IPDV_EINVAL, "attention workspace query takes 7 shape values (got %d)", n);
+      return 0;
+    }
+    return ipdv_attn_workspace_size(a[0], a[1], a[2], a[3], a[4], a[5], a[6]);
+  }
+  if (which == IPDV_WS_LMHEAD) {
+    if (n != 4) {
+      fail(IPDV_EINVAL, "LM-head workspace query takes 4 shape values (got %d)", n);
+      return 0;
+    }
+    return ipdv_lmhead_workspace_size(a[0], a[1], a[2], a[3]);
+  }
+  fail(IPDV_EINVAL, "unknown workspace kind %d", which);
+  return 0;
 }
 
 int lmhead_logsoftmax_verify(const void* hidden, const void* W, const int32_t* prop_tok,

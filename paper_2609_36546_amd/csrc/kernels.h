@@ -62,8 +62,6 @@ struct AttnLaunch {
   void* workspace;
 };
 
-int attn_sub_tokens();
-bool attn_sk_enabled();
 AttnPlan attn_plan(int n_seq, int Hq, int Hkv, int D, int max_q, int max_pages, int page_size);
 hipError_t launch_verify_attn(const AttnLaunch& L, const AttnPlan& pl, hipStream_t st);
 

@@ -832,7 +832,8 @@ __global__ __launch_bounds__(kMT) void lmhead_merge_kernel(LmParams p) {
     }
   }
   __syncthreads();
-  const bool overflow = s_n > kCap;     // many ties at theta: select from all records
+  // Many ties at theta: select from all records instead of the list.
+  bool overflow = s_n > kCap;
   int n_list = min(s_n, kCap);
 
   // Exact top-K.  Round 0 picks from the candidates; a group with three picks
@@ -891,8 +892,39 @@ __global__ __launch_bounds__(kMT) void lmhead_merge_kernel(LmParams p) {
       __syncthreads();
       recompute_logits<DT>(p, s_hid, s_split, nsplit, s_cv, s_ci);
     }
-    if (overflow) {
+    __syncthreads();
+    bool from_records = overflow;
+    if (!overflow) {
+      // survivors of split groups are replaced by the recomputed values; when
+      // the kept survivors and the recomputed logits together exceed the
+      // list, round 1 selects from all records instead
+      if (tid == 0) s_n = 0;
+      __syncthreads();
+      for (int c = tid; c < n_list; c += kMT) {
+        bool sp = false;
+        for (int t = 0; t < nsplit; ++t) sp |= (s_li[c] / kGroup == s_split[t]);
+        if (!sp) {
+          const int slot = atomicAdd(&s_n, 1);
+          if (slot < kCap) { s_lv2[slot] = s_lv[c]; s_li2[slot] = s_li[c]; }
+        }
+      }
+      __syncthreads();
+      const int kept = s_n;
+      if (kept + nsplit * kGroup <= kCap) {
+        for (int c = tid; c < nsplit * kGroup; c += kMT) {
+          s_lv2[kept + c] = s_cv[c];
+          s_li2[kept + c] = s_ci[c];
+        }
+        __syncthreads();
+        n_list = kept + nsplit * kGroup;
+        for (int c = tid; c < n_list; c += kMT) { s_lv[c] = s_lv2[c]; s_li[c] = s_li2[c]; }
+      } else {
+        from_records = true;
+      }
+    }
+    if (from_records) {
       // drop the split groups' records: their members now come from s_cv
+      overflow = true;
 #pragma unroll
       for (int u = 0; u < kMaxGPT; ++u) {
         const int gi = tid + kMT * u;
@@ -906,29 +938,6 @@ __global__ __launch_bounds__(kMT) void lmhead_merge_kernel(LmParams p) {
           }
         }
       }
-    }
-    __syncthreads();
-    if (!overflow) {
-      // survivors of split groups are replaced by the recomputed values
-      if (tid == 0) s_n = 0;
-      __syncthreads();
-      for (int c = tid; c < n_list; c += kMT) {
-        bool sp = false;
-        for (int t = 0; t < nsplit; ++t) sp |= (s_li[c] / kGroup == s_split[t]);
-        if (!sp) {
-          const int slot = atomicAdd(&s_n, 1);
-          if (slot < kCap) { s_lv2[slot] = s_lv[c]; s_li2[slot] = s_li[c]; }
-        }
-      }
-      __syncthreads();
-      const int kept = min(s_n, kCap);
-      for (int c = tid; c < nsplit * kGroup && kept + c < kCap; c += kMT) {
-        s_lv2[kept + c] = s_cv[c];
-        s_li2[kept + c] = s_ci[c];
-      }
-      __syncthreads();
-      n_list = min(kept + nsplit * kGroup, kCap);
-      for (int c = tid; c < n_list; c += kMT) { s_lv[c] = s_lv2[c]; s_li[c] = s_li2[c]; }
     }
     __syncthreads();
   }
@@ -1140,18 +1149,8 @@ __global__ __launch_bounds__(kMT) void sample_kernel(LmParams p, SampleParams s)
 // hidden size is a multiple of four stages, fp32 the register-staged one.
 template <int RB>
 void launch_gemm(const LmParams& p, dim3 grid, hipStream_t st, bf16) {
-  // Ring depth (IPDV_LM_NBUF overrides it for tuning sweeps).
-  static const int nbuf_env = [] {
-    const char* e = getenv("IPDV_LM_NBUF");
-    return e ? atoi(e) : 0;
-  }();
-  const int nbuf = (nbuf_env >= 3 && nbuf_env <= 5) ? nbuf_env : 4;
   if (p.Hd % kDStage != 0)
     hipLaunchKernelGGL((lmhead_gemm_kernel<bf16, RB>), grid, dim3(256), 0, st, p);
-  else if (nbuf == 3)
-    hipLaunchKernelGGL((lmhead_gemm_dlds_kernel<RB, 3>), grid, dim3(256), 0, st, p);
-  else if (nbuf == 5 && RB <= 4)
-    hipLaunchKernelGGL((lmhead_gemm_dlds_kernel<RB, 5>), grid, dim3(256), 0, st, p);
   else
     hipLaunchKernelGGL((lmhead_gemm_dlds_kernel<RB, 4>), grid, dim3(256), 0, st, p);
 }
@@ -1186,10 +1185,6 @@ LmPlan lm_plan(int M, int Hd, int V, int K, bool bf16) {
   // double-buffered stage fits the LDS.
   const int rows = M < 256 ? M : 256;
   pl.rb = rows <= 64 ? 1 : rows <= 128 ? 2 : rows <= 192 ? 3 : 4;
-  if (const char* e = getenv("IPDV_LM_RB")) {     // tuning sweeps only
-    const int x = atoi(e);
-    if (x >= 1 && x <= 4) pl.rb = x;
-  }
   if (!bf16) pl.rb = 1;
   pl.n_rt = (M + 64 * pl.rb - 1) / (64 * pl.rb);
   const size_t recs = (size_t)M * pl.n_groups;

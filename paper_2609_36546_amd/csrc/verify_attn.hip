@@ -1003,9 +1003,8 @@ AttnPlan attn_plan(int n_seq, int Hq, int Hkv, int D, int max_q, int max_pages, 
   pl.qt = rows >= kRows ? 4 : (int)((rows + 15) / 16);
   // Keys per wave: the largest split that still yields enough workgroups
   // (>= 4 per CU, by the host-side upper bound of the key count) for the
-  // hardware to balance ragged lengths.  IPDV_ATTN_SUB overrides it.
-  pl.sub = attn_sub_tokens();
-  if (pl.sub == 0) {
+  // hardware to balance ragged lengths.
+  {
     const long max_keys_ub = (long)max_pages * page_size;
     pl.sub = 128;
     for (int s = 1024; s >= 256; s /= 2) {
@@ -1031,7 +1030,7 @@ AttnPlan attn_plan(int n_seq, int Hq, int Hkv, int D, int max_q, int max_pages, 
   const long n_it = (long)n_seq * Hkv * pl.n_qg;
   const long maxblk = (max_keys + kBlk - 1) / kBlk;
   const long share = (n_it * maxblk + kSkGrid - 1) / kSkGrid;
-  pl.sk = D == 128 && page_size == 16 && pl.qt == 4 && attn_sk_enabled() &&
+  pl.sk = D == 128 && page_size == 16 && pl.qt == 4 &&
           2 * (n_it + 1) + 4L * n_seq + 3 * share + n_it <= kSkMeta;
   if (pl.sk) {
     const size_t sk_slots = (size_t)n_it + kSkGrid;

@@ -49,6 +49,11 @@ def lib() -> ctypes.CDLL:
         L.verify_attn_paged.restype = ci
         L.ipdv_lmhead_workspace_size.argtypes = [ci] * 4
         L.ipdv_lmhead_workspace_size.restype = cs
+        L.ipdv_workspace_size.argtypes = [ci, ctypes.POINTER(ctypes.c_int32), ci]
+        L.ipdv_workspace_size.restype = cs
+        L.ipdv_check_page_table.argtypes = [vp, ci, ci, vp, vp, vp, ci, ci, ci, ci,
+                                            ctypes.POINTER(ctypes.c_int32)]
+        L.ipdv_check_page_table.restype = ci
         L.lmhead_logsoftmax_verify.argtypes = [vp, vp, i32p, i32p, ci, ci, ci, ci, f32p, f32p, i32p,
                                                i32p, f32p, f32p, ci, vp, cs, vp]
         L.lmhead_logsoftmax_verify.restype = ci
@@ -151,14 +156,43 @@ def attn_workspace_size(n_seq, Hq, Hkv, D, max_q, max_pages, page_size) -> int:
     return int(lib().ipdv_attn_workspace_size(n_seq, Hq, Hkv, D, max_q, max_pages, page_size))
 
 
+def check_page_table(page_table, ctx_lens, cu_q, max_q: int, page_size: int, num_pages: int,
+                     seq_ids=None, n_seq: Optional[int] = None):
+    """ipdv_check_page_table on host copies of the arrays (tensors on any
+    device, or numpy arrays).  Raises IpdvError naming the first contract
+    violation; returns None when the table is valid."""
+    import numpy as np
+
+    def host(x):
+        if isinstance(x, torch.Tensor):
+            x = x.detach().cpu().numpy()
+        return np.ascontiguousarray(np.asarray(x, np.int32))
+
+    pt, ctx, cu = host(page_table), host(ctx_lens), host(cu_q)
+    sid = None if seq_ids is None else host(seq_ids)
+    B = ctx.shape[0]
+    if pt.ndim != 2 or pt.shape[0] != B or cu.shape[0] != B + 1:
+        raise ValueError("page_table must be [B, maxp] and cu_q [B+1]")
+    if n_seq is None:
+        n_seq = B if sid is None else sid.shape[0]
+    p = lambda a: None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+    bad = ctypes.c_int32(-1)
+    st = lib().ipdv_check_page_table(p(pt), B, pt.shape[1], p(ctx), p(cu), p(sid), n_seq, max_q,
+                                     page_size, num_pages, ctypes.byref(bad))
+    _check("ipdv_check_page_table", st)
+
+
 def verify_attn_paged(q, k_new, v_new, k_cache, v_cache, page_table, ctx_lens, cu_q,
                       max_q: int, seq_ids=None, n_seq: Optional[int] = None,
-                      scale: Optional[float] = None, out=None, workspace=None):
+                      scale: Optional[float] = None, out=None, workspace=None,
+                      validate: bool = False):
     """Append the window to the paged cache and attend (see include/ipdv.h).
 
     q [T,Hq,D], k_new/v_new [T,Hkv,D], k_cache [P,Hkv,D/32,ps,32], v_cache [P,Hkv,D,ps]
     (bf16 or fp32), page_table [B,maxp] int32, ctx_lens [B] int32, cu_q [B+1]
-    int32, seq_ids [n] int32 or None.  Returns out [T,Hq,D].
+    int32, seq_ids [n] int32 or None.  Returns out [T,Hq,D].  validate=True
+    first runs check_page_table on host copies (a device-to-host copy and a
+    synchronisation; for debugging).
     """
     dev = q.device
     dt = q.dtype
@@ -192,6 +226,8 @@ def verify_attn_paged(q, k_new, v_new, k_cache, v_cache, page_table, ctx_lens, c
     else:
         _need(out, "out", dt, dev, 3)
     maxp = page_table.shape[1]
+    if validate:
+        check_page_table(page_table, ctx_lens, cu_q, max_q, ps, P, seq_ids=seq_ids, n_seq=n_seq)
     need = attn_workspace_size(n_seq, Hq, Hkv, D, max_q, maxp, ps)
     if workspace is None:
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)

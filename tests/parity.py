@@ -3,8 +3,12 @@ run the oracle on the same inputs, and compare at the stated tolerances.
 
 Tolerances (bf16 inputs, fp32 accumulation):
 * attention: per (row, head) relative L2 error <= 1e-2 (fp32 inputs: 1e-4);
-  as a sanity bound, every element within 5e-2 x the row's rms (bf16 P and a
-  bf16 output alone reach ~1.2e-2 x rms on N(0,1) data; see the design notes);
+  every element within 2^-8 |o_ref| + 1e-2 x the row's rms (bf16; fp32:
+  2^-24 |o_ref| + 1e-4 x rms).  The first term is the worst case of rounding
+  the output to bf16 (unit roundoff 2^-8); the second covers rounding the
+  softmax weights P to bf16 for the P.V product, whose element error measured
+  by emulating that rounding on 2900 rows of N(0, 1) data (contexts 2..5000,
+  D = 128) stays below 7.3e-3 x rms;
 * log-probs (lse, logp_prop, topk_logp matched by index, entropy): 2e-3 abs;
 * argmax, top-K sets and accept positions: bit-exact wherever the oracle's
   decision margin exceeds 1e-3; rows under the margin are checked for
@@ -26,6 +30,14 @@ LOGP_TOL = 2e-3
 
 def attn_tol(dtype):
     return 1e-2 if dtype == torch.bfloat16 else 1e-4
+
+
+def attn_elem_bound(ref, rms, dtype):
+    """Per-element bound: output rounding (unit roundoff of the output type)
+    times |o_ref|, plus the P-rounding allowance times the row's rms."""
+    if dtype == torch.bfloat16:
+        return 2.0 ** -8 * np.abs(ref) + 1e-2 * rms[..., None]
+    return 2.0 ** -24 * np.abs(ref) + 1e-4 * rms[..., None]
 
 
 def run_gpu_attention(mdl, batch, seq_ids=None, max_q=None, page_table=None, ctx=None, cu=None):
@@ -61,11 +73,15 @@ def check_attention_rows(gpu_out, ref_out, rows, dtype):
     den = np.linalg.norm(r, axis=-1)
     rel = num / np.maximum(den, 1e-30)
     rms = den / np.sqrt(r.shape[-1])
-    mx = np.abs(g - r).max(axis=-1)
     worst = float(rel.max()) if rel.size else 0.0
     assert worst <= tol, f"attention rel err {worst:.3e} > {tol}"
-    assert np.all(mx <= 5 * tol * np.maximum(rms, 1e-30) + 1e-30), \
-        f"attention max-abs err {float((mx / np.maximum(rms, 1e-30)).max()):.3e} x rms"
+    bound = attn_elem_bound(r, rms, dtype) + 1e-30
+    ratio = np.abs(g - r) / bound
+    worst_elem = float(ratio.max()) if ratio.size else 0.0
+    elem_rms = float((np.abs(g - r) / np.maximum(rms, 1e-30)[..., None]).max()) if ratio.size else 0.0
+    print(f"  attention: worst rel L2 {worst:.3e}; worst element error {elem_rms:.3e} x rms, "
+          f"{worst_elem:.3f} of its bound", flush=True)
+    assert worst_elem <= 1.0, f"attention element error {worst_elem:.3f} x its bound"
     return worst
 
 
@@ -154,6 +170,11 @@ def oracle_attention_subset(mdl, batch, seqs, D):
 # probabilities (fp32 group masses over up to 2048 groups and 128 entries,
 # relative rounding below 2048 * 6e-8 of the total, plus fp32-vs-fp64 logits).
 DRAW_TOL = 1.2e-4
+# The expected error of the same cumulative sums: fp32 logits within about
+# 1e-6 relative, sums blocked over at most 16 levels of 2^-24; ten times that.
+# Every draw, decided or not, must put u within CDF_TOL of the drawn token's
+# interval in the oracle's CDF.
+CDF_TOL = 1e-5
 
 
 def check_takeover_draws(tok, fin, fin0, ref, logits_of_row, cu_q, driver, event_row, u, eos_id,
@@ -178,13 +199,13 @@ def check_takeover_draws(tok, fin, fin0, ref, logits_of_row, cu_q, driver, event
         if ref["margin"][b] > DRAW_TOL:
             assert tok[b] == ref["token"][b], (b, tok[b], ref["token"][b], ref["margin"][b])
             exact += 1
-        else:
-            p = np.exp(l - l.max())
-            p /= p.sum()
-            c = np.cumsum(p)
-            lo = c[tok[b] - 1] if tok[b] > 0 else 0.0
-            assert p[tok[b]] > 0 and lo - DRAW_TOL <= u[b] < c[tok[b]] + DRAW_TOL, \
-                (b, tok[b], u[b], lo, c[tok[b]])
+        p = np.exp(l - l.max())
+        p /= p.sum()
+        c = np.cumsum(p)
+        t = int(tok[b])
+        assert 0 <= t < len(l), (b, t)
+        lo = c[t - 1] if t > 0 else 0.0
+        assert p[t] > 0 and lo - CDF_TOL <= u[b] < c[t] + CDF_TOL, (b, t, u[b], lo, c[t])
         assert fin[b] == (1 if tok[b] == eos_id else fin0[b]), b
     return exact
 

@@ -69,6 +69,25 @@ def test_workspace_size_queries():
     assert ops.lmhead_workspace_size(8, 100, 1024, 16) == 0
 
 
+def _ws(which, args, n=None):
+    arr = (ctypes.c_int32 * max(len(args), 1))(*args)
+    return ops.lib().ipdv_workspace_size(which, arr, len(args) if n is None else n)
+
+
+def test_workspace_size_dispatcher_matches_the_typed_queries():
+    for a in [(64, 32, 4, 128, 8, 513, 16), (32, 16, 8, 128, 8, 257, 16), (3, 4, 2, 64, 4, 9, 32),
+              (64, 32, 4, 96, 8, 513, 16)]:
+        assert _ws(0, a) == ops.attn_workspace_size(*a)
+    for a in [(512, 2048, 151936, 16), (8, 256, 1024, 32), (512, 2048, 151936, 33)]:
+        assert _ws(1, a) == ops.lmhead_workspace_size(*a)
+    assert _ws(0, (64, 32, 4, 128, 8, 513)) == 0          # wrong count
+    assert _ws(1, (512, 2048, 151936, 16), n=5) == 0
+    assert _ws(2, (512, 2048, 151936, 16)) == 0          # unknown kind
+    assert ops.lib().ipdv_workspace_size(1, None, 4) == 0
+    assert "shape" in ops.lib().ipdv_last_error().decode() or \
+        "NULL" in ops.lib().ipdv_last_error().decode()
+
+
 def _lm(**kw):
     a = dict(h=1, W=1, prop=1, rows=None, M=8, Hd=256, V=1024, K=16, lse=1, lp=1, am=1, ti=1, tl=1,
              ent=None, dtype=ops.IPDV_F32, ws=1, wsb=1 << 30)
@@ -235,3 +254,84 @@ def test_tiled_w_argument_errors():
     assert st == -2
     st = L.lmhead_sample(vp(1), vp(1), 4, 64, 100, 4, vp(1), 1 << 30, vp(1), vp(1), 0x10, None)
     assert st == -2
+
+
+def _table(seed=0, B=6, ps=16, maxp=12):
+    """A valid page table: every sequence's pages distinct, drawn from a pool."""
+    import numpy as np
+    rng = np.random.default_rng(seed)
+    ctx = rng.integers(0, maxp * ps - 20, size=B).astype(np.int32)
+    k = rng.integers(0, 9, size=B).astype(np.int32)
+    cu = np.concatenate([[0], np.cumsum(k)]).astype(np.int32)
+    P = B * maxp + 3
+    pt = rng.permutation(P)[:B * maxp].reshape(B, maxp).astype(np.int32)
+    return pt, ctx, cu, P
+
+
+def test_page_table_check_accepts_valid_tables():
+    import numpy as np
+    for seed in range(5):
+        pt, ctx, cu, P = _table(seed)
+        ops.check_page_table(pt, ctx, cu, max_q=8, page_size=16, num_pages=P)
+        ops.check_page_table(pt, ctx, cu, max_q=8, page_size=16, num_pages=P,
+                             seq_ids=np.array([4, 1, 2], np.int32))
+    # entries past a sequence's need are never read: any value is accepted
+    pt, ctx, cu, P = _table(7)
+    need = -(-(ctx + np.diff(cu)) // 16)
+    for b in range(len(ctx)):
+        pt[b, need[b]:] = -5
+    ops.check_page_table(pt, ctx, cu, max_q=8, page_size=16, num_pages=P)
+    # a shared prefix page that no window writes is fine
+    pt, ctx, cu, P = _table(8)
+    ctx[:2] = 40
+    cu = np.concatenate([[0], np.cumsum(np.diff(cu))]).astype(np.int32)
+    pt[1, 0] = pt[0, 0]
+    ops.check_page_table(pt, ctx, cu, max_q=8, page_size=16, num_pages=P)
+
+
+def test_page_table_check_names_each_violation():
+    import numpy as np
+
+    def expect(fragment, pt, ctx, cu, P, seq, **kw):
+        with pytest.raises(ops.IpdvError, match=fragment):
+            ops.check_page_table(pt, ctx, cu, page_size=16, num_pages=P, **kw)
+        bad = ctypes.c_int32(-7)
+        p = lambda a: None if a is None else np.ascontiguousarray(a, np.int32).ctypes.data_as(ctypes.c_void_p)
+        sid = kw.get("seq_ids")
+        n = len(ctx) if sid is None else len(sid)
+        assert ops.lib().ipdv_check_page_table(
+            p(pt), len(ctx), pt.shape[1], p(ctx), p(cu), p(sid), n, kw["max_q"], 16, P,
+            ctypes.byref(bad)) == -1
+        assert bad.value == seq
+
+    pt, ctx, cu, P = _table(1)
+    k = np.diff(cu)
+    b = int(np.argmax(ctx + k))
+    x = pt.copy()
+    x[b, (ctx[b] + k[b] - 1) // 16] = P                  # page id out of range
+    expect("not in", x, ctx, cu, P, b, max_q=8)
+    x = pt.copy()
+    x[b, 0] = -1
+    expect("not in", x, ctx, cu, P, b, max_q=8)
+    c = ctx.copy()
+    c[2] = -3                                            # negative context
+    expect("ctx_len", pt, c, cu, P, 2, max_q=8)
+    c = ctx.copy()
+    c[3] = 12 * 16                                       # does not fit the table
+    expect("do not fit", pt, c, cu, P, 3, max_q=8)
+    expect("exceeds max_q", pt, ctx, cu, P, int(np.argmax(k)), max_q=int(k.max()) - 1)
+    u = cu.copy()
+    u[0] = 1
+    expect("cu_q", pt, ctx, u, P, 0, max_q=8)
+    # two windows writing one page, and a window page read by another sequence
+    c = ctx.copy()
+    c[0], c[1] = 33, 50
+    u = np.concatenate([[0], np.cumsum(np.r_[4, 4, k[2:]])]).astype(np.int32)
+    x = pt.copy()
+    x[1, 3] = x[0, 2]
+    expect("written by the windows", x, c, u, P, 1, max_q=8)
+    x = pt.copy()
+    x[1, 0] = x[0, 2]
+    expect("read by sequence", x, c, u, P, 1, max_q=8)
+    expect("listed twice", pt, ctx, cu, P, 2, max_q=8, seq_ids=np.array([2, 2], np.int32))
+    expect("seq_ids", pt, ctx, cu, P, -1, max_q=8, seq_ids=np.array([0, 9], np.int32))

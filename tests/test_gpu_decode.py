@@ -23,7 +23,7 @@ from tests import parity
 from tests.workload import to_np
 
 pytestmark = pytest.mark.gpu
-CDF_TOL = 1e-5
+CDF_TOL = parity.CDF_TOL
 
 
 def _say(msg):

@@ -121,3 +121,31 @@ def test_full_size_teacher_rows_sampled():
     sub = {k: (v[torch.from_numpy(rows).cuda()] if v is not None else None) for k, v in g.items()}
     c = parity.check_lmhead(sub, ref, logits, 16)
     _say(f"  excluded {c['excluded']} of {c['rows']}")
+
+
+def test_recompute_with_a_long_survivor_list():
+    """Ten groups each hold four of the top-32 logits, so the merge recomputes
+    all ten (1280 logits); 1470 other records tie at the lower bound theta
+    and survive, so the survivors and the recomputed logits together exceed
+    the merge's list and it must select from all group records.  Logits are
+    exact (one non-zero channel), the ties are broken by index, so the top-K
+    list is unique and compared in full."""
+    V, Hd, K = 64000, 64, 32
+    _say(f"[lmhead] long survivor list with recompute V={V} K={K}")
+    W = torch.zeros(V, Hd)
+    W[:, 0] = 0.5                                    # every other logit: 0.5
+    for grp in range(10):                            # groups 0..9: four members each
+        W[grp * 128 + 0, 0] = 4.0
+        W[grp * 128 + 1, 0] = 3.0
+        W[grp * 128 + 2, 0] = 2.0
+        W[grp * 128 + 3, 0] = 1.0 + grp / 16.0       # the fourth members rank by group
+    h = torch.zeros(2, Hd)
+    h[:, 0] = 1.0
+    h, W = h.cuda().to(torch.bfloat16), W.cuda().to(torch.bfloat16)
+    prop = np.array([3, 9 * 128 + 3])
+    g, ref, logits = _check(h, W, prop, K)
+    want = ([grp * 128 for grp in range(10)] + [grp * 128 + 1 for grp in range(10)]
+            + [grp * 128 + 2 for grp in range(10)] + [9 * 128 + 3, 8 * 128 + 3])
+    for r in range(2):
+        assert to_np(g["topk_idx"])[r].tolist() == want
+        assert ref["topk_idx"][r].tolist() == want

@@ -56,3 +56,30 @@ def batch_proposals(batch, logits_per_model=None) -> np.ndarray:
         prop[rows] = compose_proposals(lg, batch.u_mode[rows], batch.u_tok[rows],
                                        cfg.p_argmax, cfg.alt_mode, cfg.alt_temperature)
     return prop
+
+
+def gpu_proposals(batch, mdl) -> torch.Tensor:
+    """The synthetic proposer for full-size batches, on the GPU: per row of
+    ``mdl``, the verifier's argmax with probability p_argmax, else a uniform
+    token or an inverse-CDF sample of softmax(l / T_alt), from fp32 logits of
+    a torch matmul.  Workload synthesis only: both the GPU path and the
+    oracle score the tokens it returns (int32 [M], on the GPU)."""
+    cfg = batch.cfg
+    dev = mdl.hidden.device
+    rows = to_np(mdl.rows).astype(np.int64)
+    M = len(rows)
+    um = torch.from_numpy(batch.u_mode[rows]).to(dev)
+    ut = torch.from_numpy(batch.u_tok[rows]).to(dev)
+    Wf = mdl.W.float()
+    out = torch.empty(M, dtype=torch.int64, device=dev)
+    for r0 in range(0, M, 64):
+        l = mdl.hidden[r0:r0 + 64].float() @ Wf.T
+        am = l.argmax(1)
+        if cfg.alt_mode == "uniform":
+            alt = torch.clamp((ut[r0:r0 + 64] * l.shape[1]).long(), max=l.shape[1] - 1)
+        else:
+            cdf = torch.softmax(l.double() / cfg.alt_temperature, 1).cumsum(1)
+            alt = torch.searchsorted(cdf, (ut[r0:r0 + 64] * cdf[:, -1]).unsqueeze(1)).squeeze(1)
+            alt = torch.clamp(alt, max=l.shape[1] - 1)
+        out[r0:r0 + 64] = torch.where(um[r0:r0 + 64] < cfg.p_argmax, am, alt)
+    return out.int()
