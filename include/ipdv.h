@@ -220,6 +220,35 @@ int ipdv_check_page_table(const int32_t* page_table, int B, int max_pages_per_se
                           const int32_t* seq_ids, int n_seq, int max_q,
                           int page_size, int num_pages, int32_t* bad_seq);
 
+/*
+ * verify_attn_paged_noalloc -- verify_attn_paged without a workspace
+ * argument, for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid allocation).
+ * Same arguments, contract and results as verify_attn_paged (the same
+ * kernels and split plan); the split-KV partials go to a scratch array of
+ * IPDV_NOALLOC_SCRATCH_BYTES that the library holds on each GPU it runs on
+ * until the process ends.  The call allocates nothing.
+ *
+ * Limit: calls whose workspace (ipdv_attn_workspace_size) exceeds
+ * IPDV_NOALLOC_SCRATCH_BYTES return IPDV_EUNSUPPORTED before launching.
+ * Every call on one GPU uses the same scratch: calls that may overlap on one
+ * GPU (different streams without ordering, or other threads) race and must
+ * be serialised by the caller.  Nothing in the scratch needs to start at
+ * zero.
+ *
+ * Errors: those of verify_attn_paged except IPDV_EWORKSPACE; IPDV_EUNSUPPORTED
+ * for a call above the limit.
+ */
+#define IPDV_NOALLOC_SCRATCH_BYTES (128u << 20)
+int verify_attn_paged_noalloc(const void* q, const void* k_new, const void* v_new,
+                              void* k_cache, void* v_cache,
+                              const int32_t* page_table, int max_pages_per_seq,
+                              const int32_t* ctx_lens, const int32_t* cu_q,
+                              const int32_t* seq_ids, int n_seq, int max_q,
+                              void* out,
+                              int Hq, int Hkv, int D, int page_size, int num_pages, float scale,
+                              int dtype, void* hip_stream);
+
 /* Workspace bytes lmhead_logsoftmax_verify needs (0 if invalid). */
 size_t ipdv_lmhead_workspace_size(int M, int Hd, int V, int K);
 

@@ -18,6 +18,7 @@
 // include the C header); these keep the two in step.
 static_assert(IPDV_MAX_K == IPDV_MAX_K_DEV, "top-K limit");
 static_assert(IPDV_MAX_GATHER == IPDV_MAX_GATHER_DEV, "gather limit");
+static_assert(IPDV_NOALLOC_SCRATCH_BYTES == IPDV_NOALLOC_SCRATCH_BYTES_DEV, "scratch size");
 static_assert(IPDV_DRIVER_S == IPDV_DRIVER_S_DEV, "driver code");
 static_assert(IPDV_SRC_S == IPDV_SRC_S_DEV && IPDV_SRC_T == IPDV_SRC_T_DEV, "source labels");
 static_assert(IPDV_TAKE_COVERAGE == IPDV_TAKE_COVERAGE_DEV &&
@@ -113,21 +114,41 @@ size_t ipdv_attn_workspace_size(int n_seq, int Hq, int Hkv, int D, int max_q,
   return ipdv::attn_plan(n_seq, Hq, Hkv, D, max_q, max_pages_per_seq, page_size).workspace_bytes;
 }
 
-int verify_attn_paged(const void* q, const void* k_new, const void* v_new, void* k_cache,
-                      void* v_cache, const int32_t* page_table, int max_pages_per_seq,
-                      const int32_t* ctx_lens, const int32_t* cu_q, const int32_t* seq_ids,
-                      int n_seq, int max_q, void* out, int Hq, int Hkv, int D, int page_size,
-                      int num_pages, float scale, int dtype, void* workspace,
-                      size_t workspace_bytes, void* hip_stream) {
+// Argument checks shared by both attention entry points (everything but the
+// workspace).  Returns IPDV_OK with *empty set when there is nothing to launch.
+static int attn_args_check(const void* q, const void* k_new, const void* v_new, void* k_cache,
+                           void* v_cache, const int32_t* page_table, int max_pages_per_seq,
+                           const int32_t* ctx_lens, const int32_t* cu_q, int n_seq, int max_q,
+                           void* out, int Hq, int Hkv, int D, int page_size, int num_pages,
+                           float scale, int dtype, bool* empty) {
+  *empty = false;
   int st = attn_shape_check(n_seq, Hq, Hkv, D, max_q, max_pages_per_seq, page_size);
   if (st != IPDV_OK) return st;
   if (dtype != IPDV_F32 && dtype != IPDV_BF16) return fail(IPDV_EUNSUPPORTED, "dtype %d", dtype);
   if (dtype == IPDV_F32 && D != 64) return fail(IPDV_EUNSUPPORTED, "fp32 attention supports D=64 only");
   if (num_pages < 1) return fail(IPDV_EINVAL, "num_pages must be >= 1 (got %d)", num_pages);
   if (!std::isfinite(scale) || !(scale > 0.f)) return fail(IPDV_EINVAL, "scale must be positive and finite");
-  if (n_seq == 0) return ok();
+  if (n_seq == 0) {
+    *empty = true;
+    return IPDV_OK;
+  }
   if (!q || !k_new || !v_new || !k_cache || !v_cache || !page_table || !ctx_lens || !cu_q || !out)
     return fail(IPDV_EINVAL, "null required pointer");
+  return IPDV_OK;
+}
+
+int verify_attn_paged(const void* q, const void* k_new, const void* v_new, void* k_cache,
+                      void* v_cache, const int32_t* page_table, int max_pages_per_seq,
+                      const int32_t* ctx_lens, const int32_t* cu_q, const int32_t* seq_ids,
+                      int n_seq, int max_q, void* out, int Hq, int Hkv, int D, int page_size,
+                      int num_pages, float scale, int dtype, void* workspace,
+                      size_t workspace_bytes, void* hip_stream) {
+  bool empty;
+  int st = attn_args_check(q, k_new, v_new, k_cache, v_cache, page_table, max_pages_per_seq,
+                           ctx_lens, cu_q, n_seq, max_q, out, Hq, Hkv, D, page_size, num_pages,
+                           scale, dtype, &empty);
+  if (st != IPDV_OK) return st;
+  if (empty) return ok();
   const ipdv::AttnPlan pl = ipdv::attn_plan(n_seq, Hq, Hkv, D, max_q, max_pages_per_seq, page_size);
   if (!workspace || workspace_bytes < pl.workspace_bytes)
     return fail(IPDV_EWORKSPACE, "workspace of %zu bytes needed (got %zu)", pl.workspace_bytes,
@@ -137,6 +158,32 @@ int verify_attn_paged(const void* q, const void* k_new, const void* v_new, void*
                      scale, dtype == IPDV_BF16, workspace};
   hipError_t e = ipdv::launch_verify_attn(L, pl, reinterpret_cast<hipStream_t>(hip_stream));
   if (e != hipSuccess) return hip_fail("verify_attn_paged launch", e);
+  return ok();
+}
+
+int verify_attn_paged_noalloc(const void* q, const void* k_new, const void* v_new, void* k_cache,
+                              void* v_cache, const int32_t* page_table, int max_pages_per_seq,
+                              const int32_t* ctx_lens, const int32_t* cu_q, const int32_t* seq_ids,
+                              int n_seq, int max_q, void* out, int Hq, int Hkv, int D,
+                              int page_size, int num_pages, float scale, int dtype,
+                              void* hip_stream) {
+  bool empty;
+  int st = attn_args_check(q, k_new, v_new, k_cache, v_cache, page_table, max_pages_per_seq,
+                           ctx_lens, cu_q, n_seq, max_q, out, Hq, Hkv, D, page_size, num_pages,
+                           scale, dtype, &empty);
+  if (st != IPDV_OK) return st;
+  if (empty) return ok();
+  const ipdv::AttnPlan pl = ipdv::attn_plan(n_seq, Hq, Hkv, D, max_q, max_pages_per_seq, page_size);
+  if (pl.workspace_bytes > IPDV_NOALLOC_SCRATCH_BYTES)
+    return fail(IPDV_EUNSUPPORTED,
+                "this call needs %zu bytes of split-KV scratch; the allocation-free entry point "
+                "holds %zu (use verify_attn_paged with a workspace)",
+                pl.workspace_bytes, (size_t)IPDV_NOALLOC_SCRATCH_BYTES);
+  ipdv::AttnLaunch L{q, k_new, v_new, k_cache, v_cache, page_table, max_pages_per_seq,
+                     ctx_lens, cu_q, seq_ids, n_seq, out, Hq, Hkv, D, page_size, num_pages,
+                     scale, dtype == IPDV_BF16, nullptr};
+  hipError_t e = ipdv::launch_verify_attn_noalloc(L, pl, reinterpret_cast<hipStream_t>(hip_stream));
+  if (e != hipSuccess) return hip_fail("verify_attn_paged_noalloc", e);
   return ok();
 }
 

@@ -7,6 +7,7 @@
 
 #define IPDV_MAX_K_DEV 32
 #define IPDV_MAX_GATHER_DEV 64
+#define IPDV_NOALLOC_SCRATCH_BYTES_DEV (128u << 20)
 #define IPDV_DRIVER_S_DEV 0
 #define IPDV_TAKE_COVERAGE_DEV 0
 #define IPDV_TAKE_ENTROPY_DEV 1
@@ -64,6 +65,10 @@ struct AttnLaunch {
 
 AttnPlan attn_plan(int n_seq, int Hq, int Hkv, int D, int max_q, int max_pages, int page_size);
 hipError_t launch_verify_attn(const AttnLaunch& L, const AttnPlan& pl, hipStream_t st);
+// The same launches with the split-KV partials in the library's per-device
+// scratch array (L.workspace is ignored); pl.workspace_bytes must not exceed
+// IPDV_NOALLOC_SCRATCH_BYTES_DEV.
+hipError_t launch_verify_attn_noalloc(const AttnLaunch& L, const AttnPlan& pl, hipStream_t st);
 
 // ---- LM head + log-softmax ----
 struct LmPlan {

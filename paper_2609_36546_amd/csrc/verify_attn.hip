@@ -44,6 +44,7 @@
 // between workgroups (stream-K).  Both kernels share the block arithmetic
 // (attend_block) and the pool layouts.
 #include <algorithm>
+#include <mutex>
 
 #include "common.h"
 #include "kernels.h"
@@ -1039,6 +1040,50 @@ AttnPlan attn_plan(int n_seq, int Hq, int Hkv, int D, int max_q, int max_pages, 
     pl.workspace_bytes = pl.sk_o_bytes + pl.sk_lse_bytes + (n_it + 1) * sizeof(int32_t) + 256;
   }
   return pl;
+}
+
+// Split-KV scratch of the allocation-free entry point (verify_attn_paged_noalloc):
+// every partial and item start a call reads is written earlier in the same
+// call, so nothing in it needs clearing.  Each GPU the library runs on holds
+// its own copy until the process ends; calls that overlap on one GPU share it
+// and race.
+static __device__ __align__(256) char scratch[IPDV_NOALLOC_SCRATCH_BYTES_DEV];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices];   // device address of `scratch`, per device
+
+// The current device's address of `scratch`, looked up once per device with
+// that device current.  In host code the array's name is not a device address.
+hipError_t scratch_address(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return hipSuccess;
+}
+
+}  // namespace
+
+hipError_t launch_verify_attn_noalloc(const AttnLaunch& L, const AttnPlan& pl, hipStream_t st) {
+  if (pl.workspace_bytes > IPDV_NOALLOC_SCRATCH_BYTES_DEV) return hipErrorInvalidValue;
+  void* ws = nullptr;
+  const hipError_t e = scratch_address(&ws);
+  if (e != hipSuccess) return e;
+  AttnLaunch l2 = L;
+  l2.workspace = ws;
+  return launch_verify_attn(l2, pl, st);
 }
 
 hipError_t launch_verify_attn(const AttnLaunch& L, const AttnPlan& pl, hipStream_t st) {

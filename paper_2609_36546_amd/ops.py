@@ -54,6 +54,9 @@ def lib() -> ctypes.CDLL:
         L.ipdv_check_page_table.argtypes = [vp, ci, ci, vp, vp, vp, ci, ci, ci, ci,
                                             ctypes.POINTER(ctypes.c_int32)]
         L.ipdv_check_page_table.restype = ci
+        L.verify_attn_paged_noalloc.argtypes = [vp, vp, vp, vp, vp, i32p, ci, i32p, i32p, i32p, ci,
+                                                ci, vp, ci, ci, ci, ci, ci, cf, ci, vp]
+        L.verify_attn_paged_noalloc.restype = ci
         L.lmhead_logsoftmax_verify.argtypes = [vp, vp, i32p, i32p, ci, ci, ci, ci, f32p, f32p, i32p,
                                                i32p, f32p, f32p, ci, vp, cs, vp]
         L.lmhead_logsoftmax_verify.restype = ci
@@ -237,6 +240,54 @@ def verify_attn_paged(q, k_new, v_new, k_cache, v_cache, page_table, ctx_lens, c
         Hq, Hkv, D, ps, P, float(scale), _dtype_code(dt), _ptr(workspace),
         workspace.numel() * workspace.element_size(), _stream(dev))
     _check("verify_attn_paged", st)
+    return out
+
+
+NOALLOC_SCRATCH_BYTES = 128 << 20
+
+
+def verify_attn_paged_noalloc(q, k_new, v_new, k_cache, v_cache, page_table, ctx_lens, cu_q,
+                              max_q: int, seq_ids=None, n_seq: Optional[int] = None,
+                              scale: Optional[float] = None, out=None):
+    """verify_attn_paged_noalloc (see include/ipdv.h): verify_attn_paged with
+    its split-KV partials in the library's per-device scratch.  Allocates
+    nothing when `out` is given."""
+    dev = q.device
+    dt = q.dtype
+    _need(q, "q", dt, dev, 3)
+    T, Hq, D = q.shape
+    _need(k_new, "k_new", dt, dev, 3)
+    _need(v_new, "v_new", dt, dev, 3)
+    Hkv = k_new.shape[1]
+    _need(k_cache, "k_cache", dt, dev, 5)
+    _need(v_cache, "v_cache", dt, dev, 4)
+    P, ps = k_cache.shape[0], k_cache.shape[3]
+    if tuple(k_cache.shape) != (P, Hkv, D // 32, ps, 32) or tuple(v_cache.shape) != (P, Hkv, D, ps):
+        raise ValueError("k_cache must be [P,Hkv,D/32,ps,32] and v_cache [P,Hkv,D,ps]")
+    if tuple(k_new.shape) != (T, Hkv, D) or tuple(v_new.shape) != (T, Hkv, D):
+        raise ValueError("k_new / v_new must be [T,Hkv,D]")
+    _need(page_table, "page_table", torch.int32, dev, 2)
+    _need(ctx_lens, "ctx_lens", torch.int32, dev, 1)
+    _need(cu_q, "cu_q", torch.int32, dev, 1)
+    B = ctx_lens.shape[0]
+    if cu_q.shape[0] != B + 1 or page_table.shape[0] != B:
+        raise ValueError("cu_q must be [B+1] and page_table [B, maxp]")
+    if seq_ids is not None:
+        _need(seq_ids, "seq_ids", torch.int32, dev, 1)
+        n_seq = seq_ids.shape[0] if n_seq is None else n_seq
+    elif n_seq is None:
+        n_seq = B
+    if scale is None:
+        scale = 1.0 / math.sqrt(D)
+    if out is None:
+        out = torch.empty_like(q)
+    else:
+        _need(out, "out", dt, dev, 3)
+    st = lib().verify_attn_paged_noalloc(
+        _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(k_cache), _ptr(v_cache), _ptr(page_table),
+        page_table.shape[1], _ptr(ctx_lens), _ptr(cu_q), _ptr(seq_ids), n_seq, max_q, _ptr(out),
+        Hq, Hkv, D, ps, P, float(scale), _dtype_code(dt), _stream(dev))
+    _check("verify_attn_paged_noalloc", st)
     return out
 
 

@@ -233,6 +233,8 @@ def test_binding_and_oracle_constants_match_the_header():
                         ("SRC_S", "IPDV_SRC_S"), ("SRC_T", "IPDV_SRC_T"),
                         ("SRC_DISCARDED", "IPDV_SRC_DISCARDED")):
         assert getattr(oracle, name) == defs[macro], name
+    m = re.search(r"#define\s+IPDV_NOALLOC_SCRATCH_BYTES\s+\((\d+)u\s*<<\s*(\d+)\)", open(HEADER).read())
+    assert ops.NOALLOC_SCRATCH_BYTES == int(m.group(1)) << int(m.group(2))
 
 
 def test_tiled_w_argument_errors():
@@ -335,3 +337,22 @@ def test_page_table_check_names_each_violation():
     expect("read by sequence", x, c, u, P, 1, max_q=8)
     expect("listed twice", pt, ctx, cu, P, 2, max_q=8, seq_ids=np.array([2, 2], np.int32))
     expect("seq_ids", pt, ctx, cu, P, -1, max_q=8, seq_ids=np.array([0, 9], np.int32))
+
+
+def test_noalloc_attention_rejects_calls_above_its_scratch_on_the_host():
+    """The allocation-free entry point checks its arguments like
+    verify_attn_paged and refuses a call whose split-KV partials exceed its
+    scratch, before any HIP call (dummy pointers: nothing is launched)."""
+    vp = ctypes.c_void_p
+    L = ops.lib()
+
+    def call(maxp, n_seq=4, D=128, q=1):
+        return L.verify_attn_paged_noalloc(vp(q), vp(1), vp(1), vp(1), vp(1), vp(1), maxp, vp(1),
+                                           vp(1), None, n_seq, 8, vp(1), 32, 4, D, 16, 8, 0.088,
+                                           ops.IPDV_BF16, None)
+    assert ops.attn_workspace_size(4, 32, 4, 128, 8, 200000, 16) > ops.NOALLOC_SCRATCH_BYTES
+    assert call(200000) == -2
+    assert "scratch" in L.ipdv_last_error().decode()
+    assert call(100, D=96) == -2                 # the same argument checks as verify_attn_paged
+    assert call(100, q=None) == -1
+    assert call(100, n_seq=0, q=None) == 0       # nothing to do
