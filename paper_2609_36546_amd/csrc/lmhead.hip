@@ -348,18 +348,19 @@ constexpr int kDStage = 32;   // hidden channels per stage (64 bytes per row)
 
 __device__ __forceinline__ int dl_off(int r, int c) { return 64 * r + 16 * (c ^ ((r >> 2) & 3)); }
 
-template <int RB, int NBUF>
-__global__ __launch_bounds__(256) void lmhead_gemm_dlds_kernel(LmParams p) {
+template <int RB, int NBUF, int NW>
+__global__ __launch_bounds__(64 * NW) void lmhead_gemm_dlds_kernel(LmParams p) {
   static_assert(NBUF >= 3 && NBUF <= 5, "ring depth");
+  static_assert(NW == 4 || NW == 8, "2 x (NW / 2) waves");
   int vt, rt;
   if (!gemm_tile(p, vt, rt)) return;
-  constexpr int NM = 64 * RB;
+  constexpr int NM = 32 * RB * (NW / 2);        // hidden rows per workgroup
   constexpr int WB = kVT * 64;                  // W tile bytes per stage
   constexpr int SB = WB + NM * 64;              // stage bytes
   constexpr int NBLK = (kVT + NM) / 16;         // 1 KB load blocks per stage
-  constexpr int PW = NBLK / 4;                  // load instructions per wave and stage
+  constexpr int PW = NBLK / NW;                 // load instructions per wave and stage
   constexpr int KS = kDStage / 16;              // MFMA k-steps per stage
-  static_assert(KS == 2 && (NBUF - 2) * PW <= 63, "pipeline shape");
+  static_assert(KS == 2 && (NBUF - 2) * PW <= 63 && NBLK % NW == 0, "pipeline shape");
   const int m0 = rt * NM;
   const int v0 = vt * kVT;
   const int tid = threadIdx.x;
@@ -378,7 +379,7 @@ __global__ __launch_bounds__(256) void lmhead_gemm_dlds_kernel(LmParams p) {
   const bf16* src[PW];
 #pragma unroll
   for (int j = 0; j < PW; ++j) {
-    const int u = w + 4 * j;
+    const int u = w + NW * j;
     const int r = (u < kVT / 16 ? 16 * u : 16 * (u - kVT / 16)) + (lane >> 2);
     const int c = (lane & 3) ^ ((r >> 2) & 3);
     if (u < kVT / 16) {
@@ -401,14 +402,15 @@ __global__ __launch_bounds__(256) void lmhead_gemm_dlds_kernel(LmParams p) {
   // one into a free buffer, so that every wave has the same number of loads
   // in flight at every boundary.  dma(st, j0, j1): this wave's load blocks
   // [j0, j1) of stage st.
-  // Load blocks j < kVT / 64 are W (for every wave); a stage advances a tiled
+  // Load blocks j < kVT / (16 NW) are W (for every wave); a stage advances a tiled
   // W block by 512 elements per 32 channels.
   const int wk = p.w_tiled ? 16 : 1;
   auto dma = [&](int st, int j0, int j1) {
     char* buf = s_ring + (st % NBUF) * SB;
     const int k0 = min(st, nst - 1) * kDStage;
 #pragma unroll
-    for (int j = j0; j < j1; ++j) dma16(src[j] + (j < kVT / 64 ? wk * k0 : k0), buf + 1024 * (w + 4 * j));
+    for (int j = j0; j < j1; ++j)
+      dma16(src[j] + (j < kVT / (16 * NW) ? wk * k0 : k0), buf + 1024 * (w + NW * j));
   };
   // Operand offsets of this lane within a stage.  Chunk 2 ks + h of a row sits
   // at 16 ((2 ks + h) ^ q), q = row bits 2-3, which is the ks = 0 offset xor
@@ -1149,10 +1151,17 @@ __global__ __launch_bounds__(kMT) void sample_kernel(LmParams p, SampleParams s)
 // hidden size is a multiple of four stages, fp32 the register-staged one.
 template <int RB>
 void launch_gemm(const LmParams& p, dim3 grid, hipStream_t st, bf16) {
+  // 64 * RB hidden rows per workgroup.  256 and 128 rows take eight waves
+  // (two per SIMD, each 128 vocabulary entries x 32 * RB / 2 rows), 64 and
+  // 192 rows four.
   if (p.Hd % kDStage != 0)
     hipLaunchKernelGGL((lmhead_gemm_kernel<bf16, RB>), grid, dim3(256), 0, st, p);
+  else if constexpr (RB == 4)
+    hipLaunchKernelGGL((lmhead_gemm_dlds_kernel<2, 4, 8>), grid, dim3(512), 0, st, p);
+  else if constexpr (RB == 2)
+    hipLaunchKernelGGL((lmhead_gemm_dlds_kernel<1, 4, 8>), grid, dim3(512), 0, st, p);
   else
-    hipLaunchKernelGGL((lmhead_gemm_dlds_kernel<RB, 4>), grid, dim3(256), 0, st, p);
+    hipLaunchKernelGGL((lmhead_gemm_dlds_kernel<RB, 4, 4>), grid, dim3(256), 0, st, p);
 }
 
 template <int RB>
