@@ -74,6 +74,7 @@ hipError_t launch_verify_attn_noalloc(const AttnLaunch& L, const AttnPlan& pl, h
 struct LmPlan {
   int n_groups, n_vt, n_rt, rb;
   size_t rec_bytes, workspace_bytes;
+  size_t hid_off;      // byte offset of the packed hidden copy (bf16) in the workspace
 };
 
 struct LmLaunch {

@@ -40,6 +40,7 @@ constexpr float kLn2 = 0.6931471805599453f;
 
 struct LmParams {
   const void* hidden;
+  const void* hidden_tiled;   // bf16 hidden rows in W's tiled block layout (workspace copy)
   const void* W;
   const int32_t* prop_tok;
   const int32_t* out_rows;
@@ -73,6 +74,23 @@ struct LmParams {
 __device__ __forceinline__ size_t w_off(const LmParams& p, int v, int c) {
   return p.w_tiled ? ((size_t)(v >> 4) * (p.Hd >> 5) + (c >> 5)) * 512 + (v & 15) * 32 + (c & 31)
                    : (size_t)v * p.Hd + c;
+}
+
+// W [V][Hd] -> [ceil(V/16)][Hd/32][16][32]: one thread per 16-byte chunk of
+// the output, in output order (rows past V are zero).
+__global__ __launch_bounds__(256) void pack_w_kernel(const bf16* W, int V, int Hd, bf16* Wt,
+                                                     size_t n_chunks) {
+  const size_t t = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (t >= n_chunks) return;
+  const size_t blk = t >> 6;                 // 64 chunks per 1 KB block
+  const int within = (int)(t & 63);
+  const int nb_c = Hd >> 5;
+  const int v = (int)(blk / nb_c) * 16 + (within >> 2);
+  const int c = (int)(blk % nb_c) * 32 + (within & 3) * 8;
+  typedef __attribute__((__vector_size__(16))) int i32x4;
+  i32x4 x = {0, 0, 0, 0};
+  if (v < V) x = ld16<i32x4>(W + (size_t)v * Hd + c);
+  *reinterpret_cast<i32x4*>(Wt + t * 8) = x;
 }
 
 // MFMA flavour per input type.  STAGE = hidden channels per pipeline stage;
@@ -374,7 +392,7 @@ __global__ __launch_bounds__(64 * NW) void lmhead_gemm_dlds_kernel(LmParams p) {
   __shared__ __attribute__((aligned(1024))) char s_ring[NBUF * SB];
 
   const bf16* Wp = reinterpret_cast<const bf16*>(p.W);
-  const bf16* Hp = reinterpret_cast<const bf16*>(p.hidden);
+  const bf16* Hp = reinterpret_cast<const bf16*>(p.hidden_tiled);
   // This lane's source row and chunk for each of its load blocks.
   const bf16* src[PW];
 #pragma unroll
@@ -394,8 +412,10 @@ __global__ __launch_bounds__(64 * NW) void lmhead_gemm_dlds_kernel(LmParams p) {
         src[j] = Wp + (size_t)v * p.Hd + 8 * c;
       }
     } else {
-      const int m = min(m0 + r, p.M - 1);       // rows past M: any valid row, never stored
-      src[j] = Hp + (size_t)m * p.Hd + 8 * c;
+      // hidden rows come from the per-call copy in the same 16-row x 32-channel
+      // block layout (rows past M there are zero and never stored)
+      const int mb = min((m0 >> 4) + (u - kVT / 16), ((p.M + 15) >> 4) - 1);
+      src[j] = Hp + (size_t)mb * (p.Hd >> 5) * 512 + (lane >> 2) * 32 + 8 * c;
     }
   }
   // Stage st goes to buffer st % NBUF.  Stages past the end reload the last
@@ -403,14 +423,14 @@ __global__ __launch_bounds__(64 * NW) void lmhead_gemm_dlds_kernel(LmParams p) {
   // in flight at every boundary.  dma(st, j0, j1): this wave's load blocks
   // [j0, j1) of stage st.
   // Load blocks j < kVT / (16 NW) are W (for every wave); a stage advances a tiled
-  // W block by 512 elements per 32 channels.
+  // block (W when packed, the hidden copy always) by 512 elements per 32 channels.
   const int wk = p.w_tiled ? 16 : 1;
   auto dma = [&](int st, int j0, int j1) {
     char* buf = s_ring + (st % NBUF) * SB;
     const int k0 = min(st, nst - 1) * kDStage;
 #pragma unroll
     for (int j = j0; j < j1; ++j)
-      dma16(src[j] + (j < kVT / (16 * NW) ? wk * k0 : k0), buf + 1024 * (w + NW * j));
+      dma16(src[j] + (j < kVT / (16 * NW) ? wk : 16) * k0, buf + 1024 * (w + NW * j));
   };
   // Operand offsets of this lane within a stage.  Chunk 2 ks + h of a row sits
   // at 16 ((2 ks + h) ^ q), q = row bits 2-3, which is the ks = 0 offset xor
@@ -1153,10 +1173,18 @@ template <int RB>
 void launch_gemm(const LmParams& p, dim3 grid, hipStream_t st, bf16) {
   // 64 * RB hidden rows per workgroup.  256 and 128 rows take eight waves
   // (two per SIMD, each 128 vocabulary entries x 32 * RB / 2 rows), 64 and
-  // 192 rows four.
-  if (p.Hd % kDStage != 0)
+  // 192 rows four.  The direct-to-LDS kernels read the hidden rows from a
+  // copy in W's tiled block layout, written first into the workspace, so
+  // that every operand load reads whole cache lines.
+  if (p.Hd % kDStage != 0) {
     hipLaunchKernelGGL((lmhead_gemm_kernel<bf16, RB>), grid, dim3(256), 0, st, p);
-  else if constexpr (RB == 4)
+    return;
+  }
+  const size_t n_chunks = (size_t)((p.M + 15) / 16) * 16 * p.Hd / 8;
+  hipLaunchKernelGGL(pack_w_kernel, dim3((unsigned)((n_chunks + 255) / 256)), dim3(256), 0, st,
+                     reinterpret_cast<const bf16*>(p.hidden), p.M, p.Hd,
+                     reinterpret_cast<bf16*>(const_cast<void*>(p.hidden_tiled)), n_chunks);
+  if constexpr (RB == 4)
     hipLaunchKernelGGL((lmhead_gemm_dlds_kernel<2, 4, 8>), grid, dim3(512), 0, st, p);
   else if constexpr (RB == 2)
     hipLaunchKernelGGL((lmhead_gemm_dlds_kernel<1, 4, 8>), grid, dim3(512), 0, st, p);
@@ -1198,8 +1226,8 @@ LmPlan lm_plan(int M, int Hd, int V, int K, bool bf16) {
   pl.n_rt = (M + 64 * pl.rb - 1) / (64 * pl.rb);
   const size_t recs = (size_t)M * pl.n_groups;
   pl.rec_bytes = recs * sizeof(float);
-  pl.workspace_bytes = 12 * ((pl.rec_bytes + 255) / 256 * 256) + 256;
-  (void)Hd;
+  pl.hid_off = 12 * ((pl.rec_bytes + 255) / 256 * 256);
+  pl.workspace_bytes = pl.hid_off + (bf16 ? (size_t)((M + 15) / 16) * 16 * Hd * 2 : 0) + 256;
   (void)K;
   return pl;
 }
@@ -1212,6 +1240,7 @@ LmParams lm_params(const void* hidden, const void* W, int M, int Hd, int V, int 
                    void* workspace) {
   LmParams p{};
   p.hidden = hidden;
+  p.hidden_tiled = reinterpret_cast<char*>(workspace) + pl.hid_off;
   p.W = W;
   p.M = M;
   p.Hd = Hd;
@@ -1342,27 +1371,6 @@ hipError_t launch_sample_takeover(const SampleLaunch& L, const LmPlan& pl, hipSt
   trace_mark(st);
   return e;
 }
-
-namespace {
-
-// W [V][Hd] -> [ceil(V/16)][Hd/32][16][32]: one thread per 16-byte chunk of
-// the output, in output order (rows past V are zero).
-__global__ __launch_bounds__(256) void pack_w_kernel(const bf16* W, int V, int Hd, bf16* Wt,
-                                                     size_t n_chunks) {
-  const size_t t = (size_t)blockIdx.x * 256 + threadIdx.x;
-  if (t >= n_chunks) return;
-  const size_t blk = t >> 6;                 // 64 chunks per 1 KB block
-  const int within = (int)(t & 63);
-  const int nb_c = Hd >> 5;
-  const int v = (int)(blk / nb_c) * 16 + (within >> 2);
-  const int c = (int)(blk % nb_c) * 32 + (within & 3) * 8;
-  typedef __attribute__((__vector_size__(16))) int i32x4;
-  i32x4 x = {0, 0, 0, 0};
-  if (v < V) x = ld16<i32x4>(W + (size_t)v * Hd + c);
-  *reinterpret_cast<i32x4*>(Wt + t * 8) = x;
-}
-
-}  // namespace
 
 hipError_t launch_pack_w(const void* W, int V, int Hd, void* W_tiled, hipStream_t st) {
   const size_t n_chunks = (size_t)((V + 15) / 16) * 16 * Hd / 8;
