@@ -47,6 +47,7 @@ struct LmParams {
   int M, Hd, V, K;
   int w_tiled;        // W in 16-row x 32-channel blocks (lmhead_pack_w), else [V][Hd]
   int n_groups, n_rt, n_vt;
+  int vt_base, n_vt_run;   // this launch's vocabulary tiles: vt_base .. vt_base + n_vt_run - 1
   // Group records, [M][n_groups] each: the three largest logits of the group
   // with their indices, the fourth largest value, sum exp(l - v1) over each
   // 32-entry quarter of the group (rec_sq[q]: entries 32 q .. 32 q + 31) and
@@ -246,15 +247,16 @@ __device__ __forceinline__ void lm_epilogue_any(const LmParams& p, floatx16 (&ac
 // and the row tiles of one vocabulary tile run back to back on it: the W tile
 // they share is fetched from HBM once into that XCD's L2, and every 64-byte
 // line of the group records (16 groups = 8 vocabulary tiles of one row) is
-// completed inside one L2 before it is written back.  The grid holds
-// ceil(n_vt / 8) * 8 * n_rt workgroups; the surplus returns at once.
+// completed inside one L2 before it is written back.  A launch covers the
+// vocabulary tiles vt_base .. vt_base + n_vt_run - 1; its grid holds
+// ceil(n_vt_run / 8) * 8 * n_rt workgroups; the surplus returns at once.
 __device__ __forceinline__ bool gemm_tile(const LmParams& p, int& vt, int& rt) {
   const int id = blockIdx.x;
   const int xcd = id & 7, local = id >> 3;
-  const int per = p.n_vt / 8, extra = p.n_vt % 8;
+  const int per = p.n_vt_run / 8, extra = p.n_vt_run % 8;
   const int j = local / p.n_rt;
   if (j >= per + (xcd < extra ? 1 : 0)) return false;
-  vt = xcd * per + min(xcd, extra) + j;
+  vt = p.vt_base + xcd * per + min(xcd, extra) + j;
   rt = local % p.n_rt;
   return true;
 }
@@ -1169,6 +1171,22 @@ __global__ __launch_bounds__(kMT) void sample_kernel(LmParams p, SampleParams s)
 
 // GEMM launch per input type: bf16 takes the direct-to-LDS kernel when the
 // hidden size is a multiple of four stages, fp32 the register-staged one.
+// Compute units of the current device (cached per device).
+int device_cus() {
+  static int cus[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cus[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+      n = 256;
+    cus[dev] = n;
+  }
+  return cus[dev];
+}
+
+dim3 gemm_grid(const LmParams& p) { return dim3((p.n_vt_run + 7) / 8 * 8 * p.n_rt); }
+
 template <int RB>
 void launch_gemm(const LmParams& p, dim3 grid, hipStream_t st, bf16) {
   // 64 * RB hidden rows per workgroup.  256 and 128 rows take eight waves
@@ -1184,9 +1202,29 @@ void launch_gemm(const LmParams& p, dim3 grid, hipStream_t st, bf16) {
   hipLaunchKernelGGL(pack_w_kernel, dim3((unsigned)((n_chunks + 255) / 256)), dim3(256), 0, st,
                      reinterpret_cast<const bf16*>(p.hidden), p.M, p.Hd,
                      reinterpret_cast<bf16*>(const_cast<void*>(p.hidden_tiled)), n_chunks);
-  if constexpr (RB == 4)
-    hipLaunchKernelGGL((lmhead_gemm_dlds_kernel<2, 4, 8>), grid, dim3(512), 0, st, p);
-  else if constexpr (RB == 2)
+  if constexpr (RB == 4) {
+    // With one row tile (M <= 256): 256-row tiles for as many whole rounds
+    // of one tile per compute unit as the vocabulary fills; the vocabulary
+    // tiles left over for a last, partial round run as 128-row tiles in a
+    // second launch, which spreads that round's work over twice as many
+    // compute units (M = 256: 594 tiles were 2.3 rounds).  With more row
+    // tiles the single launch's own tail balancing does better than a second
+    // launch after a kernel boundary (measured at M = 464 and 512).
+    const int cus = device_cus();
+    const int n_main = p.n_rt == 1 ? p.n_vt / cus * cus : p.n_vt;
+    LmParams q = p;
+    if (n_main > 0) {
+      q.vt_base = 0;
+      q.n_vt_run = n_main;
+      hipLaunchKernelGGL((lmhead_gemm_dlds_kernel<2, 4, 8>), gemm_grid(q), dim3(512), 0, st, q);
+    }
+    if (n_main < p.n_vt) {
+      q.vt_base = n_main;
+      q.n_vt_run = p.n_vt - n_main;
+      q.n_rt = (p.M + 127) / 128;
+      hipLaunchKernelGGL((lmhead_gemm_dlds_kernel<1, 4, 8>), gemm_grid(q), dim3(512), 0, st, q);
+    }
+  } else if constexpr (RB == 2)
     hipLaunchKernelGGL((lmhead_gemm_dlds_kernel<1, 4, 8>), grid, dim3(512), 0, st, p);
   else
     hipLaunchKernelGGL((lmhead_gemm_dlds_kernel<RB, 4, 4>), grid, dim3(256), 0, st, p);
@@ -1199,8 +1237,7 @@ void launch_gemm(const LmParams& p, dim3 grid, hipStream_t st, float) {
 
 template <typename DT, int RB>
 hipError_t launch_rb(const LmParams& p, hipStream_t st) {
-  const int n_vt_pad = (p.n_vt + 7) / 8 * 8;
-  dim3 grid(n_vt_pad * p.n_rt);
+  const dim3 grid = gemm_grid(p);
   trace_begin(st);
   launch_gemm<RB>(p, grid, st, DT{});
   hipError_t e = hipGetLastError();
@@ -1249,6 +1286,8 @@ LmParams lm_params(const void* hidden, const void* W, int M, int Hd, int V, int 
   p.n_groups = pl.n_groups;
   p.n_rt = pl.n_rt;
   p.n_vt = pl.n_vt;
+  p.vt_base = 0;
+  p.n_vt_run = pl.n_vt;
   const size_t stride = (pl.rec_bytes + 255) / 256 * 256;
   char* ws = reinterpret_cast<char*>(workspace);
   p.rec_v1 = reinterpret_cast<float*>(ws);
