@@ -73,6 +73,7 @@ hipError_t launch_verify_attn_noalloc(const AttnLaunch& L, const AttnPlan& pl, h
 // ---- LM head + log-softmax ----
 struct LmPlan {
   int n_groups, n_vt, n_rt, rb;
+  int rec_stride;      // record entries per row (n_groups rounded up to a multiple of 4)
   size_t rec_bytes, workspace_bytes;
   size_t hid_off;      // byte offset of the packed hidden copy (bf16) in the workspace
 };

@@ -47,8 +47,9 @@ struct LmParams {
   int M, Hd, V, K;
   int w_tiled;        // W in 16-row x 32-channel blocks (lmhead_pack_w), else [V][Hd]
   int n_groups, n_rt, n_vt;
+  int rec_stride;          // record entries per row: n_groups rounded up to a multiple of 4
   int vt_base, n_vt_run;   // this launch's vocabulary tiles: vt_base .. vt_base + n_vt_run - 1
-  // Group records, [M][n_groups] each: the three largest logits of the group
+  // Group records, [M][rec_stride] each: the three largest logits of the group
   // with their indices, the fourth largest value, sum exp(l - v1) over each
   // 32-entry quarter of the group (rec_sq[q]: entries 32 q .. 32 q + 31) and
   // sum exp(l - v1) * l over the group.
@@ -218,7 +219,7 @@ __device__ __forceinline__ void lm_epilogue(const LmParams& p, floatx16 (&acc)[4
     for (int q = 0; q < 4; ++q) sq[q] += __shfl_xor(sq[q], 32, kWave);
     ee += __shfl_xor(ee, 32, kWave);
     if (h == 0 && m < p.M && g < p.n_groups) {
-      const size_t r = (size_t)m * p.n_groups + g;
+      const size_t r = (size_t)m * p.rec_stride + g;
       p.rec_v1[r] = v1;
       p.rec_v2[r] = v2;
       p.rec_v3[r] = v3;
@@ -637,31 +638,41 @@ __device__ __forceinline__ void wave_topk(const float (&cv)[N], const int (&ci)[
   }
 }
 
-// wave_topk for at most 128 candidates with distinct indices, held two per
-// lane in registers: each round takes the wave's best remaining candidate and
-// its lane drops it, so no round re-reads LDS.  The picks come out in the same
-// order as wave_topk's.  A NaN value is never picked there, so it is dropped
-// on loading here.
-__device__ __forceinline__ void wave_topk_regs(const float* xv, const int* xi, int nx, int K,
-                                               float* out_v, int* out_i) {
-  const int lane = lane_id();
-  float v0 = -INFINITY, v1 = -INFINITY;
-  int i0 = 0x7fffffff, i1 = 0x7fffffff;
-  if (lane < nx) { v0 = xv[lane]; i0 = xi[lane]; }
-  if (lane + kWave < nx) { v1 = xv[lane + kWave]; i1 = xi[lane + kWave]; }
-  if (!(v0 >= -INFINITY)) { v0 = -INFINITY; i0 = 0x7fffffff; }
-  if (!(v1 >= -INFINITY)) { v1 = -INFINITY; i1 = 0x7fffffff; }
-  for (int k = 0; k < K; ++k) {
-    float bv = v0;
-    int bi = i0;
-    if (before(v1, i1, bv, bi)) { bv = v1; bi = i1; }
-    wave_best(bv, bi);
-    if (lane == 0) { out_v[k] = bv; out_i[k] = bi; }
-    if (bi != 0x7fffffff) {
-      if (i0 == bi) { v0 = -INFINITY; i0 = 0x7fffffff; }
-      if (i1 == bi) { v1 = -INFINITY; i1 = 0x7fffffff; }
+// Top-K of the n <= kMT entries of an LDS list with distinct indices, by
+// rank: thread t takes entry t and counts the entries before it in the
+// (value desc, index asc) order, reading the list as LDS broadcasts; an entry
+// of rank r < K goes to position r.  Positions without an entry get
+// (-inf, 0x7fffffff).  NaN values are never picked and precede nothing.
+// All threads of the block take part (two barriers).
+__device__ __forceinline__ void block_topk_rank(const float* lv, const int* li, int n, int K,
+                                                float* out_v, int* out_i) {
+  const int tid = threadIdx.x;
+  if (tid < K) {
+    out_v[tid] = -INFINITY;
+    out_i[tid] = 0x7fffffff;
+  }
+  __syncthreads();
+  if (tid < n) {
+    const float v = lv[tid];
+    const int i = li[tid];
+    if (v == v) {
+      // 16-byte broadcast reads of four entries at a time; entries past n
+      // (any contents) are excluded by their position
+      int r = 0;
+#pragma unroll 4
+      for (int c = 0; c < n; c += 4) {
+        const floatx4 y = *reinterpret_cast<const floatx4*>(lv + c);
+        const i32x4 yi = *reinterpret_cast<const i32x4*>(li + c);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) r += (c + e < n && before(y[e], yi[e], v, i)) ? 1 : 0;
+      }
+      if (r < K) {
+        out_v[r] = v;
+        out_i[r] = i;
+      }
     }
   }
+  __syncthreads();
 }
 
 constexpr int kCap = 2048;     // survivor list capacity (candidates >= theta)
@@ -747,18 +758,19 @@ __global__ __launch_bounds__(kMT) void lmhead_merge_kernel(LmParams p) {
   const int lane = lane_id();
   const int G = p.n_groups;
   const int K = p.K;
-  const size_t base = (size_t)m * G;
+  const size_t base = (size_t)m * p.rec_stride;
   constexpr int NW = kMT / kWave;
   __shared__ float s_red[3 * NW];
   __shared__ float s_theta[NW];
+  __shared__ __attribute__((aligned(16))) float s_tm[kMT];   // thread maxima (theta)
   __shared__ float s_wv[NW][IPDV_MAX_K_DEV];
   __shared__ int s_wi[NW][IPDV_MAX_K_DEV];
   __shared__ float s_top_v[IPDV_MAX_K_DEV];
   __shared__ int s_top_i[IPDV_MAX_K_DEV];
   __shared__ int s_split[kMaxSplit];
   __shared__ int s_nsplit, s_n;
-  __shared__ float s_lv[kCap];          // survivors, then survivors + recomputed logits
-  __shared__ int s_li[kCap];
+  __shared__ __attribute__((aligned(16))) float s_lv[kCap];   // survivors, then survivors + recomputed logits
+  __shared__ __attribute__((aligned(16))) int s_li[kCap];
   __shared__ float s_cv[kSplitCand];    // recomputed logits of split groups
   __shared__ int s_ci[kSplitCand];
   __shared__ float s_hid[kMaxHd];       // the row's hidden state, for recomputes
@@ -784,25 +796,45 @@ __global__ __launch_bounds__(kMT) void lmhead_merge_kernel(LmParams p) {
     }
   }
 
-  // This thread's groups: tid, tid + kMT, ... (register resident).
+  // This thread's groups (register resident): slot u holds group
+  // merge_group(u) = 4 kMT (u / 4) + 4 tid + u % 4, so each record field of
+  // four consecutive groups arrives in one 16-byte load.
   float cv[kCPG * kMaxGPT];
   int ci[kCPG * kMaxGPT];
   float rs[kMaxGPT], re[kMaxGPT];
   float mx = -INFINITY;
 #pragma unroll
-  for (int u = 0; u < kMaxGPT; ++u) {
-    const int gi = tid + kMT * u;
-    const bool ok = gi < G;
-    cv[kCPG * u] = ok ? p.rec_v1[base + gi] : -INFINITY;
-    cv[kCPG * u + 1] = ok ? p.rec_v2[base + gi] : -INFINITY;
-    cv[kCPG * u + 2] = ok ? p.rec_v3[base + gi] : -INFINITY;
-    ci[kCPG * u] = ok ? p.rec_i1[base + gi] : 0x7fffffff;
-    ci[kCPG * u + 1] = ok ? p.rec_i2[base + gi] : 0x7fffffff;
-    ci[kCPG * u + 2] = ok ? p.rec_i3[base + gi] : 0x7fffffff;
-    rs[u] = ok ? (p.rec_sq[0][base + gi] + p.rec_sq[1][base + gi]) +
-                     (p.rec_sq[2][base + gi] + p.rec_sq[3][base + gi]) : 0.f;
-    re[u] = ok ? p.rec_e[base + gi] : 0.f;
-    mx = fmaxf(mx, cv[kCPG * u]);
+  for (int blk = 0; blk < kMaxGPT / 4; ++blk) {
+    const int g4 = 4 * kMT * blk + 4 * tid;
+    const bool ok4 = g4 < G;
+    // loads are unconditional (a group past G reads group 0 of the row, or
+    // the padding of the last four; both are masked below)
+    const size_t o = base + (ok4 ? g4 : 0);
+    const floatx4 v1 = ld16<floatx4>(p.rec_v1 + o);
+    const floatx4 v2 = ld16<floatx4>(p.rec_v2 + o);
+    const floatx4 v3 = ld16<floatx4>(p.rec_v3 + o);
+    const i32x4 i1 = ld16<i32x4>(p.rec_i1 + o);
+    const i32x4 i2 = ld16<i32x4>(p.rec_i2 + o);
+    const i32x4 i3 = ld16<i32x4>(p.rec_i3 + o);
+    const floatx4 q0 = ld16<floatx4>(p.rec_sq[0] + o);
+    const floatx4 q1 = ld16<floatx4>(p.rec_sq[1] + o);
+    const floatx4 q2 = ld16<floatx4>(p.rec_sq[2] + o);
+    const floatx4 q3 = ld16<floatx4>(p.rec_sq[3] + o);
+    const floatx4 ee = ld16<floatx4>(p.rec_e + o);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int u = 4 * blk + e;
+      const bool ok = g4 + e < G;
+      cv[kCPG * u] = ok ? v1[e] : -INFINITY;
+      cv[kCPG * u + 1] = ok ? v2[e] : -INFINITY;
+      cv[kCPG * u + 2] = ok ? v3[e] : -INFINITY;
+      ci[kCPG * u] = ok ? i1[e] : 0x7fffffff;
+      ci[kCPG * u + 1] = ok ? i2[e] : 0x7fffffff;
+      ci[kCPG * u + 2] = ok ? i3[e] : 0x7fffffff;
+      rs[u] = ok ? (q0[e] + q1[e]) + (q2[e] + q3[e]) : 0.f;
+      re[u] = ok ? ee[e] : 0.f;
+      mx = fmaxf(mx, cv[kCPG * u]);
+    }
   }
   if (tid == 0) { s_n = 0; s_nsplit = 0; }
 
@@ -812,7 +844,7 @@ __global__ __launch_bounds__(kMT) void lmhead_merge_kernel(LmParams p) {
   float S = 0.f, E = 0.f;
 #pragma unroll
   for (int u = 0; u < kMaxGPT; ++u) {
-    const int gi = tid + kMT * u;
+    const int gi = 4 * kMT * (u / 4) + 4 * tid + u % 4;
     if (gi < G) {
       const float wgt = fast_exp2((cv[kCPG * u] - Mu) * kLog2e);
       S += rs[u] * wgt;
@@ -830,19 +862,23 @@ __global__ __launch_bounds__(kMT) void lmhead_merge_kernel(LmParams p) {
   const float lse = Mu + fast_log2(S) * kLn2;
 
   // theta: a lower bound of the K-th largest logit.  The K largest lane
-  // maxima of a wave are K distinct logits, so the smallest of them bounds
-  // the K-th largest from below; theta is the best of the waves' bounds.
+  // maxima of a wave are K distinct logits, so the K-th largest of them bounds
+  // the K-th largest logit from below; theta is the best of the waves'
+  // bounds.  Each lane ranks its maximum against the wave's 64 (16-byte
+  // broadcast LDS reads; ties by lane), and the lane of rank K - 1 publishes.
+  if (lane == 0) s_theta[wv] = -INFINITY;
+  s_tm[tid] = mx;
+  __syncthreads();
   {
-    float lm = mx;
-    float th = -INFINITY;
-    for (int k = 0; k < K; ++k) {
-      float bv = lm;
-      int bl = lane;
-      wave_best(bv, bl);
-      if (k == K - 1) th = bv;
-      if (lane == bl) lm = -INFINITY;
+    const float* wm = s_tm + kWave * wv;
+    int r = 0;
+#pragma unroll
+    for (int c = 0; c < kWave; c += 4) {
+      const floatx4 y = *reinterpret_cast<const floatx4*>(wm + c);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) r += (y[e] > mx || (y[e] == mx && c + e < lane)) ? 1 : 0;
     }
-    if (lane == 0) s_theta[wv] = th;
+    if (r == K - 1) s_theta[wv] = mx;
   }
   __syncthreads();
   float theta = s_theta[0];
@@ -880,8 +916,8 @@ __global__ __launch_bounds__(kMT) void lmhead_merge_kernel(LmParams p) {
         const int fi[2] = {xi0, xi1};
         wave_topk(fv, fi, s_cv, s_ci, 0, K, s_top_v, s_top_i);
       }
-    } else if (wv == 0 && n_list <= 2 * kWave) {
-      wave_topk_regs(s_lv, s_li, n_list, K, s_top_v, s_top_i);
+    } else if (n_list <= kMT) {
+      block_topk_rank(s_lv, s_li, n_list, K, s_top_v, s_top_i);
     } else if (wv == 0) {
       const float none[1] = {-INFINITY};
       const int nonei[1] = {0x7fffffff};
@@ -951,7 +987,7 @@ __global__ __launch_bounds__(kMT) void lmhead_merge_kernel(LmParams p) {
       overflow = true;
 #pragma unroll
       for (int u = 0; u < kMaxGPT; ++u) {
-        const int gi = tid + kMT * u;
+        const int gi = 4 * kMT * (u / 4) + 4 * tid + u % 4;
         bool sp = false;
         for (int t = 0; t < nsplit; ++t) sp |= (s_split[t] == gi);
         if (sp) {
@@ -1053,18 +1089,29 @@ __global__ __launch_bounds__(kMT) void sample_kernel(LmParams p, SampleParams s)
     }
   }
   const int G = p.n_groups;
-  const size_t base = (size_t)m * G;
-  // Thread t holds the records of groups [t per, (t+1) per) in registers; the
-  // hidden row is staged in LDS meanwhile (for the recompute below).
-  const int per = (G + kMT - 1) / kMT;          // <= kMaxGPT (V <= kMT kMaxGPT kGroup)
+  const size_t base = (size_t)m * p.rec_stride;
+  // Thread t holds the records of groups [t per, (t+1) per) in registers, per
+  // a multiple of 4 (16-byte loads); the hidden row is staged in LDS
+  // meanwhile (for the recompute below).
+  const int per = ((G + kMT - 1) / kMT + 3) / 4 * 4;   // <= kMaxGPT (V <= kMT kMaxGPT kGroup)
   const int g0 = tid * per;
   float v1r[kMaxGPT], wr[kMaxGPT];
 #pragma unroll
-  for (int i = 0; i < kMaxGPT; ++i) {
-    const bool ok = i < per && g0 + i < G;
-    v1r[i] = ok ? p.rec_v1[base + g0 + i] : -INFINITY;
-    wr[i] = ok ? (p.rec_sq[0][base + g0 + i] + p.rec_sq[1][base + g0 + i]) +
-                     (p.rec_sq[2][base + g0 + i] + p.rec_sq[3][base + g0 + i]) : 0.f;
+  for (int blk = 0; blk < kMaxGPT / 4; ++blk) {
+    const int g4 = g0 + 4 * blk;
+    const bool ok4 = 4 * blk < per && g4 < G;
+    const size_t o = base + (ok4 ? g4 : 0);   // unconditional loads, masked below
+    const floatx4 v1 = ld16<floatx4>(p.rec_v1 + o);
+    const floatx4 q0 = ld16<floatx4>(p.rec_sq[0] + o);
+    const floatx4 q1 = ld16<floatx4>(p.rec_sq[1] + o);
+    const floatx4 q2 = ld16<floatx4>(p.rec_sq[2] + o);
+    const floatx4 q3 = ld16<floatx4>(p.rec_sq[3] + o);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const bool ok = ok4 && g4 + e < G;
+      v1r[4 * blk + e] = ok ? v1[e] : -INFINITY;
+      wr[4 * blk + e] = ok ? (q0[e] + q1[e]) + (q2[e] + q3[e]) : 0.f;
+    }
   }
   {
     const DT* hr = reinterpret_cast<const DT*>(p.hidden) + (size_t)m * p.Hd;
@@ -1261,7 +1308,8 @@ LmPlan lm_plan(int M, int Hd, int V, int K, bool bf16) {
   pl.rb = rows <= 64 ? 1 : rows <= 128 ? 2 : rows <= 192 ? 3 : 4;
   if (!bf16) pl.rb = 1;
   pl.n_rt = (M + 64 * pl.rb - 1) / (64 * pl.rb);
-  const size_t recs = (size_t)M * pl.n_groups;
+  pl.rec_stride = (pl.n_groups + 3) / 4 * 4;
+  const size_t recs = (size_t)M * pl.rec_stride;
   pl.rec_bytes = recs * sizeof(float);
   pl.hid_off = 12 * ((pl.rec_bytes + 255) / 256 * 256);
   pl.workspace_bytes = pl.hid_off + (bf16 ? (size_t)((M + 15) / 16) * 16 * Hd * 2 : 0) + 256;
@@ -1284,6 +1332,7 @@ LmParams lm_params(const void* hidden, const void* W, int M, int Hd, int V, int 
   p.V = V;
   p.K = K;
   p.n_groups = pl.n_groups;
+  p.rec_stride = pl.rec_stride;
   p.n_rt = pl.n_rt;
   p.n_vt = pl.n_vt;
   p.vt_base = 0;
