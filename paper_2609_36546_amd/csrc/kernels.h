@@ -40,6 +40,8 @@ struct AttnPlan {
   int chunk;           // keys per workgroup
   int max_chunks;      // chunk slots per group (padded to a multiple of 8)
   int sk;              // full 64-row groups of 16-slot D = 128 pages: persistent stream-K kernel (bf16)
+  int sk_qt;           // stream-K: 16-row tiles per wave (1: 64-row items, 2: 128-row items)
+  int sk_n_qg;         // stream-K: items per (sequence, KV head)
   size_t part_o_bytes, part_lse_bytes, workspace_bytes;
   size_t sk_o_bytes, sk_lse_bytes;   // stream-K partial layout (when sk)
 };

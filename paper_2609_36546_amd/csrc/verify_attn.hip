@@ -69,8 +69,8 @@ struct AttnParams {
   const int32_t* cu_q;
   const int32_t* seq_ids;
   void* out;
-  float* part_o;      // [slots][kRows][D]
-  float* part_lse;    // [slots][kRows]
+  float* part_o;      // [slots][kRows][D] (stream-K: [slots][item_rows][D])
+  float* part_lse;    // [slots][kRows] (stream-K: [slots][item_rows])
   int max_pages;
   int Hq, Hkv, G;
   int page_size, log2ps, num_pages;
@@ -79,6 +79,7 @@ struct AttnParams {
   float scale_log2;   // softmax scale * log2(e)
   int32_t* sk_start;  // stream-K: first block of every item (written by the attention kernel)
   int sk_grid;        // stream-K: persistent workgroups
+  int item_rows;      // stream-K: packed query rows per item (64, or 128 with two tiles per wave)
 };
 
 template <typename DT, int D> struct Frags;
@@ -194,6 +195,12 @@ template <int D> struct RegQ {
   bf16x8 q[D / 32];
   __device__ __forceinline__ bf16x8 get(int, int ks) const { return q[ks]; }
 };
+// QT tiles' fragments in registers.
+template <int D, int QT> struct RegQT {
+  bf16x8 q[QT][D / 32];
+  __device__ __forceinline__ bf16x8 get(int t, int ks) const { return q[t][ks]; }
+};
+
 
 template <typename DT, int D, int QT, bool TAIL, class QS, class FS>
 __device__ __forceinline__ void attend_block(const AttnParams& a, const FS& f,
@@ -263,24 +270,39 @@ __device__ __forceinline__ void attend_block(const AttnParams& a, const FS& f,
       for (int dt = 0; dt < D / 16; ++dt) acc[t][dt] *= alpha;
     }
   }
+  if constexpr (sizeof(DT) == 2) {
+    // Probabilities of every tile first, then one pass over the value
+    // fragments: each fragment read from LDS feeds all QT tiles.
+    bf16x8 pf[QT];
 #pragma unroll
-  for (int t = 0; t < QT; ++t) {
-    float p[8];
-    float ps = 0.f;
+    for (int t = 0; t < QT; ++t) {
+      float ps = 0.f;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      p[e] = fast_exp2(fmaf(s[t][e >> 2][e & 3], c, -m_use[t]));
-      ps += p[e];
+      for (int e = 0; e < 8; ++e) {
+        const float p = fast_exp2(fmaf(s[t][e >> 2][e & 3], c, -m_use[t]));
+        ps += p;
+        pf[t][e] = static_cast<bf16>(p);
+      }
+      l_run[t] += ps;
     }
-    l_run[t] += ps;
-    if constexpr (sizeof(DT) == 2) {
-      bf16x8 pf;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) pf[e] = static_cast<bf16>(p[e]);
+    for (int dt = 0; dt < D / 16; ++dt) {
+      const bf16x8 v = f.vf(dt);
 #pragma unroll
-      for (int dt = 0; dt < D / 16; ++dt)
-        acc[t][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f.vf(dt), pf, acc[t][dt], 0, 0, 0);
-    } else {
+      for (int t = 0; t < QT; ++t)
+        acc[t][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(v, pf[t], acc[t][dt], 0, 0, 0);
+    }
+  } else {
+#pragma unroll
+    for (int t = 0; t < QT; ++t) {
+      float p[8];
+      float ps = 0.f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        p[e] = fast_exp2(fmaf(s[t][e >> 2][e & 3], c, -m_use[t]));
+        ps += p[e];
+      }
+      l_run[t] += ps;
 #pragma unroll
       for (int dt = 0; dt < D / 16; ++dt)
 #pragma unroll
@@ -593,16 +615,19 @@ __device__ __forceinline__ SkItem sk_item(const AttnParams& a, const int* s_seq,
   m.L = s_seq[4 * m.slot + 1];
   m.r0 = s_seq[4 * m.slot + 2];
   const int rows_total = s_seq[4 * m.slot + 3] * a.G;
-  m.pr0 = qg * kRows;
-  m.pr_last = min(rows_total, m.pr0 + kRows) - 1;
+  m.pr0 = qg * a.item_rows;
+  m.pr_last = min(rows_total, m.pr0 + a.item_rows) - 1;
   m.n_keys = m.L + m.pr_last / a.G + 1;
   m.nb = m.pr0 < rows_total ? min((m.n_keys + kBlk - 1) / kBlk, maxblk) : 0;
   return m;
 }
 
+template <int QT>
 __global__ __launch_bounds__(256, 2) void verify_attn_sk_kernel(AttnParams a) {
+  static_assert(QT == 1 || QT == 2, "tiles per wave");
   constexpr int D = 128;
   constexpr int PS = 16;
+  constexpr int kRowsI = 64 * QT;      // rows per item: QT query units of 64 rows
   const int tid = threadIdx.x;
   const int t = tid / kWave;           // row tile
   const int lane = lane_id();
@@ -688,19 +713,21 @@ __global__ __launch_bounds__(256, 2) void verify_attn_sk_kernel(AttnParams a) {
     return l0;
   };
   const int i_first = uni(item_of(lo)), i_last = uni(item_of(hi - 1));
-  const int n_units = (hi - lo) + s_ne[i_last + 1] - s_ne[i_first];
+  const int n_units = (hi - lo) + QT * (s_ne[i_last + 1] - s_ne[i_first]);
   if (2 * (n_it + 1) + 4 * a.n_seq + 2 * (hi - lo) + n_units > kSkMeta) return;
   int* s_uq = s_pg + 2 * (hi - lo);          // [n_units] the workgroup's units, in order
-  // Unit records: a query unit holds 4 item + 1; a key/value unit holds
-  // 4 x + 2 (last block of the item's piece) with x the block's offset in the
-  // share.  Block x of item i is unit (x - lo) + (non-empty items from
-  // i_first through i); the unit before an item's first block is its query.
+  // Unit records: query unit h (rows 64 h .. 64 h + 63 of the item) holds
+  // 4 item + 2 h + 1; a key/value unit holds 4 x + 2 (last block of the
+  // item's piece) with x the block's offset in the share.  Block x of item i is
+  // unit (x - lo) + QT (non-empty items from i_first through i); the QT units
+  // before an item's first block are its queries.
   for (int x = lo + tid; x < hi; x += 256) {
     const int i = item_of(x);
-    const int u = (x - lo) + s_ne[i + 1] - s_ne[i_first];
+    const int u = (x - lo) + QT * (s_ne[i + 1] - s_ne[i_first]);
     const int last = (x + 1 == s_start[i + 1] || x + 1 == hi) ? 2 : 0;
     s_uq[u] = 4 * (x - lo) + last;
-    if (x == max(lo, s_start[i])) s_uq[u - 1] = 4 * i + 1;
+    if (x == max(lo, s_start[i]))
+      for (int h = 0; h < QT; ++h) s_uq[u - QT + h] = 4 * i + 2 * h + 1;
     const SkItem m = sk_item(a, s_seq, i, maxblk);
     const int* pt_row = a.page_table + (size_t)m.b * a.max_pages;
     const int pl = 2 * (x - s_start[i]);
@@ -728,11 +755,12 @@ __global__ __launch_bounds__(256, 2) void verify_attn_sk_kernel(AttnParams a) {
     char* buf = s_ring + (m % kSkBuf) * kSkUnit;
     if (d_rec & 1) {
       const SkItem it = sk_item(a, s_seq, d_rec >> 2, maxblk);
+      const int h0 = 64 * ((d_rec >> 1) & 1);
       d_g = it.g;
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         const int r = 16 * t + 4 * u + (lane >> 4);
-        const int pr = min(it.pr0 + r, it.pr_last);
+        const int pr = min(it.pr0 + h0 + r, it.pr_last);
         const bf16* row = qp + ((size_t)(it.r0 + pr / a.G) * a.Hq + it.g * a.G + pr % a.G) * D;
         dma16(row + 8 * ((lane & 15) ^ (r & 7)), buf + 1024 * (4 * t + u));
       }
@@ -764,17 +792,18 @@ __global__ __launch_bounds__(256, 2) void verify_attn_sk_kernel(AttnParams a) {
 
   for (int m = 0; m < kSkBuf - 1; ++m) dma_unit(m);
 
-  // Compute side: the current item's data, set at its query unit.
+  // Compute side: the current item's data, set at its query units.  Tile tt
+  // of this wave holds the item's rows 64 tt + 16 t .. 64 tt + 16 t + 15.
   SkItem it{};
   int c_item = 0;
   int x0 = 0;          // offset in the share of the item's block 0 (may be negative)
   bool full = false;   // the whole item lies in this share
-  RegQ<D> qf;
-  int qlimit[1] = {0};
-  int prq = 0;
-  bool has_rows = false;
-  floatx4 acc[1][D / 16];
-  float m_run[1], l_run[1];
+  RegQT<D, QT> qf;
+  int qlimit[QT] = {};
+  int prq[QT] = {};
+  bool has_rows[QT] = {};
+  floatx4 acc[QT][D / 16];
+  float m_run[QT], l_run[QT];
   int c_rec = uni(s_uq[0]);
   for (int n = 0; n < n_units; ++n) {
     // Unit n of this wave's loads has landed (the next one may still be in
@@ -789,64 +818,84 @@ __global__ __launch_bounds__(256, 2) void verify_attn_sk_kernel(AttnParams a) {
     const char* buf = s_ring + (n % kSkBuf) * kSkUnit;
     if (rec & 1) {
       const int i = rec >> 2;
-      c_item = i;
-      it = sk_item(a, s_seq, i, maxblk);
-      it.g = uni(it.g);
-      it.L = uni(it.L);
-      it.r0 = uni(it.r0);
-      it.pr0 = uni(it.pr0);
-      it.pr_last = uni(it.pr_last);
-      it.n_keys = uni(it.n_keys);
-      x0 = uni(s_start[i] - lo);
-      full = uni(s_start[i] >= lo && s_start[i + 1] <= hi);
-      prq = it.pr0 + 16 * t + c16;
-      qlimit[0] = it.L + min(prq, it.pr_last) / a.G + 1;
-      has_rows = it.pr0 + 16 * t <= it.pr_last;
-      const int r = 16 * t + c16;
+      const int h = (rec >> 1) & 1;
+      if (h == 0) {
+        c_item = i;
+        it = sk_item(a, s_seq, i, maxblk);
+        it.g = uni(it.g);
+        it.L = uni(it.L);
+        it.r0 = uni(it.r0);
+        it.pr0 = uni(it.pr0);
+        it.pr_last = uni(it.pr_last);
+        it.n_keys = uni(it.n_keys);
+        x0 = uni(s_start[i] - lo);
+        full = uni(s_start[i] >= lo && s_start[i + 1] <= hi);
 #pragma unroll
-      for (int ks = 0; ks < D / 32; ++ks) {
-        qf.q[ks] = *reinterpret_cast<const bf16x8*>(buf + 256 * r + 16 * ((j + 4 * ks) ^ (r & 7)));
-        if (prq > it.pr_last) qf.q[ks] = bf16x8{};
+        for (int tt = 0; tt < QT; ++tt) {
+          m_run[tt] = -INFINITY;
+          l_run[tt] = 0.f;
+#pragma unroll
+          for (int dt = 0; dt < D / 16; ++dt) acc[tt][dt] = floatx4{0.f, 0.f, 0.f, 0.f};
+        }
       }
-      m_run[0] = -INFINITY;
-      l_run[0] = 0.f;
 #pragma unroll
-      for (int dt = 0; dt < D / 16; ++dt) acc[0][dt] = floatx4{0.f, 0.f, 0.f, 0.f};
+      for (int tt = 0; tt < QT; ++tt) {
+        if (tt != h) continue;
+        prq[tt] = it.pr0 + 64 * tt + 16 * t + c16;
+        qlimit[tt] = it.L + min(prq[tt], it.pr_last) / a.G + 1;
+        has_rows[tt] = it.pr0 + 64 * tt + 16 * t <= it.pr_last;
+        const int r = 16 * t + c16;
+#pragma unroll
+        for (int ks = 0; ks < D / 32; ++ks) {
+          qf.q[tt][ks] = *reinterpret_cast<const bf16x8*>(buf + 256 * r + 16 * ((j + 4 * ks) ^ (r & 7)));
+          if (prq[tt] > it.pr_last) qf.q[tt][ks] = bf16x8{};
+        }
+      }
       continue;
     }
-    if (!has_rows) continue;
-    const int t0 = kBlk * ((rec >> 2) - x0);
-    const int main_end = min(it.n_keys, it.L & ~(kBlk - 1));
-    if (t0 + kBlk <= main_end) {
-      const LdsFrags<false> f{buf, k_off[0], k_off[1], v_off0, 0, 0};
-      attend_block<bf16, D, 1, false>(a, f, qf, qlimit, t0, acc, m_run, l_run);
-    } else {
-      const LdsFrags<true> f{buf, k_off[0], k_off[1], v_off0, t0 + 8 * j, it.n_keys};
-      attend_block<bf16, D, 1, true>(a, f, qf, qlimit, t0, acc, m_run, l_run);
+    if (has_rows[0]) {
+      const int t0 = kBlk * ((rec >> 2) - x0);
+      const int main_end = min(it.n_keys, it.L & ~(kBlk - 1));
+      const bool tail = t0 + kBlk > main_end;
+      // All QT tiles run, also where the last has no rows (its query
+      // fragments are zero and its results are never written).
+      if (!tail) {
+        const LdsFrags<false> f{buf, k_off[0], k_off[1], v_off0, 0, 0};
+        attend_block<bf16, D, QT, false>(a, f, qf, qlimit, t0, acc, m_run, l_run);
+      } else {
+        const LdsFrags<true> f{buf, k_off[0], k_off[1], v_off0, t0 + 8 * j, it.n_keys};
+        attend_block<bf16, D, QT, true>(a, f, qf, qlimit, t0, acc, m_run, l_run);
+      }
     }
     if (!(rec & 2)) continue;
     // The item's piece ends here.  A whole item is written out; a piece
     // leaves a partial at slot item + workgroup.
-    float l_tot = l_run[0] + __shfl_xor(l_run[0], 16, kWave);
-    l_tot += __shfl_xor(l_tot, 32, kWave);
-    const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-    if (prq <= it.pr_last && full) {
-      const int i = prq / a.G, hl = prq % a.G;
-      bf16* orow = reinterpret_cast<bf16*>(a.out) + ((size_t)(it.r0 + i) * a.Hq + it.g * a.G + hl) * D;
 #pragma unroll
-      for (int dt = 0; dt < D / 16; ++dt) {
-        bf16x4 v;
+    for (int tt = 0; tt < QT; ++tt) {
+      float l_tot = l_run[tt] + __shfl_xor(l_run[tt], 16, kWave);
+      l_tot += __shfl_xor(l_tot, 32, kWave);
+      const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+      if (!has_rows[tt] || prq[tt] > it.pr_last) continue;
+      if (full) {
+        const int i = prq[tt] / a.G, hl = prq[tt] % a.G;
+        bf16* orow = reinterpret_cast<bf16*>(a.out) + ((size_t)(it.r0 + i) * a.Hq + it.g * a.G + hl) * D;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) v[e] = static_cast<bf16>(acc[0][dt][e] * inv);
-        *reinterpret_cast<bf16x4*>(orow + 16 * dt + 4 * j) = v;
+        for (int dt = 0; dt < D / 16; ++dt) {
+          bf16x4 v;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] = static_cast<bf16>(acc[tt][dt][e] * inv);
+          *reinterpret_cast<bf16x4*>(orow + 16 * dt + 4 * j) = v;
+        }
+      } else {
+        const size_t ps = (size_t)c_item + w;
+        const int row = 64 * tt + 16 * t + c16;
+        float* po = a.part_o + (ps * kRowsI + row) * D;
+#pragma unroll
+        for (int dt = 0; dt < D / 16; ++dt)
+          *reinterpret_cast<floatx4*>(po + 16 * dt + 4 * j) = acc[tt][dt] * inv;
+        if (j == 0)
+          a.part_lse[ps * kRowsI + row] = l_tot > 0.f ? m_run[tt] + fast_log2(l_tot) : -INFINITY;
       }
-    } else if (prq <= it.pr_last) {
-      const size_t ps = (size_t)c_item + w;
-      float* po = a.part_o + (ps * kRows + (16 * t + c16)) * D;
-#pragma unroll
-      for (int dt = 0; dt < D / 16; ++dt) *reinterpret_cast<floatx4*>(po + 16 * dt + 4 * j) = acc[0][dt] * inv;
-      if (j == 0)
-        a.part_lse[ps * kRows + 16 * t + c16] = l_tot > 0.f ? m_run[0] + fast_log2(l_tot) : -INFINITY;
     }
   }
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // reloads past the end
@@ -856,10 +905,11 @@ __global__ __launch_bounds__(256, 2) void verify_attn_sk_kernel(AttnParams a) {
 // workgroups: piece w of item it sits at slot it + w, for the workgroups w
 // whose share of blocks meets the item.
 __global__ __launch_bounds__(256) void attn_combine_sk_kernel(AttnParams a) {
-  // Grid x = 4 row quarters per row group: 16 packed rows per workgroup,
+  // Grid x = item_rows / 16 parts per item: 16 packed rows per workgroup,
   // 16 threads per row, 8 channels per thread.
   constexpr int D = 128;
-  const int qg = blockIdx.x / 4, rq = blockIdx.x % 4;
+  const int R = a.item_rows;
+  const int qg = blockIdx.x / (R / 16), rq = blockIdx.x % (R / 16);
   const int slot = blockIdx.y / a.Hkv, g = blockIdx.y % a.Hkv;
   const int it = (slot * a.Hkv + g) * a.n_qg + qg;
   const int n_it = a.n_seq * a.Hkv * a.n_qg;
@@ -877,17 +927,17 @@ __global__ __launch_bounds__(256) void attn_combine_sk_kernel(AttnParams a) {
   const int G = a.G;
   const int r = 16 * rq + threadIdx.x / 16;           // packed row within the group
   const int dq = (threadIdx.x % 16) * (D / 16);
-  const int pr = qg * kRows + r;
-  if (pr >= min(kb * G, (qg + 1) * kRows)) return;
+  const int pr = qg * R + r;
+  if (pr >= min(kb * G, (qg + 1) * R)) return;
   float M = -INFINITY;
-  for (int w = w0; w <= w1; ++w) M = fmaxf(M, a.part_lse[((size_t)it + w) * kRows + r]);
+  for (int w = w0; w <= w1; ++w) M = fmaxf(M, a.part_lse[((size_t)it + w) * R + r]);
   const float Mu = (M == -INFINITY) ? 0.f : M;
   floatx4 o0 = {0.f, 0.f, 0.f, 0.f}, o1 = {0.f, 0.f, 0.f, 0.f};
   float wsum = 0.f;
   for (int w = w0; w <= w1; ++w) {
-    const float wgt = fast_exp2(a.part_lse[((size_t)it + w) * kRows + r] - Mu);
+    const float wgt = fast_exp2(a.part_lse[((size_t)it + w) * R + r] - Mu);
     wsum += wgt;
-    const float* po = a.part_o + (((size_t)it + w) * kRows + r) * D + dq;
+    const float* po = a.part_o + (((size_t)it + w) * R + r) * D + dq;
     o0 += wgt * ld16<floatx4>(po);
     o1 += wgt * ld16<floatx4>(po + 4);
   }
@@ -974,11 +1024,14 @@ hipError_t launch_sk(const AttnParams& p, dim3 cgrid, hipStream_t st) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   trace_mark(st);
-  hipLaunchKernelGGL(verify_attn_sk_kernel, dim3(p.sk_grid), dim3(256), 0, st, p);
+  if (p.item_rows == 128)
+    hipLaunchKernelGGL(verify_attn_sk_kernel<2>, dim3(p.sk_grid), dim3(256), 0, st, p);
+  else
+    hipLaunchKernelGGL(verify_attn_sk_kernel<1>, dim3(p.sk_grid), dim3(256), 0, st, p);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   trace_mark(st);
-  hipLaunchKernelGGL(attn_combine_sk_kernel, dim3(4 * cgrid.x, cgrid.y), dim3(256), 0, st, p);
+  hipLaunchKernelGGL(attn_combine_sk_kernel, dim3(cgrid.x * (p.item_rows / 16), cgrid.y), dim3(256), 0, st, p);
   e = hipGetLastError();
   trace_mark(st);
   return e;
@@ -1027,16 +1080,21 @@ AttnPlan attn_plan(int n_seq, int Hq, int Hkv, int D, int max_q, int max_pages, 
   // kernel (bf16; the launch checks the type) when its LDS tables fit: item
   // starts and non-empty counts, sequence data, and per workgroup two page
   // ids per block and one record per unit (a share is at most every item at
-  // its largest block count over the grid; its units add one per item).
-  const long n_it = (long)n_seq * Hkv * pl.n_qg;
+  // its largest block count over the grid; its units add sk_qt per item).
+  // More than 64 rows per (sequence, KV head) take 128-row items, two 16-row
+  // tiles per wave, so that each key is read once per 128 rows.
+  pl.sk_qt = rows > kRows ? 2 : 1;
+  pl.sk_n_qg = (int)((rows + 64L * pl.sk_qt - 1) / (64L * pl.sk_qt));
+  const long n_it = (long)n_seq * Hkv * pl.sk_n_qg;
   const long maxblk = (max_keys + kBlk - 1) / kBlk;
   const long share = (n_it * maxblk + kSkGrid - 1) / kSkGrid;
   pl.sk = D == 128 && page_size == 16 && pl.qt == 4 &&
-          2 * (n_it + 1) + 4L * n_seq + 3 * share + n_it <= kSkMeta;
+          2 * (n_it + 1) + 4L * n_seq + 3 * share + pl.sk_qt * n_it <= kSkMeta;
   if (pl.sk) {
     const size_t sk_slots = (size_t)n_it + kSkGrid;
-    pl.sk_o_bytes = std::max(pl.part_o_bytes, sk_slots * kRows * D * sizeof(float));
-    pl.sk_lse_bytes = std::max(pl.part_lse_bytes, sk_slots * kRows * sizeof(float));
+    const size_t sk_rows = 64 * (size_t)pl.sk_qt;
+    pl.sk_o_bytes = std::max(pl.part_o_bytes, sk_slots * sk_rows * D * sizeof(float));
+    pl.sk_lse_bytes = std::max(pl.part_lse_bytes, sk_slots * sk_rows * sizeof(float));
     pl.workspace_bytes = pl.sk_o_bytes + pl.sk_lse_bytes + (n_it + 1) * sizeof(int32_t) + 256;
   }
   return pl;
@@ -1119,7 +1177,9 @@ hipError_t launch_verify_attn(const AttnLaunch& L, const AttnPlan& pl, hipStream
     p.part_lse = reinterpret_cast<float*>(reinterpret_cast<char*>(L.workspace) + pl.sk_o_bytes);
     p.sk_start = reinterpret_cast<int32_t*>(reinterpret_cast<char*>(L.workspace) + pl.sk_o_bytes + pl.sk_lse_bytes);
     p.sk_grid = kSkGrid;
-    return launch_sk(p, cgrid, st);
+    p.n_qg = pl.sk_n_qg;
+    p.item_rows = 64 * pl.sk_qt;
+    return launch_sk(p, dim3(pl.sk_n_qg, L.n_seq * L.Hkv), st);
   }
   if (L.dtype_bf16) {
     return L.D == 64 ? launch_d<bf16, 64>(p, pl.qt, grid, cgrid, st)
