@@ -629,7 +629,7 @@ __global__ __launch_bounds__(256, 2) void verify_attn_sk_kernel(AttnParams a) {
   constexpr int PS = 16;
   constexpr int kRowsI = 64 * QT;      // rows per item: QT query units of 64 rows
   const int tid = threadIdx.x;
-  const int t = tid / kWave;           // row tile
+  const int t = uni(tid / kWave);      // row tile (wave-uniform)
   const int lane = lane_id();
   const int c16 = lane & 15, j = lane >> 4;
   const int n_it = a.n_seq * a.Hkv * a.n_qg;
@@ -792,82 +792,88 @@ __global__ __launch_bounds__(256, 2) void verify_attn_sk_kernel(AttnParams a) {
 
   for (int m = 0; m < kSkBuf - 1; ++m) dma_unit(m);
 
-  // Compute side: the current item's data, set at its query units.  Tile tt
-  // of this wave holds the item's rows 64 tt + 16 t .. 64 tt + 16 t + 15.
-  SkItem it{};
-  int c_item = 0;
-  int x0 = 0;          // offset in the share of the item's block 0 (may be negative)
-  bool full = false;   // the whole item lies in this share
-  RegQT<D, QT> qf;
-  int qlimit[QT] = {};
-  int prq[QT] = {};
-  bool has_rows[QT] = {};
-  floatx4 acc[QT][D / 16];
-  float m_run[QT], l_run[QT];
+  // Compute side.  The units come as items: QT query units, then the item's
+  // key/value units up to the one that ends its piece.  Tile tt of this wave
+  // holds the item's rows 64 tt + 16 t .. 64 tt + 16 t + 15.
   int c_rec = uni(s_uq[0]);
-  for (int n = 0; n < n_units; ++n) {
-    // Unit n of this wave's loads has landed (the next one may still be in
-    // flight); after the barrier every wave's pieces of it are visible, and
-    // every wave is done with unit n - 1, whose buffer the next issue refills.
+  int n = 0;
+  // Unit n of this wave's loads has landed (the next one may still be in
+  // flight); after the barrier every wave's pieces of it are visible, and
+  // every wave is done with unit n - 1, whose buffer the next issue refills.
+  auto next_unit = [&](int& rec) -> const char* {
     asm volatile("s_waitcnt vmcnt(%0)" ::"n"(4 * (kSkBuf - 2)) : "memory");
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
     dma_unit(n + kSkBuf - 1);
-    const int rec = c_rec;
+    rec = c_rec;
     c_rec = uni(s_uq[min(n + 1, n_units - 1)]);
     const char* buf = s_ring + (n % kSkBuf) * kSkUnit;
-    if (rec & 1) {
-      const int i = rec >> 2;
-      const int h = (rec >> 1) & 1;
-      if (h == 0) {
-        c_item = i;
-        it = sk_item(a, s_seq, i, maxblk);
-        it.g = uni(it.g);
-        it.L = uni(it.L);
-        it.r0 = uni(it.r0);
-        it.pr0 = uni(it.pr0);
-        it.pr_last = uni(it.pr_last);
-        it.n_keys = uni(it.n_keys);
-        x0 = uni(s_start[i] - lo);
-        full = uni(s_start[i] >= lo && s_start[i + 1] <= hi);
+    ++n;
+    return buf;
+  };
+  while (n < n_units) {
+    int rec;
+    const int i = uni(c_rec >> 2);
+    SkItem it = sk_item(a, s_seq, i, maxblk);
+    it.g = uni(it.g);
+    it.L = uni(it.L);
+    it.r0 = uni(it.r0);
+    it.pr0 = uni(it.pr0);
+    it.pr_last = uni(it.pr_last);
+    it.n_keys = uni(it.n_keys);
+    const int x0 = uni(s_start[i] - lo);   // offset in the share of the item's block 0 (may be negative)
+    const bool full = uni(s_start[i] >= lo && s_start[i + 1] <= hi);   // the whole item lies in this share
+    RegQT<D, QT> qf;
+    int qlimit[QT], prq[QT];
+    bool has_rows[QT];
 #pragma unroll
-        for (int tt = 0; tt < QT; ++tt) {
-          m_run[tt] = -INFINITY;
-          l_run[tt] = 0.f;
+    for (int tt = 0; tt < QT; ++tt) {
+      const char* buf = next_unit(rec);
+      prq[tt] = it.pr0 + 64 * tt + 16 * t + c16;
+      qlimit[tt] = it.L + min(prq[tt], it.pr_last) / a.G + 1;
+      has_rows[tt] = uni(it.pr0 + 64 * tt + 16 * t <= it.pr_last);
+      const int r = 16 * t + c16;
 #pragma unroll
-          for (int dt = 0; dt < D / 16; ++dt) acc[tt][dt] = floatx4{0.f, 0.f, 0.f, 0.f};
-        }
+      for (int ks = 0; ks < D / 32; ++ks) {
+        qf.q[tt][ks] = *reinterpret_cast<const bf16x8*>(buf + 256 * r + 16 * ((j + 4 * ks) ^ (r & 7)));
+        if (prq[tt] > it.pr_last) qf.q[tt][ks] = bf16x8{};
       }
-#pragma unroll
-      for (int tt = 0; tt < QT; ++tt) {
-        if (tt != h) continue;
-        prq[tt] = it.pr0 + 64 * tt + 16 * t + c16;
-        qlimit[tt] = it.L + min(prq[tt], it.pr_last) / a.G + 1;
-        has_rows[tt] = it.pr0 + 64 * tt + 16 * t <= it.pr_last;
-        const int r = 16 * t + c16;
-#pragma unroll
-        for (int ks = 0; ks < D / 32; ++ks) {
-          qf.q[tt][ks] = *reinterpret_cast<const bf16x8*>(buf + 256 * r + 16 * ((j + 4 * ks) ^ (r & 7)));
-          if (prq[tt] > it.pr_last) qf.q[tt][ks] = bf16x8{};
-        }
-      }
-      continue;
     }
-    if (has_rows[0]) {
-      const int t0 = kBlk * ((rec >> 2) - x0);
-      const int main_end = min(it.n_keys, it.L & ~(kBlk - 1));
-      const bool tail = t0 + kBlk > main_end;
-      // All QT tiles run, also where the last has no rows (its query
-      // fragments are zero and its results are never written).
-      if (!tail) {
+    floatx4 acc[QT][D / 16];
+    float m_run[QT], l_run[QT];
+#pragma unroll
+    for (int tt = 0; tt < QT; ++tt) {
+      m_run[tt] = -INFINITY;
+      l_run[tt] = 0.f;
+#pragma unroll
+      for (int dt = 0; dt < D / 16; ++dt) acc[tt][dt] = floatx4{0.f, 0.f, 0.f, 0.f};
+    }
+    // Blocks that end at or before main_end hold no key past any row's
+    // limit and no stand-in key: they take the unmasked block, in a loop of
+    // their own; the item's last blocks (the window's) follow, masked.  All
+    // QT tiles run, also where the last has no rows (its query fragments are
+    // zero and its results are never written).
+    const int main_end = min(it.n_keys, it.L & ~(kBlk - 1));
+    bool ended = false;
+    while (n < n_units) {
+      const int t0 = kBlk * ((c_rec >> 2) - x0);   // the next unit: a key/value unit of this item
+      if (t0 + kBlk > main_end) break;
+      const char* buf = next_unit(rec);
+      if (has_rows[0]) {
         const LdsFrags<false> f{buf, k_off[0], k_off[1], v_off0, 0, 0};
         attend_block<bf16, D, QT, false>(a, f, qf, qlimit, t0, acc, m_run, l_run);
-      } else {
+      }
+      if (rec & 2) { ended = true; break; }
+    }
+    while (!ended && n < n_units) {
+      const char* buf = next_unit(rec);
+      const int t0 = kBlk * ((rec >> 2) - x0);
+      if (has_rows[0]) {
         const LdsFrags<true> f{buf, k_off[0], k_off[1], v_off0, t0 + 8 * j, it.n_keys};
         attend_block<bf16, D, QT, true>(a, f, qf, qlimit, t0, acc, m_run, l_run);
       }
+      ended = rec & 2;
     }
-    if (!(rec & 2)) continue;
     // The item's piece ends here.  A whole item is written out; a piece
     // leaves a partial at slot item + workgroup.
 #pragma unroll
@@ -877,8 +883,8 @@ __global__ __launch_bounds__(256, 2) void verify_attn_sk_kernel(AttnParams a) {
       const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
       if (!has_rows[tt] || prq[tt] > it.pr_last) continue;
       if (full) {
-        const int i = prq[tt] / a.G, hl = prq[tt] % a.G;
-        bf16* orow = reinterpret_cast<bf16*>(a.out) + ((size_t)(it.r0 + i) * a.Hq + it.g * a.G + hl) * D;
+        const int ri = prq[tt] / a.G, hl = prq[tt] % a.G;
+        bf16* orow = reinterpret_cast<bf16*>(a.out) + ((size_t)(it.r0 + ri) * a.Hq + it.g * a.G + hl) * D;
 #pragma unroll
         for (int dt = 0; dt < D / 16; ++dt) {
           bf16x4 v;
@@ -887,7 +893,7 @@ __global__ __launch_bounds__(256, 2) void verify_attn_sk_kernel(AttnParams a) {
           *reinterpret_cast<bf16x4*>(orow + 16 * dt + 4 * j) = v;
         }
       } else {
-        const size_t ps = (size_t)c_item + w;
+        const size_t ps = (size_t)i + w;
         const int row = 64 * tt + 16 * t + c16;
         float* po = a.part_o + (ps * kRowsI + row) * D;
 #pragma unroll
