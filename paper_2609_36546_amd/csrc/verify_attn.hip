@@ -1094,7 +1094,7 @@ AttnPlan attn_plan(int n_seq, int Hq, int Hkv, int D, int max_q, int max_pages, 
   const long n_it = (long)n_seq * Hkv * pl.sk_n_qg;
   const long maxblk = (max_keys + kBlk - 1) / kBlk;
   const long share = (n_it * maxblk + kSkGrid - 1) / kSkGrid;
-  pl.sk = D == 128 && page_size == 16 && pl.qt == 4 &&
+  pl.sk = D == 128 && page_size == 16 &&
           2 * (n_it + 1) + 4L * n_seq + 3 * share + pl.sk_qt * n_it <= kSkMeta;
   if (pl.sk) {
     const size_t sk_slots = (size_t)n_it + kSkGrid;
