@@ -716,26 +716,6 @@ __global__ __launch_bounds__(256, 2) void verify_attn_sk_kernel(AttnParams a) {
   const int n_units = (hi - lo) + QT * (s_ne[i_last + 1] - s_ne[i_first]);
   if (2 * (n_it + 1) + 4 * a.n_seq + 2 * (hi - lo) + n_units > kSkMeta) return;
   int* s_uq = s_pg + 2 * (hi - lo);          // [n_units] the workgroup's units, in order
-  // Unit records: query unit h (rows 64 h .. 64 h + 63 of the item) holds
-  // 4 item + 2 h + 1; a key/value unit holds 4 x + 2 (last block of the
-  // item's piece) with x the block's offset in the share.  Block x of item i is
-  // unit (x - lo) + QT (non-empty items from i_first through i); the QT units
-  // before an item's first block are its queries.
-  for (int x = lo + tid; x < hi; x += 256) {
-    const int i = item_of(x);
-    const int u = (x - lo) + QT * (s_ne[i + 1] - s_ne[i_first]);
-    const int last = (x + 1 == s_start[i + 1] || x + 1 == hi) ? 2 : 0;
-    s_uq[u] = 4 * (x - lo) + last;
-    if (x == max(lo, s_start[i]))
-      for (int h = 0; h < QT; ++h) s_uq[u - QT + h] = 4 * i + 2 * h + 1;
-    const SkItem m = sk_item(a, s_seq, i, maxblk);
-    const int* pt_row = a.page_table + (size_t)m.b * a.max_pages;
-    const int pl = 2 * (x - s_start[i]);
-    s_pg[2 * (x - lo)] = clampi(pt_row[min(pl, a.max_pages - 1)], 0, a.num_pages - 1);
-    s_pg[2 * (x - lo) + 1] = clampi(pt_row[min(pl + 1, a.max_pages - 1)], 0, a.num_pages - 1);
-  }
-  __syncthreads();
-
   // Lane-fixed parts of this wave's loads: key slice t and value channels
   // 32t .. 32t+31 of each page; query rows 16t .. 16t+15, four per load.
   const int ksl = lane >> 2;
@@ -750,8 +730,8 @@ __global__ __launch_bounds__(256, 2) void verify_attn_sk_kernel(AttnParams a) {
   // one is loaded again, so that every wait below has the same count.  The
   // next unit's record and page ids are read one issue ahead.
   int d_g = 0;                               // KV head of the load side's current item
-  int d_rec = uni(s_uq[0]), d_pg0 = 0, d_pg1 = 0;
-  auto dma_unit = [&](int m) {
+  int d_rec = 4 * i_first + 1, d_pg0 = 0, d_pg1 = 0;   // unit 0: the first item's first query unit
+  auto dma_issue = [&](int m) {
     char* buf = s_ring + (m % kSkBuf) * kSkUnit;
     if (d_rec & 1) {
       const SkItem it = sk_item(a, s_seq, d_rec >> 2, maxblk);
@@ -772,12 +752,80 @@ __global__ __launch_bounds__(256, 2) void verify_attn_sk_kernel(AttnParams a) {
       dma16(kc + b1 + k_src, buf + 1024 * (4 + t));
       dma16(vc + b1 + v_src, buf + 1024 * (12 + t));
     }
+  };
+  auto dma_next = [&](int m) {
     d_rec = uni(s_uq[min(m + 1, n_units - 1)]);
     if (!(d_rec & 1)) {
       d_pg0 = uni(s_pg[(d_rec >> 2) * 2]);
       d_pg1 = uni(s_pg[(d_rec >> 2) * 2 + 1]);
     }
   };
+  auto dma_unit = [&](int m) {
+    dma_issue(m);
+    dma_next(m);
+  };
+  // The first query unit needs no table: it is issued now, so that its load
+  // overlaps the page-table reads and the window append below.
+  dma_issue(0);
+
+
+  // Window append: the window's keys and values at positions L .. L+k-1 go
+  // to the pages, for the positions inside this share's blocks (every window
+  // position lies in some item's blocks; positions in two shares are written
+  // twice, with the same values).  Each workgroup writes the positions it
+  // reads, and waits for the writes before it loads any key/value unit; the
+  // stores are issued first, so that the page-table reads below overlap them.
+  {
+    bf16* kw = reinterpret_cast<bf16*>(a.k_cache);
+    bf16* vw = reinterpret_cast<bf16*>(a.v_cache);
+    const bf16* kn = reinterpret_cast<const bf16*>(a.k_new);
+    const bf16* vn = reinterpret_cast<const bf16*>(a.v_new);
+    for (int i = i_first; i <= i_last; ++i) {
+      const SkItem m = sk_item(a, s_seq, i, maxblk);
+      if (m.nb == 0) continue;
+      const int kb = s_seq[4 * m.slot + 3];
+      const int xb = max(lo, s_start[i]) - s_start[i], xe = min(hi, s_start[i + 1]) - s_start[i];
+      const int p_lo = max(m.L, kBlk * xb), p_hi = min(m.L + kb, kBlk * xe);
+      const int* pt_row = a.page_table + (size_t)m.b * a.max_pages;
+      for (int e = tid; e < (p_hi - p_lo) * (D / 8); e += 256) {
+        const int pos = p_lo + e / (D / 8), d0 = 8 * (e % (D / 8));
+        const int page = clampi(pt_row[clampi(pos >> 4, 0, a.max_pages - 1)], 0, a.num_pages - 1);
+        const int sl = pos & (PS - 1);
+        const size_t src = ((size_t)(m.r0 + pos - m.L) * a.Hkv + m.g) * D + d0;
+        const bf16x8 kv = *reinterpret_cast<const bf16x8*>(kn + src);
+        const bf16x8 vv = *reinterpret_cast<const bf16x8*>(vn + src);
+        const size_t pb = (size_t)(page * a.Hkv + m.g) * PS * D;
+        *reinterpret_cast<bf16x8*>(kw + pb + (d0 / 32) * (PS * 32) + sl * 32 + (d0 & 31)) = kv;
+#pragma unroll
+        for (int c = 0; c < 8; ++c) vw[pb + (size_t)(d0 + c) * PS + sl] = vv[c];
+      }
+    }
+  }
+  // Unit records: query unit h (rows 64 h .. 64 h + 63 of the item) holds
+  // 4 item + 2 h + 1; a key/value unit holds 4 x + 2 (last block of the
+  // item's piece) with x the block's offset in the share.  Block x of item i is
+  // unit (x - lo) + QT (non-empty items from i_first through i); the QT units
+  // before an item's first block are its queries.
+  for (int x = lo + tid; x < hi; x += 256) {
+    const int i = item_of(x);
+    const int u = (x - lo) + QT * (s_ne[i + 1] - s_ne[i_first]);
+    const int last = (x + 1 == s_start[i + 1] || x + 1 == hi) ? 2 : 0;
+    s_uq[u] = 4 * (x - lo) + last;
+    if (x == max(lo, s_start[i]))
+      for (int h = 0; h < QT; ++h) s_uq[u - QT + h] = 4 * i + 2 * h + 1;
+    const SkItem m = sk_item(a, s_seq, i, maxblk);
+    const int* pt_row = a.page_table + (size_t)m.b * a.max_pages;
+    const int pl = 2 * (x - s_start[i]);
+    s_pg[2 * (x - lo)] = clampi(pt_row[min(pl, a.max_pages - 1)], 0, a.num_pages - 1);
+    s_pg[2 * (x - lo) + 1] = clampi(pt_row[min(pl + 1, a.max_pages - 1)], 0, a.num_pages - 1);
+  }
+
+  // The window's stores and the page-table reads are done and the tables are
+  // visible before the first key/value unit is issued.
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  dma_next(0);
+  for (int m = 1; m < kSkBuf - 1; ++m) dma_unit(m);
 
   // Per-lane LDS offsets of the MFMA operands within a unit.  Channel
   // 16 dt + c16 lies in value piece dt / 2 at unit 2 (16 (dt % 2) + c16) + h',
@@ -790,18 +838,19 @@ __global__ __launch_bounds__(256, 2) void verify_attn_sk_kernel(AttnParams a) {
   }
   const int v_off0 = 8192 + 4096 * (j >> 1) + 16 * vpiece_unit(c16, j & 1);
 
-  for (int m = 0; m < kSkBuf - 1; ++m) dma_unit(m);
-
   // Compute side.  The units come as items: QT query units, then the item's
   // key/value units up to the one that ends its piece.  Tile tt of this wave
   // holds the item's rows 64 tt + 16 t .. 64 tt + 16 t + 15.
   int c_rec = uni(s_uq[0]);
   int n = 0;
   // Unit n of this wave's loads has landed (the next one may still be in
-  // flight); after the barrier every wave's pieces of it are visible, and
-  // every wave is done with unit n - 1, whose buffer the next issue refills.
+  // flight) and every LDS read this wave issued has returned (the query
+  // fragments are read into registers one unit or more before their first
+  // use, so the compiler would not wait for them here); after the barrier
+  // every wave's pieces of unit n are visible, and every wave is done with
+  // unit n - 1, whose buffer the next issue refills.
   auto next_unit = [&](int& rec) -> const char* {
-    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(4 * (kSkBuf - 2)) : "memory");
+    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)" ::"n"(4 * (kSkBuf - 2)) : "memory");
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
     dma_unit(n + kSkBuf - 1);
@@ -903,6 +952,11 @@ __global__ __launch_bounds__(256, 2) void verify_attn_sk_kernel(AttnParams a) {
           a.part_lse[ps * kRowsI + row] = l_tot > 0.f ? m_run[tt] + fast_log2(l_tot) : -INFINITY;
       }
     }
+    // The loop's count-based waits ("all but the newest unit's loads") count
+    // on the memory operations in flight completing in issue order, which is
+    // not promised once stores are mixed in: the piece's stores (and the
+    // units in flight) are waited for here.
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   }
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // reloads past the end
 }
@@ -1025,11 +1079,11 @@ hipError_t launch_t(const AttnParams& p, dim3 grid, dim3 cgrid, hipStream_t st) 
 }
 
 hipError_t launch_sk(const AttnParams& p, dim3 cgrid, hipStream_t st) {
+  // The window append happens inside the attention kernel (an empty
+  // interval in the trace where the other path has its append kernel).
   trace_begin(st);
-  hipLaunchKernelGGL((append_window_kernel<bf16, 128>), dim3(cgrid.y), dim3(256), 0, st, p);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
   trace_mark(st);
+  hipError_t e;
   if (p.item_rows == 128)
     hipLaunchKernelGGL(verify_attn_sk_kernel<2>, dim3(p.sk_grid), dim3(256), 0, st, p);
   else
