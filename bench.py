@@ -384,6 +384,9 @@ def main():
                     help="top-K coverage width (default: the workload's, 16); the coverage-width "
                          "ablation sweeps 4, 8, 16, 32")
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--profile-pass", action="store_true",
+                    help="only run W + K eager steps of the verify path (no other timing "
+                         "sections), for counter collection; prints the number of steps run")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only copy MIB MiB device-to-device 5 times (a kernel of known "
                          "traffic for scaling the HBM byte counters), then exit")
@@ -420,6 +423,13 @@ def main():
     for i in range(args.warmup):
         steps[i % n_rep].run()
     torch.cuda.synchronize()
+    if args.profile_pass:
+        for i in range(args.steps):
+            steps[i % n_rep].run()
+        torch.cuda.synchronize()
+        print(json.dumps({"profile_pass": True, "workload": cfg.name, "steps_run": args.warmup + args.steps,
+                          "n_models": len(step.per_model)}), flush=True)
+        return
 
     # the timed region: K steps, no per-kernel events inside it
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)

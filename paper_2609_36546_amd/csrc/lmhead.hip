@@ -1074,6 +1074,7 @@ __global__ __launch_bounds__(kMT) void sample_kernel(LmParams p, SampleParams s)
   __shared__ int s_first, s_last;
   __shared__ float s_cv[32];
   __shared__ int s_ci[32];
+  __shared__ float s_gq[4];
   int b, m;
   if (PER_ROW) {
     b = m = blockIdx.x;
@@ -1095,7 +1096,7 @@ __global__ __launch_bounds__(kMT) void sample_kernel(LmParams p, SampleParams s)
   // meanwhile (for the recompute below).
   const int per = ((G + kMT - 1) / kMT + 3) / 4 * 4;   // <= kMaxGPT (V <= kMT kMaxGPT kGroup)
   const int g0 = tid * per;
-  float v1r[kMaxGPT], wr[kMaxGPT];
+  float v1r[kMaxGPT], wr[kMaxGPT], qr[4][kMaxGPT];   // qr: each group's quarter sums
 #pragma unroll
   for (int blk = 0; blk < kMaxGPT / 4; ++blk) {
     const int g4 = g0 + 4 * blk;
@@ -1111,6 +1112,10 @@ __global__ __launch_bounds__(kMT) void sample_kernel(LmParams p, SampleParams s)
       const bool ok = ok4 && g4 + e < G;
       v1r[4 * blk + e] = ok ? v1[e] : -INFINITY;
       wr[4 * blk + e] = ok ? (q0[e] + q1[e]) + (q2[e] + q3[e]) : 0.f;
+      qr[0][4 * blk + e] = q0[e];
+      qr[1][4 * blk + e] = q1[e];
+      qr[2][4 * blk + e] = q2[e];
+      qr[3][4 * blk + e] = q3[e];
     }
   }
   {
@@ -1144,7 +1149,7 @@ __global__ __launch_bounds__(kMT) void sample_kernel(LmParams p, SampleParams s)
     const bool crossing = s_first < kMT;
     float c = incl - mine;
     int gi = -1;
-    float before = 0.f, w = 1.f;
+    float before = 0.f, w = 1.f, gq[4] = {0.f, 0.f, 0.f, 0.f};
     bool found = false;
 #pragma unroll
     for (int i = 0; i < kMaxGPT; ++i) {
@@ -1152,12 +1157,16 @@ __global__ __launch_bounds__(kMT) void sample_kernel(LmParams p, SampleParams s)
         gi = g0 + i;
         before = c;
         w = wr[i];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) gq[q] = qr[q][i];
         found = crossing && c + wr[i] > t;
       }
       c += wr[i];
     }
     s_g[0] = gi;
     s_red[2 * NW] = found ? fminf(fmaxf((t - before) / w, 0.f), 1.f) : 1.f;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) s_gq[q] = gq[q];   // the group's quarter sums, for every thread
   }
   __syncthreads();
   const int gsel = s_g[0];
@@ -1167,8 +1176,7 @@ __global__ __launch_bounds__(kMT) void sample_kernel(LmParams p, SampleParams s)
     return;
   }
   // the quarter of the group (32 entries) holding the draw, from its sums
-  const float q0 = p.rec_sq[0][base + gsel], q1 = p.rec_sq[1][base + gsel];
-  const float q2 = p.rec_sq[2][base + gsel], q3 = p.rec_sq[3][base + gsel];
+  const float q0 = s_gq[0], q1 = s_gq[1], q2 = s_gq[2], q3 = s_gq[3];
   const float qs[4] = {q0, q1, q2, q3};
   const float tq = frac * ((q0 + q1) + (q2 + q3));
   // first quarter whose cumulative sum passes tq; the last with mass when

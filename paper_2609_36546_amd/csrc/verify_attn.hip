@@ -973,33 +973,40 @@ __global__ __launch_bounds__(256) void attn_combine_sk_kernel(AttnParams a) {
   const int slot = blockIdx.y / a.Hkv, g = blockIdx.y % a.Hkv;
   const int it = (slot * a.Hkv + g) * a.n_qg + qg;
   const int n_it = a.n_seq * a.Hkv * a.n_qg;
+  // the item's block range and the sequence's rows, loaded side by side
   const int B_tot = a.sk_start[n_it];
   const int s0 = a.sk_start[it], s1 = a.sk_start[it + 1];
+  const int b = a.seq_ids ? a.seq_ids[slot] : slot;
+  const int r0 = a.cu_q[b];
+  const int kb = a.cu_q[b + 1] - r0;
   if (s1 <= s0) return;
   const int W = min(a.sk_grid, B_tot);
   // Workgroup whose share [B w / W, B (w+1) / W) holds block x.
   auto wg_of = [&](int x) { return min(W - 1, (int)(((long)(x + 1) * W - 1) / B_tot)); };
   const int w0 = wg_of(s0), w1 = wg_of(s1 - 1);
   if (w0 == w1) return;   // written whole by one workgroup
-  const int b = a.seq_ids ? a.seq_ids[slot] : slot;
-  const int r0 = a.cu_q[b];
-  const int kb = a.cu_q[b + 1] - r0;
   const int G = a.G;
   const int r = 16 * rq + threadIdx.x / 16;           // packed row within the group
   const int dq = (threadIdx.x % 16) * (D / 16);
   const int pr = qg * R + r;
   if (pr >= min(kb * G, (qg + 1) * R)) return;
-  float M = -INFINITY;
-  for (int w = w0; w <= w1; ++w) M = fmaxf(M, a.part_lse[((size_t)it + w) * R + r]);
-  const float Mu = (M == -INFINITY) ? 0.f : M;
+  // One pass over the pieces with a running maximum: each piece's weight and
+  // partial are loaded together.
+  float M = -INFINITY, wsum = 0.f;
   floatx4 o0 = {0.f, 0.f, 0.f, 0.f}, o1 = {0.f, 0.f, 0.f, 0.f};
-  float wsum = 0.f;
+#pragma unroll 4
   for (int w = w0; w <= w1; ++w) {
-    const float wgt = fast_exp2(a.part_lse[((size_t)it + w) * R + r] - Mu);
-    wsum += wgt;
+    const float lse = a.part_lse[((size_t)it + w) * R + r];
     const float* po = a.part_o + (((size_t)it + w) * R + r) * D + dq;
-    o0 += wgt * ld16<floatx4>(po);
-    o1 += wgt * ld16<floatx4>(po + 4);
+    const floatx4 p0 = ld16<floatx4>(po), p1 = ld16<floatx4>(po + 4);
+    const float Mn = fmaxf(M, lse);
+    const float Mu = (Mn == -INFINITY) ? 0.f : Mn;
+    const float sc = fast_exp2(M - Mu);                 // 0 while M is -inf
+    const float wgt = fast_exp2(lse - Mu);
+    wsum = wsum * sc + wgt;
+    o0 = o0 * sc + wgt * p0;
+    o1 = o1 * sc + wgt * p1;
+    M = Mn;
   }
   const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
   const int i = pr / G, hl = pr % G;

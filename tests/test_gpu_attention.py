@@ -85,6 +85,36 @@ def test_mixed_windows_and_two_models():
     _check_all(b, 1)
 
 
+def test_mixed_windows_repeated_nan_workspace():
+    """Regression: short-context, mixed-window teacher-shape batch (items of
+    32 rows in 128-row tiles, one block per workgroup, every item split into
+    pieces), called repeatedly on a NaN-filled workspace, so that a partial
+    read before it is written, or a ring slot refilled before its query
+    fragments were read, shows up as a non-finite or wrong row."""
+    cfg = inputs.scaled(inputs.WORKLOADS["dual-cache-bf16"], B=10, ctx_lo=0, ctx_hi=700,
+                        models=(inputs.scaled_shape(inputs.STUDENT, vocab=512, hidden=64),
+                                inputs.scaled_shape(inputs.TEACHER, vocab=512, hidden=64)))
+    b = _case(cfg, seed=5)
+    mdl = b.models[1]
+    seqs = to_np(mdl.seq_ids).astype(np.int64)
+    ref, _, _ = parity.oracle_attention(mdl, b, seqs, mdl.shape.D)
+    rows = to_np(mdl.rows).astype(np.int64)
+    dev = mdl.q.device
+    ctx = torch.from_numpy(np.asarray(b.ctx_lens, np.int32)).to(dev)
+    cu = torch.from_numpy(np.asarray(b.cu_q, np.int32)).to(dev)
+    max_q = int(np.max(np.diff(b.cu_q)))
+    n_ws = ops.attn_workspace_size(len(seqs), mdl.shape.Hq, mdl.shape.Hkv, mdl.shape.D, max_q,
+                                   mdl.page_table.shape[1], cfg.page_size)
+    for rep in range(8):
+        ws = torch.full((n_ws,), 0xFF, dtype=torch.uint8, device=dev)   # NaN as float32
+        kc, vc = mdl.k_pool.clone(), mdl.v_pool.clone()
+        out = ops.verify_attn_paged(mdl.q, mdl.k_new, mdl.v_new, kc, vc, mdl.page_table, ctx, cu,
+                                    max_q=max_q, seq_ids=mdl.seq_ids, workspace=ws)
+        torch.cuda.synchronize()
+        worst = parity.check_attention_rows(out, ref, rows, mdl.q.dtype)
+        _say(f"  rep {rep}: worst rel err {worst:.2e}")
+
+
 def test_head_dim_64_bf16():
     shape = inputs.ModelShape("d64", Hq=8, Hkv=2, D=64, hidden=64, vocab=512)
     cfg = inputs.scaled(inputs.WORKLOADS["teacher-bf16"], B=3, ctx_lo=5, ctx_hi=400, models=(shape,))
