@@ -82,17 +82,18 @@ __device__ __forceinline__ size_t w_off(const LmParams& p, int v, int c) {
 // the output, in output order (rows past V are zero).
 __global__ __launch_bounds__(256) void pack_w_kernel(const bf16* W, int V, int Hd, bf16* Wt,
                                                      size_t n_chunks) {
-  const size_t t = (size_t)blockIdx.x * 256 + threadIdx.x;
+  // n_chunks < 2^31 (the host checks), so the index math is 32-bit
+  const unsigned t = blockIdx.x * 256u + threadIdx.x;
   if (t >= n_chunks) return;
-  const size_t blk = t >> 6;                 // 64 chunks per 1 KB block
+  const unsigned blk = t >> 6;               // 64 chunks per 1 KB block
   const int within = (int)(t & 63);
-  const int nb_c = Hd >> 5;
+  const unsigned nb_c = (unsigned)Hd >> 5;
   const int v = (int)(blk / nb_c) * 16 + (within >> 2);
   const int c = (int)(blk % nb_c) * 32 + (within & 3) * 8;
   typedef __attribute__((__vector_size__(16))) int i32x4;
   i32x4 x = {0, 0, 0, 0};
   if (v < V) x = ld16<i32x4>(W + (size_t)v * Hd + c);
-  *reinterpret_cast<i32x4*>(Wt + t * 8) = x;
+  *reinterpret_cast<i32x4*>(Wt + (size_t)t * 8) = x;
 }
 
 // MFMA flavour per input type.  STAGE = hidden channels per pipeline stage;
@@ -1292,6 +1293,7 @@ void launch_gemm(const LmParams& p, dim3 grid, hipStream_t st, float) {
 
 template <typename DT, int RB>
 hipError_t launch_rb(const LmParams& p, hipStream_t st) {
+  if ((size_t)((p.M + 15) / 16) * 16 * p.Hd / 8 >= (size_t(1) << 31)) return hipErrorInvalidValue;   // pack index range
   const dim3 grid = gemm_grid(p);
   trace_begin(st);
   launch_gemm<RB>(p, grid, st, DT{});
@@ -1471,6 +1473,7 @@ hipError_t launch_sample_takeover(const SampleLaunch& L, const LmPlan& pl, hipSt
 hipError_t launch_pack_w(const void* W, int V, int Hd, void* W_tiled, hipStream_t st) {
   const size_t n_chunks = (size_t)((V + 15) / 16) * 16 * Hd / 8;
   if (n_chunks == 0) return hipSuccess;
+  if (n_chunks >= (size_t(1) << 31)) return hipErrorInvalidValue;   // pack index range
   trace_begin(st);
   hipLaunchKernelGGL(pack_w_kernel, dim3((unsigned)((n_chunks + 255) / 256)), dim3(256), 0, st,
                      reinterpret_cast<const bf16*>(W), V, Hd, reinterpret_cast<bf16*>(W_tiled),
