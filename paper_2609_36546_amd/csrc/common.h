@@ -29,6 +29,59 @@ __device__ __forceinline__ float wave_max_xor(float v, int mask) {
   return fmaxf(v, __shfl_xor(v, mask, kWave));
 }
 
+// ---- wave reductions and scans with DPP moves (VALU, no LDS round trip) ----
+// DPP controls (GFX9): quad_perm p0 | p1 << 2 | p2 << 4 | p3 << 6, row_shr:n
+// 0x110 + n, row_mirror 0x140, row_half_mirror 0x141.  Rows are 16 lanes.
+template <int CTRL>
+__device__ __forceinline__ float dpp_move(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xf, 0xf, true));
+}
+// The value of lane i ^ 32 / i ^ 16 (v_permlane32_swap / v_permlane16_swap).
+__device__ __forceinline__ float lane_xor32(float v) {
+  const unsigned u = __float_as_uint(v);
+  const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  return __uint_as_float(lane_id() < 32 ? r[1] : r[0]);
+}
+__device__ __forceinline__ int lane_xor32(int v) {
+  const auto r = __builtin_amdgcn_permlane32_swap((unsigned)v, (unsigned)v, false, false);
+  return (int)(lane_id() < 32 ? r[1] : r[0]);
+}
+__device__ __forceinline__ float lane_xor16(float v) {
+  const unsigned u = __float_as_uint(v);
+  const auto r = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  return __uint_as_float((lane_id() & 16) ? r[0] : r[1]);
+}
+// Combine over the wave, result in every lane: a butterfly inside each row
+// (mirror, half mirror, then the quad swaps 2 and 1 pair disjoint lane sets
+// at every step, so each lane's value enters once), then across the rows.
+template <class OP>
+__device__ __forceinline__ float wave_reduce(float v, OP op) {
+  v = op(v, dpp_move<0x140>(v));
+  v = op(v, dpp_move<0x141>(v));
+  v = op(v, dpp_move<0x4E>(v));   // quad_perm [2, 3, 0, 1]
+  v = op(v, dpp_move<0xB1>(v));   // quad_perm [1, 0, 3, 2]
+  v = op(v, lane_xor16(v));
+  return op(v, lane_xor32(v));
+}
+__device__ __forceinline__ float wave_sum(float v) {
+  return wave_reduce(v, [](float a, float b) { return a + b; });
+}
+__device__ __forceinline__ float wave_max(float v) {
+  return wave_reduce(v, [](float a, float b) { return fmaxf(a, b); });
+}
+// Inclusive prefix sum over the wave's lanes (lane order).
+__device__ __forceinline__ float wave_incl_scan(float v) {
+  v += dpp_move<0x111>(v);   // row_shr:1 (lanes without a source add 0)
+  v += dpp_move<0x112>(v);
+  v += dpp_move<0x114>(v);
+  v += dpp_move<0x118>(v);
+  const float r0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 15));
+  const float r1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 31));
+  const float r2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 47));
+  const int row = lane_id() >> 4;
+  return v + (row > 0 ? r0 : 0.f) + (row > 1 ? r1 : 0.f) + (row > 2 ? r2 : 0.f);
+}
+
 __device__ __forceinline__ float to_f32(float x) { return x; }
 __device__ __forceinline__ float to_f32(bf16 x) { return static_cast<float>(x); }
 

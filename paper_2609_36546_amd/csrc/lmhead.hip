@@ -193,10 +193,10 @@ __device__ __forceinline__ void lm_epilogue(const LmParams& p, floatx16 (&acc)[4
     {
       // merge the partner lane's top-3: the fourth of the union is the max of
       // the fourth after pushing its top-3 and its own fourth
-      const float ov1 = __shfl_xor(v1, 32, kWave), ov2 = __shfl_xor(v2, 32, kWave);
-      const float ov3 = __shfl_xor(v3, 32, kWave), ov4 = __shfl_xor(v4, 32, kWave);
-      const int oi1 = __shfl_xor(i1, 32, kWave), oi2 = __shfl_xor(i2, 32, kWave);
-      const int oi3 = __shfl_xor(i3, 32, kWave);
+      const float ov1 = lane_xor32(v1), ov2 = lane_xor32(v2);
+      const float ov3 = lane_xor32(v3), ov4 = lane_xor32(v4);
+      const int oi1 = lane_xor32(i1), oi2 = lane_xor32(i2);
+      const int oi3 = lane_xor32(i3);
       top3_push(ov1, oi1, v1, i1, v2, i2, v3, i3, v4);
       top3_push(ov2, oi2, v1, i1, v2, i2, v3, i3, v4);
       top3_push(ov3, oi3, v1, i1, v2, i2, v3, i3, v4);
@@ -217,8 +217,8 @@ __device__ __forceinline__ void lm_epilogue(const LmParams& p, floatx16 (&acc)[4
         ee += (x != -INFINITY) ? pe * x : 0.f;
     }
 #pragma unroll
-    for (int q = 0; q < 4; ++q) sq[q] += __shfl_xor(sq[q], 32, kWave);
-    ee += __shfl_xor(ee, 32, kWave);
+    for (int q = 0; q < 4; ++q) sq[q] += lane_xor32(sq[q]);
+    ee += lane_xor32(ee);
     if (h == 0 && m < p.M && g < p.n_groups) {
       const size_t r = (size_t)m * p.rec_stride + g;
       p.rec_v1[r] = v1;
@@ -545,7 +545,7 @@ __device__ __forceinline__ bool before(float a, int ia, float b, int ib) {
 }
 
 __device__ float block_sum(float x, float* s) {
-  for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o, kWave);
+  x = wave_sum(x);
   const int w = threadIdx.x >> 6;
   __syncthreads();
   if (lane_id() == 0) s[w] = x;
@@ -557,11 +557,9 @@ __device__ float block_sum(float x, float* s) {
 
 // Block sums of three values at once (s holds 3 * waves floats).
 __device__ void block_sum3(float& a, float& b, float& c, float* s) {
-  for (int o = 32; o > 0; o >>= 1) {
-    a += __shfl_xor(a, o, kWave);
-    b += __shfl_xor(b, o, kWave);
-    c += __shfl_xor(c, o, kWave);
-  }
+  a = wave_sum(a);
+  b = wave_sum(b);
+  c = wave_sum(c);
   constexpr int NW = kMT / kWave;
   const int w = threadIdx.x >> 6;
   __syncthreads();
@@ -572,7 +570,7 @@ __device__ void block_sum3(float& a, float& b, float& c, float* s) {
 }
 
 __device__ float block_max(float x, float* s) {
-  for (int o = 32; o > 0; o >>= 1) x = fmaxf(x, __shfl_xor(x, o, kWave));
+  x = wave_max(x);
   const int w = threadIdx.x >> 6;
   __syncthreads();
   if (lane_id() == 0) s[w] = x;
@@ -732,7 +730,7 @@ __device__ void recompute_entries(const LmParams& p, const float* s_hid, int n, 
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
       float a = acc[b];
-      for (int o = 32; o > 0; o >>= 1) a += __shfl_xor(a, o, kWave);
+      a = wave_sum(a);
       if (lane == 0 && e0 + b < n) {
         const bool ok = vv[b] < p.V;
         out_v[e0 + b] = ok ? a : -INFINITY;
@@ -1044,11 +1042,7 @@ struct SampleParams {
 __device__ float block_scan(float x, float* s_w, float* total) {
   const int lane = lane_id(), w = threadIdx.x / kWave;
   constexpr int NW = kMT / kWave;
-#pragma unroll
-  for (int o = 1; o < kWave; o <<= 1) {
-    const float y = __shfl_up(x, o, kWave);
-    if (lane >= o) x += y;
-  }
+  x = wave_incl_scan(x);
   __syncthreads();
   if (lane == kWave - 1) s_w[w] = x;
   __syncthreads();
@@ -1140,8 +1134,15 @@ __global__ __launch_bounds__(kMT) void sample_kernel(LmParams p, SampleParams s)
   // t above every cumulative sum, the last group with mass is taken
   if (tid == 0) { s_first = kMT; s_last = -1; s_g[0] = -1; }
   __syncthreads();
-  if (mine > 0.f && incl > t) atomicMin(&s_first, tid);
-  if (mine > 0.f) atomicMax(&s_last, tid);
+  {
+    // one LDS atomic per wave: its first thread whose range passes t, its
+    // last thread with mass
+    const unsigned long long m_in = __ballot(mine > 0.f && incl > t);
+    const unsigned long long m_nz = __ballot(mine > 0.f);
+    const int w0 = tid & ~(kWave - 1);
+    if (lane_id() == 0 && m_in) atomicMin(&s_first, w0 + __builtin_ctzll(m_in));
+    if (lane_id() == 0 && m_nz) atomicMax(&s_last, w0 + 63 - __builtin_clzll(m_nz));
+  }
   __syncthreads();
   const int owner = s_first < kMT ? s_first : s_last;
   if (tid == owner) {
@@ -1203,15 +1204,10 @@ __global__ __launch_bounds__(kMT) void sample_kernel(LmParams p, SampleParams s)
   if (tid < kWave) {
     const float a = tid < 32 ? s_cv[tid] : -INFINITY;
     float gm = a;
-    for (int o = 32; o > 0; o >>= 1) gm = fmaxf(gm, __shfl_xor(gm, o, kWave));
+    gm = wave_max(gm);
     const float pr = a == -INFINITY ? 0.f : fast_exp2((a - gm) * kLog2e);
-    float c = pr;
-#pragma unroll
-    for (int o = 1; o < kWave; o <<= 1) {
-      const float y = __shfl_up(c, o, kWave);
-      if (tid >= o) c += y;
-    }
-    const float S = __shfl(c, kWave - 1, kWave);
+    const float c = wave_incl_scan(pr);
+    const float S = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(c), kWave - 1));
     const float th = frac2 * S;
     const unsigned long long in = __ballot(pr > 0.f && c > th);
     const unsigned long long nz = __ballot(pr > 0.f);

@@ -245,9 +245,9 @@ __device__ __forceinline__ void attend_block(const AttnParams& a, const FS& f,
     }
   }
 #pragma unroll
-  for (int t = 0; t < QT; ++t) bm[t] = wave_max_xor(bm[t], 16);
+  for (int t = 0; t < QT; ++t) bm[t] = fmaxf(bm[t], lane_xor16(bm[t]));
 #pragma unroll
-  for (int t = 0; t < QT; ++t) bm[t] = wave_max_xor(bm[t], 32);
+  for (int t = 0; t < QT; ++t) bm[t] = fmaxf(bm[t], lane_xor32(bm[t]));
   const float c = a.scale_log2;
   float m_use[QT];
   bool rescale = false;
@@ -437,8 +437,8 @@ __global__ __launch_bounds__(256) void verify_attn_kernel(AttnParams a) {
   // Row sums are partial per lane group: reduce over the 4 groups.
 #pragma unroll
   for (int t = 0; t < QT; ++t) {
-    l_run[t] += __shfl_xor(l_run[t], 16, kWave);
-    l_run[t] += __shfl_xor(l_run[t], 32, kWave);
+    l_run[t] += lane_xor16(l_run[t]);
+    l_run[t] += lane_xor32(l_run[t]);
   }
 
   // Merge the four waves' partials.
@@ -927,8 +927,8 @@ __global__ __launch_bounds__(256, 2) void verify_attn_sk_kernel(AttnParams a) {
     // leaves a partial at slot item + workgroup.
 #pragma unroll
     for (int tt = 0; tt < QT; ++tt) {
-      float l_tot = l_run[tt] + __shfl_xor(l_run[tt], 16, kWave);
-      l_tot += __shfl_xor(l_tot, 32, kWave);
+      float l_tot = l_run[tt] + lane_xor16(l_run[tt]);
+      l_tot += lane_xor32(l_tot);
       const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
       if (!has_rows[tt] || prq[tt] > it.pr_last) continue;
       if (full) {
