@@ -121,13 +121,19 @@ template <> struct Mm<float> {
   __device__ static int koff(int ks, int h) { return 16 * h + ks; }
 };
 
+// (value desc, index asc) order: true if (a, ia) ranks before (b, ib).
+__device__ __forceinline__ bool before(float a, int ia, float b, int ib) {
+  // bitwise, not short-circuit: compares and selects, no branches in loops
+  return (a > b) | ((a == b) & (ia < ib));
+}
+
 // Top-3 (value desc, index asc) insertion of (x, ix), with the fourth value:
 // (v1, i1) >= (v2, i2) >= (v3, i3) >= v4.
 __device__ __forceinline__ void top3_push(float x, int ix, float& v1, int& i1, float& v2, int& i2,
                                           float& v3, int& i3, float& v4) {
-  const bool c1 = x > v1 || (x == v1 && ix < i1);
-  const bool c2 = x > v2 || (x == v2 && ix < i2);
-  const bool c3 = x > v3 || (x == v3 && ix < i3);
+  const bool c1 = before(x, ix, v1, i1);
+  const bool c2 = before(x, ix, v2, i2);
+  const bool c3 = before(x, ix, v3, i3);
   v4 = __builtin_amdgcn_fmed3f(v3, v4, x);
   const float nv3 = c2 ? v2 : (c3 ? x : v3);
   const int ni3 = c2 ? i2 : (c3 ? ix : i3);
@@ -539,10 +545,6 @@ __global__ __launch_bounds__(64 * NW) void lmhead_gemm_dlds_kernel(LmParams p) {
 
 constexpr int kMT = 256;
 
-// (value desc, index asc) order: true if (a, ia) ranks before (b, ib).
-__device__ __forceinline__ bool before(float a, int ia, float b, int ib) {
-  return a > b || (a == b && ia < ib);
-}
 
 __device__ float block_sum(float x, float* s) {
   x = wave_sum(x);
@@ -663,7 +665,7 @@ __device__ __forceinline__ void block_topk_rank(const float* lv, const int* li, 
         const floatx4 y = *reinterpret_cast<const floatx4*>(lv + c);
         const i32x4 yi = *reinterpret_cast<const i32x4*>(li + c);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) r += (c + e < n && before(y[e], yi[e], v, i)) ? 1 : 0;
+        for (int e = 0; e < 4; ++e) r += ((c + e < n) & before(y[e], yi[e], v, i)) ? 1 : 0;
       }
       if (r < K) {
         out_v[r] = v;
@@ -875,7 +877,7 @@ __global__ __launch_bounds__(kMT) void lmhead_merge_kernel(LmParams p) {
     for (int c = 0; c < kWave; c += 4) {
       const floatx4 y = *reinterpret_cast<const floatx4*>(wm + c);
 #pragma unroll
-      for (int e = 0; e < 4; ++e) r += (y[e] > mx || (y[e] == mx && c + e < lane)) ? 1 : 0;
+      for (int e = 0; e < 4; ++e) r += before(y[e], c + e, mx, lane) ? 1 : 0;
     }
     if (r == K - 1) s_theta[wv] = mx;
   }
