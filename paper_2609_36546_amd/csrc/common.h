@@ -69,6 +69,22 @@ __device__ __forceinline__ float wave_sum(float v) {
 __device__ __forceinline__ float wave_max(float v) {
   return wave_reduce(v, [](float a, float b) { return fmaxf(a, b); });
 }
+// Inclusive prefix sum of ints over the wave's lanes (lane order).
+template <int CTRL>
+__device__ __forceinline__ int dpp_move_i(int v) {
+  return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xf, 0xf, true);
+}
+__device__ __forceinline__ int wave_incl_scan_i(int v) {
+  v += dpp_move_i<0x111>(v);
+  v += dpp_move_i<0x112>(v);
+  v += dpp_move_i<0x114>(v);
+  v += dpp_move_i<0x118>(v);
+  const int r0 = __builtin_amdgcn_readlane(v, 15);
+  const int r1 = __builtin_amdgcn_readlane(v, 31);
+  const int r2 = __builtin_amdgcn_readlane(v, 47);
+  const int row = lane_id() >> 4;
+  return v + (row > 0 ? r0 : 0) + (row > 1 ? r1 : 0) + (row > 2 ? r2 : 0);
+}
 // Inclusive prefix sum over the wave's lanes (lane order).
 __device__ __forceinline__ float wave_incl_scan(float v) {
   v += dpp_move<0x111>(v);   // row_shr:1 (lanes without a source add 0)

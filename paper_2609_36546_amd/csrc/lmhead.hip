@@ -884,12 +884,23 @@ __global__ __launch_bounds__(kMT) void lmhead_merge_kernel(LmParams p) {
   __syncthreads();
   float theta = s_theta[0];
   for (int w2 = 1; w2 < NW; ++w2) theta = fmaxf(theta, s_theta[w2]);
-  // survivors: candidates >= theta
+  // survivors: candidates >= theta, compacted with one LDS atomic per wave
+  // (a wave prefix of the per-thread counts places each thread's run)
+  {
+    int cnt = 0;
 #pragma unroll
-  for (int c = 0; c < kCPG * kMaxGPT; ++c) {
-    if (ci[c] != 0x7fffffff && cv[c] >= theta) {
-      const int slot = atomicAdd(&s_n, 1);
-      if (slot < kCap) { s_lv[slot] = cv[c]; s_li[slot] = ci[c]; }
+    for (int c = 0; c < kCPG * kMaxGPT; ++c) cnt += ((ci[c] != 0x7fffffff) & (cv[c] >= theta)) ? 1 : 0;
+    const int incl = wave_incl_scan_i(cnt);
+    const int wtot = __builtin_amdgcn_readlane(incl, kWave - 1);
+    int wbase = 0;
+    if (lane == 0 && wtot > 0) wbase = atomicAdd(&s_n, wtot);
+    int slot = __builtin_amdgcn_readlane(wbase, 0) + incl - cnt;
+#pragma unroll
+    for (int c = 0; c < kCPG * kMaxGPT; ++c) {
+      if ((ci[c] != 0x7fffffff) & (cv[c] >= theta)) {
+        if (slot < kCap) { s_lv[slot] = cv[c]; s_li[slot] = ci[c]; }
+        ++slot;
+      }
     }
   }
   __syncthreads();
@@ -931,13 +942,14 @@ __global__ __launch_bounds__(kMT) void lmhead_merge_kernel(LmParams p) {
     // group when it is the group's first pick and two later picks share it.
     if (tid < K) {
       const int ia = s_top_i[tid];
-      const int ga = ia / kGroup;
+      const int ga = (int)((unsigned)ia / kGroup);
       bool first = ia != 0x7fffffff;
       int later = 0;
       for (int b2 = 0; b2 < K; ++b2) {
-        const bool same = b2 != tid && s_top_i[b2] != 0x7fffffff && s_top_i[b2] / kGroup == ga;
-        first &= !(same && b2 < tid);
-        later += (same && b2 > tid) ? 1 : 0;
+        const int ib = s_top_i[b2];
+        const bool same = (b2 != tid) & (ib != 0x7fffffff) & ((int)((unsigned)ib / kGroup) == ga);
+        first &= !(same & (b2 < tid));
+        later += (same & (b2 > tid)) ? 1 : 0;
       }
       if (first && later >= kCPG - 1 && p.rec_v4[base + ga] >= s_top_v[K - 1]) {
         const int slot = atomicAdd(&s_nsplit, 1);
