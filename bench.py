@@ -38,7 +38,7 @@ from paper_2609_36546_amd import inputs, ops  # noqa: E402
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 METRIC = "verified tokens/sec at Qwen3-30B-A3B teacher shape; HBM GB/s vs peak"
-KERNELS = ["append", "attention", "combine", "lmhead_gemm", "lmhead_merge", "accept_scan",
+KERNELS = ["append", "attention", "combine", "lmhead_pack", "lmhead_gemm", "lmhead_merge", "accept_scan",
            "sample_takeover"]
 PROFILES = os.path.join(ROOT, "profiles")
 REPLICA_BYTES = 2 << 30        # data cycled by the timed steps: at least this much
@@ -226,7 +226,7 @@ def time_propose_step(dev, reps, seed=0):
     for _ in range(3):
         once()
     torch.cuda.synchronize()
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(9)] for _ in range(reps)]
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(10)] for _ in range(reps)]
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     start.record()
     for r in range(reps):
@@ -236,7 +236,8 @@ def time_propose_step(dev, reps, seed=0):
     ops.trace_events(None)
     torch.cuda.synchronize()
     ms = start.elapsed_time(stop) / reps
-    names = ["append", "attention", "combine", None, "lmhead_gemm", "lmhead_merge", None, "sample"]
+    names = ["append", "attention", "combine", None, "lmhead_pack", "lmhead_gemm", "lmhead_merge", None,
+             "sample"]
     kt = {n: sum(e[i].elapsed_time(e[i + 1]) for e in evs) / reps * 1e3
           for i, n in enumerate(names) if n}
     w_bytes = m.shape.vocab * m.shape.hidden * m.W.element_size()
@@ -427,8 +428,11 @@ def main():
         for i in range(args.steps):
             steps[i % n_rep].run()
         torch.cuda.synchronize()
+        nm = len(step.per_model)
         print(json.dumps({"profile_pass": True, "workload": cfg.name, "steps_run": args.warmup + args.steps,
-                          "n_models": len(step.per_model)}), flush=True)
+                          "n_models": nm,
+                          "alg_bytes_per_launch": {k: v[0] / nm for k, v in work.items()},
+                          "alg_flops_per_launch": {k: v[1] / nm for k, v in work.items()}}), flush=True)
         return
 
     # the timed region: K steps, no per-kernel events inside it
@@ -478,7 +482,7 @@ def main():
     # per-kernel timing, in a separate eager pass: the library records these
     # events around its kernels
     n_models = len(step.per_model)
-    per_step = 9 * n_models + 2
+    per_step = 10 * n_models + 2
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(per_step)] for _ in range(args.steps)]
     t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -494,15 +498,18 @@ def main():
     kt = {k: 0.0 for k in KERNELS}
     for s in range(args.steps):
         e = evs[s]
-        # per model: attention call records 4 events, lmhead call 3 events
+        # per model: the attention call records 4 events (begin; append,
+        # attention and combine ends), the lmhead call 4 (begin; hidden copy,
+        # GEMM and merge ends)
         i = 0
         for _ in range(n_models):
             kt["append"] += e[i].elapsed_time(e[i + 1])
             kt["attention"] += e[i + 1].elapsed_time(e[i + 2])
             kt["combine"] += e[i + 2].elapsed_time(e[i + 3])
-            kt["lmhead_gemm"] += e[i + 4].elapsed_time(e[i + 5])
-            kt["lmhead_merge"] += e[i + 5].elapsed_time(e[i + 6])
-            i += 7
+            kt["lmhead_pack"] += e[i + 4].elapsed_time(e[i + 5])
+            kt["lmhead_gemm"] += e[i + 5].elapsed_time(e[i + 6])
+            kt["lmhead_merge"] += e[i + 6].elapsed_time(e[i + 7])
+            i += 8
         kt["accept_scan"] += e[i].elapsed_time(e[i + 1])
         i += 2
         for _ in range(n_models):

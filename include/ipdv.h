@@ -527,11 +527,13 @@ int source_split_kl(int M, int K,
  * one after it, every further kernel one after it.  Recording stops when
  * `capacity` events are used.  NULL / 0 turns it off.  Returns IPDV_OK.
  * ipdv_trace_count() returns how many events have been recorded since the
- * hook was last set.  Kernels per call: verify_attn_paged 3 (append,
- * attention, split combine), lmhead_logsoftmax_verify 2 (GEMM + epilogue,
- * merge), accept_scan 1, accept_scan_rule 1, sample_takeover 1,
- * lmhead_sample 1, lmhead_pack_w 1, lmhead_logp_gather 1, source_split_kl 1
- * (+1 with cu).
+ * hook was last set.  Intervals per call: verify_attn_paged 3 (append,
+ * attention, split combine; on the bf16 D = 128 16-token-page path the
+ * attention kernel appends the window itself and the append interval is
+ * empty), lmhead_logsoftmax_verify 3 (the hidden rows' copy into the tiled
+ * layout, empty where none is made; GEMM + epilogue; merge), accept_scan 1,
+ * accept_scan_rule 1, sample_takeover 1, lmhead_sample 1, lmhead_pack_w 1,
+ * lmhead_logp_gather 1, source_split_kl 1 (+1 with cu).
  */
 int ipdv_trace_events(void* const* events, int capacity);
 int ipdv_trace_count(void);

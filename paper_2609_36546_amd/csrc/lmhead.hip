@@ -1261,6 +1261,7 @@ void launch_gemm(const LmParams& p, dim3 grid, hipStream_t st, bf16) {
   // copy in W's tiled block layout, written first into the workspace, so
   // that every operand load reads whole cache lines.
   if (p.Hd % kDStage != 0) {
+    trace_mark(st);   // no hidden copy on this path: an empty interval
     hipLaunchKernelGGL((lmhead_gemm_kernel<bf16, RB>), grid, dim3(256), 0, st, p);
     return;
   }
@@ -1268,6 +1269,7 @@ void launch_gemm(const LmParams& p, dim3 grid, hipStream_t st, bf16) {
   hipLaunchKernelGGL(pack_w_kernel, dim3((unsigned)((n_chunks + 255) / 256)), dim3(256), 0, st,
                      reinterpret_cast<const bf16*>(p.hidden), p.M, p.Hd,
                      reinterpret_cast<bf16*>(const_cast<void*>(p.hidden_tiled)), n_chunks);
+  trace_mark(st);   // the hidden copy's interval ends here; the GEMM's begins
   if constexpr (RB == 4) {
     // With one row tile (M <= 256): 256-row tiles for as many whole rounds
     // of one tile per compute unit as the vocabulary fills; the vocabulary
@@ -1298,6 +1300,7 @@ void launch_gemm(const LmParams& p, dim3 grid, hipStream_t st, bf16) {
 
 template <int RB>
 void launch_gemm(const LmParams& p, dim3 grid, hipStream_t st, float) {
+  trace_mark(st);   // no hidden copy for fp32: an empty interval
   hipLaunchKernelGGL((lmhead_gemm_kernel<float, RB>), grid, dim3(256), 0, st, p);
 }
 
