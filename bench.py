@@ -435,7 +435,6 @@ def main():
                           "alg_flops_per_launch": {k: v[1] / nm for k, v in work.items()}}), flush=True)
         return
 
-    # the timed region: K steps, no per-kernel events inside it
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     graph = None
     if args.launch == "graph":
@@ -452,19 +451,12 @@ def main():
             step.run()
         for _ in range(args.warmup):
             graph.replay()
-    torch.cuda.synchronize()
-    start.record()
-    for s in range(args.steps):
-        if graph is not None:
-            graph.replay()
-        else:
-            steps[s % n_rep].run()
-    stop.record()
-    torch.cuda.synchronize()
-    ms = start.elapsed_time(stop) / args.steps
 
-    # per-step distribution, in a separate pass of at least 50 steps with one
-    # event between steps
+    # per-step distribution, in a pass of at least 50 steps with one event
+    # between steps.  It runs before the timed region: the first steps after
+    # an idle period run slower while the GPU's clocks come up (about 15 steps
+    # at the teacher shape), so the K timed steps that follow see the steady
+    # state that a serving loop runs in.
     n_dist = max(50, args.steps)
     bounds = [torch.cuda.Event(enable_timing=True) for _ in range(n_dist + 1)]
     torch.cuda.synchronize()
@@ -478,6 +470,18 @@ def main():
     torch.cuda.synchronize()
     per_step = np.array([bounds[s].elapsed_time(bounds[s + 1]) for s in range(n_dist)])
     p10, p50, p90 = (float(np.percentile(per_step, q)) for q in (10, 50, 90))
+
+    # the timed region: K steps, no events inside it
+    torch.cuda.synchronize()
+    start.record()
+    for s in range(args.steps):
+        if graph is not None:
+            graph.replay()
+        else:
+            steps[s % n_rep].run()
+    stop.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(stop) / args.steps
 
     # per-kernel timing, in a separate eager pass: the library records these
     # events around its kernels

@@ -181,17 +181,52 @@ __device__ __forceinline__ void lm_epilogue(const LmParams& p, floatx16 (&acc)[4
     }
     float v1 = -INFINITY, v2 = -INFINITY, v3 = -INFINITY, v4 = -INFINITY;
     int j1 = 0, j2 = 0, j3 = 0;
+    bool ranked = false;
+    if (FULL) {
+      // Values first: each entry is clamped into the sorted top-4.
 #pragma unroll
-    for (int j = 0; j < 64; ++j) {
-      const float x = acc[j >> 4][rb][j & 15];
-      const bool c1 = x > v1, c2 = x > v2, c3 = x > v3;
-      v4 = __builtin_amdgcn_fmed3f(v3, v4, x);
-      v3 = __builtin_amdgcn_fmed3f(v2, v3, x);
-      v2 = __builtin_amdgcn_fmed3f(v1, v2, x);
-      v1 = c1 ? x : v1;   // a select on c1: fmaxf would add a NaN-quieting max per entry
-      j3 = c2 ? j2 : (c3 ? j : j3);
-      j2 = c1 ? j1 : (c2 ? j : j2);
-      j1 = c1 ? j : j1;
+      for (int j = 0; j < 64; ++j) {
+        const float x = acc[j >> 4][rb][j & 15];
+        v4 = __builtin_amdgcn_fmed3f(v3, v4, x);
+        v3 = __builtin_amdgcn_fmed3f(v2, v3, x);
+        v2 = __builtin_amdgcn_fmed3f(v1, v2, x);
+        // a plain v_max: fmaxf (or a med3 against infinity) would add a
+        // NaN-quieting max per entry
+        asm("v_max_f32 %0, %1, %2" : "=v"(v1) : "v"(v1), "v"(x));
+      }
+      // Equal values among a lane's top three anywhere in the wave send the
+      // wave through the single-pass ranking below.
+      ranked = __builtin_amdgcn_ballot_w64((v1 == v2) | (v2 == v3)) == 0;
+    }
+    if (ranked) {
+      // Then the indices.  With v1 > v2 > v3 the first two values occur once
+      // and v3 may recur (an equal later entry ranks behind the first), so
+      // the first entry holding each value is its index: a downward scan
+      // keeps the lowest.
+#pragma unroll
+      for (int j = 63; j >= 0; --j) {
+        const float x = acc[j >> 4][rb][j & 15];
+        j1 = (x == v1) ? j : j1;
+        j2 = (x == v2) ? j : j2;
+        j3 = (x == v3) ? j : j3;
+        // one entry at a time: hoisted compares would each hold a lane mask
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    } else {
+      v1 = v2 = v3 = v4 = -INFINITY;
+      j1 = j2 = j3 = 0;
+#pragma unroll
+      for (int j = 0; j < 64; ++j) {
+        const float x = acc[j >> 4][rb][j & 15];
+        const bool c1 = x > v1, c2 = x > v2, c3 = x > v3;
+        v4 = __builtin_amdgcn_fmed3f(v3, v4, x);
+        v3 = __builtin_amdgcn_fmed3f(v2, v3, x);
+        v2 = __builtin_amdgcn_fmed3f(v1, v2, x);
+        v1 = c1 ? x : v1;   // a select on c1: fmaxf would add a NaN-quieting max per entry
+        j3 = c2 ? j2 : (c3 ? j : j3);
+        j2 = c1 ? j1 : (c2 ? j : j2);
+        j1 = c1 ? j : j1;
+      }
     }
     int i1 = (v1 == -INFINITY) ? 0x7fffffff : vlane + epi_off(j1);
     int i2 = (v2 == -INFINITY) ? 0x7fffffff : vlane + epi_off(j2);
@@ -451,11 +486,11 @@ __global__ __launch_bounds__(64 * NW) void lmhead_gemm_dlds_kernel(LmParams p) {
   auto load = [&](int set, const char* buf, int ks) {
     const int x = 32 * ks;
 #pragma unroll
-    for (int vb = 0; vb < 4; ++vb)
-      fa[set][vb] = *reinterpret_cast<const bf16x8*>(buf + ((a_off + 2048 * vb) ^ x));
-#pragma unroll
     for (int rb = 0; rb < RB; ++rb)
       fb[set][rb] = *reinterpret_cast<const bf16x8*>(buf + ((b_off + 2048 * rb) ^ x));
+#pragma unroll
+    for (int vb = 0; vb < 4; ++vb)
+      fa[set][vb] = *reinterpret_cast<const bf16x8*>(buf + ((a_off + 2048 * vb) ^ x));
   };
 
   floatx16 acc[4][RB];
@@ -473,17 +508,20 @@ __global__ __launch_bounds__(64 * NW) void lmhead_gemm_dlds_kernel(LmParams p) {
   };
 #define IPDV_SB __builtin_amdgcn_sched_barrier(0)
 
-  // Boundary into stage b: each wave waits for its own loads of b (NBUF - 3
-  // later stages may stay in flight), the barrier makes every wave's visible,
-  // and buffer (b - 2) % NBUF starts refilling with stage b + NBUF - 2.  Every
-  // wave has consumed stage b - 2: it waited for that stage's last operands
-  // before its final MFMAs, which precede this barrier.  Stage b - 1 may still
-  // be read (its last k-step's operands can be in flight), so it is not
-  // refilled yet.  A bare s_barrier: the fence of __syncthreads would wait for
-  // every stage in flight.  The refill's loads are spread over the MFMAs up to
-  // the next boundary (a burst of them stalls the issuing wave, and with one
-  // wave per SIMD that idles the matrix pipe); the operand reads of the next
-  // k-step sit between MFMAs too.  sched_barrier pins the order.
+  // Boundary into stage b, between the two k-steps of stage b - 1: each wave
+  // waits for its own loads of b (NBUF - 3 later stages may stay in flight),
+  // the barrier makes every wave's visible, and buffer (b - 2) % NBUF starts
+  // refilling with stage b + NBUF - 2.  Every wave has consumed stage b - 2:
+  // it waited for that stage's last operands before its second k-step's
+  // MFMAs, which precede this barrier.  Stage b - 1 may still be read (its
+  // second k-step's operands can be in flight), so it is not refilled yet.  A
+  // bare s_barrier: the fence of __syncthreads would wait for every stage in
+  // flight.  The operand reads of a k-step are issued one k-step of MFMAs
+  // ahead of their use (stage b's first k-step right after the boundary, its
+  // second at the top of stage b), the hidden fragments first, since every
+  // MFMA of the k-step needs them.  The refill's loads are spread over the
+  // MFMAs (a burst of them stalls the issuing wave, and that idles its share
+  // of the matrix pipe).  sched_barrier pins the order.
   constexpr int Q1 = PW / 4, Q2 = PW / 2, Q3 = 3 * PW / 4;   // refill split points
 #pragma unroll
   for (int s0 = 0; s0 < NBUF - 1; ++s0) dma(s0, 0, PW);
@@ -494,10 +532,11 @@ __global__ __launch_bounds__(64 * NW) void lmhead_gemm_dlds_kernel(LmParams p) {
   for (int st = 0; st + 1 < nst; ++st) {
     const char* cur = s_ring + (st % NBUF) * SB;
     const int pend = st + NBUF - 2;            // refill started at the last boundary
+    load(1, cur, 1);
+    IPDV_SB;
     mma(0, 0);
     IPDV_SB;
     if (st > 0) dma(pend, Q1, Q2);
-    load(1, cur, 1);
     IPDV_SB;
     mma(0, 1);
     IPDV_SB;
@@ -508,8 +547,6 @@ __global__ __launch_bounds__(64 * NW) void lmhead_gemm_dlds_kernel(LmParams p) {
     if (st > 0) dma(pend, Q3, PW);
     IPDV_SB;
     mma(0, 3);
-    mma(1, 0);
-    mma(1, 1);
     IPDV_SB;
     asm volatile("s_waitcnt vmcnt(%0)" ::"n"((NBUF - 3) * PW) : "memory");
     __builtin_amdgcn_s_barrier();
@@ -517,14 +554,16 @@ __global__ __launch_bounds__(64 * NW) void lmhead_gemm_dlds_kernel(LmParams p) {
     dma(pend + 1, 0, Q1);
     load(0, s_ring + ((st + 1) % NBUF) * SB, 0);
     IPDV_SB;
+    mma(1, 0);
+    mma(1, 1);
     mma(1, 2);
     mma(1, 3);
     IPDV_SB;
   }
   {
     const char* cur = s_ring + ((nst - 1) % NBUF) * SB;
-    mma(0, 0);
     load(1, cur, 1);
+    mma(0, 0);
     mma(0, 1);
     mma(0, 2);
     mma(0, 3);
