@@ -452,24 +452,28 @@ def main():
         for _ in range(args.warmup):
             graph.replay()
 
-    # per-step distribution, in a pass of at least 50 steps with one event
-    # between steps.  It runs before the timed region: the first steps after
-    # an idle period run slower while the GPU's clocks come up (about 15 steps
-    # at the teacher shape), so the K timed steps that follow see the steady
-    # state that a serving loop runs in.
+    def step_pass(n):
+        # n steps with one event between steps: per-step times in ms
+        bounds = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
+        torch.cuda.synchronize()
+        bounds[0].record()
+        for s in range(n):
+            if graph is not None:
+                graph.replay()
+            else:
+                steps[s % n_rep].run()
+            bounds[s + 1].record()
+        torch.cuda.synchronize()
+        return np.array([bounds[s].elapsed_time(bounds[s + 1]) for s in range(n)])
+
+    # The first steps after an idle period run slower while the GPU's clocks
+    # come up (about 15 steps at the teacher shape).  A pass of max(50, K)
+    # steps runs first, and its first and last ten steps are reported, so the
+    # K timed steps that follow see the steady state that a serving loop runs
+    # in; a second pass of the same length after the timed region gives the
+    # per-step p10/p50/p90.
     n_dist = max(50, args.steps)
-    bounds = [torch.cuda.Event(enable_timing=True) for _ in range(n_dist + 1)]
-    torch.cuda.synchronize()
-    bounds[0].record()
-    for s in range(n_dist):
-        if graph is not None:
-            graph.replay()
-        else:
-            steps[s % n_rep].run()
-        bounds[s + 1].record()
-    torch.cuda.synchronize()
-    per_step = np.array([bounds[s].elapsed_time(bounds[s + 1]) for s in range(n_dist)])
-    p10, p50, p90 = (float(np.percentile(per_step, q)) for q in (10, 50, 90))
+    first = step_pass(n_dist)
 
     # the timed region: K steps, no events inside it
     torch.cuda.synchronize()
@@ -482,6 +486,9 @@ def main():
     stop.record()
     torch.cuda.synchronize()
     ms = start.elapsed_time(stop) / args.steps
+
+    per_step = step_pass(n_dist)
+    p10, p50, p90 = (float(np.percentile(per_step, q)) for q in (10, 50, 90))
 
     # per-kernel timing, in a separate eager pass: the library records these
     # events around its kernels
@@ -550,6 +557,7 @@ def main():
         "ms_per_step": round(ms, 4),
         "ms_per_step_p10_p50_p90": [round(p10, 4), round(p50, 4), round(p90, 4)],
         "distribution_steps": n_dist,
+        "first_pass_ms_first10_last10": [round(float(first[:10].mean()), 4), round(float(first[-10:].mean()), 4)],
         "input_replicas": n_rep,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16" if cfg.dtype == "bf16" else "f32", "data": "synthetic",
