@@ -193,6 +193,9 @@ __device__ __forceinline__ void lm_epilogue(const LmParams& p, floatx16 (&acc)[4
         // a plain v_max: fmaxf (or a med3 against infinity) would add a
         // NaN-quieting max per entry
         asm("v_max_f32 %0, %1, %2" : "=v"(v1) : "v"(v1), "v"(x));
+        // v4 here, entry by entry: left to itself the compiler keeps every
+        // intermediate v3 in a register of its own and builds v4 later
+        asm volatile("" : "+v"(v4));
       }
       // Equal values among a lane's top three anywhere in the wave send the
       // wave through the single-pass ranking below.
@@ -285,16 +288,17 @@ __device__ __forceinline__ void lm_epilogue_any(const LmParams& p, floatx16 (&ac
     lm_epilogue<RB, false>(p, acc, vt, m0, wv, wr);
 }
 
-// Tile of this workgroup.  The hardware deals workgroup ids to the 8 XCDs
-// round-robin (id % 8).  XCD x takes a contiguous range of vocabulary tiles,
-// and the row tiles of one vocabulary tile run back to back on it: the W tile
-// they share is fetched from HBM once into that XCD's L2, and every 64-byte
-// line of the group records (16 groups = 8 vocabulary tiles of one row) is
-// completed inside one L2 before it is written back.  A launch covers the
-// vocabulary tiles vt_base .. vt_base + n_vt_run - 1; its grid holds
-// ceil(n_vt_run / 8) * 8 * n_rt workgroups; the surplus returns at once.
-__device__ __forceinline__ bool gemm_tile(const LmParams& p, int& vt, int& rt) {
-  const int id = blockIdx.x;
+// Tile number id.  The hardware deals workgroup ids to the 8 XCDs
+// round-robin (id % 8), and a persistent workgroup steps its tile number by
+// the grid size, a multiple of 8, so it stays on its XCD.  XCD x takes a
+// contiguous range of vocabulary tiles, and the row tiles of one vocabulary
+// tile run side by side on it: the W tile they share is fetched from HBM
+// once into that XCD's L2, and every 64-byte line of the group records (16
+// groups = 8 vocabulary tiles of one row) is completed inside one L2 before
+// it is written back.  A launch covers the vocabulary tiles vt_base ..
+// vt_base + n_vt_run - 1, as tile numbers below ceil(n_vt_run / 8) * 8 * n_rt;
+// the others are empty (false).
+__device__ __forceinline__ bool gemm_tile(const LmParams& p, int id, int& vt, int& rt) {
   const int xcd = id & 7, local = id >> 3;
   const int per = p.n_vt_run / 8, extra = p.n_vt_run % 8;
   const int j = local / p.n_rt;
@@ -307,7 +311,7 @@ __device__ __forceinline__ bool gemm_tile(const LmParams& p, int& vt, int& rt) {
 template <typename DT, int RB>
 __global__ __launch_bounds__(256) void lmhead_gemm_kernel(LmParams p) {
   int vt, rt;
-  if (!gemm_tile(p, vt, rt)) return;
+  if (!gemm_tile(p, blockIdx.x, vt, rt)) return;
   typedef Mm<DT> MM;
   constexpr int NM = 64 * RB;                       // hidden rows per workgroup
   constexpr int LDW = MM::STAGE + 16 / (int)sizeof(DT);   // LDS row pitch (elements)
@@ -415,8 +419,8 @@ template <int RB, int NBUF, int NW>
 __global__ __launch_bounds__(64 * NW) void lmhead_gemm_dlds_kernel(LmParams p) {
   static_assert(NBUF >= 3 && NBUF <= 5, "ring depth");
   static_assert(NW == 4 || NW == 8, "2 x (NW / 2) waves");
-  int vt, rt;
-  if (!gemm_tile(p, vt, rt)) return;
+  int id = blockIdx.x, vt, rt;
+  if (!gemm_tile(p, id, vt, rt)) return;
   constexpr int NM = 32 * RB * (NW / 2);        // hidden rows per workgroup
   constexpr int WB = kVT * 64;                  // W tile bytes per stage
   constexpr int SB = WB + NM * 64;              // stage bytes
@@ -424,8 +428,6 @@ __global__ __launch_bounds__(64 * NW) void lmhead_gemm_dlds_kernel(LmParams p) {
   constexpr int PW = NBLK / NW;                 // load instructions per wave and stage
   constexpr int KS = kDStage / 16;              // MFMA k-steps per stage
   static_assert(KS == 2 && (NBUF - 2) * PW <= 63 && NBLK % NW == 0, "pipeline shape");
-  const int m0 = rt * NM;
-  const int v0 = vt * kVT;
   const int tid = threadIdx.x;
   const int w = tid >> 6;
   const int wv = w & 1, wr = w >> 1;
@@ -438,31 +440,36 @@ __global__ __launch_bounds__(64 * NW) void lmhead_gemm_dlds_kernel(LmParams p) {
 
   const bf16* Wp = reinterpret_cast<const bf16*>(p.W);
   const bf16* Hp = reinterpret_cast<const bf16*>(p.hidden_tiled);
-  // This lane's source row and chunk for each of its load blocks.
+  // This lane's source row and chunk for each of its load blocks, for tile
+  // (vt_, rt_).
   const bf16* src[PW];
+  auto set_src = [&](int vt_, int rt_) {
+    const int m0 = rt_ * NM, v0 = vt_ * kVT;
 #pragma unroll
-  for (int j = 0; j < PW; ++j) {
-    const int u = w + NW * j;
-    const int r = (u < kVT / 16 ? 16 * u : 16 * (u - kVT / 16)) + (lane >> 2);
-    const int c = (lane & 3) ^ ((r >> 2) & 3);
-    if (u < kVT / 16) {
-      if (p.w_tiled) {
-        // the stage's 16 rows x 32 channels are one 1 KB block; the lane takes
-        // the same row and (swizzled) chunk as in the row-major case, so the
-        // LDS image is identical.  Blocks past V: any valid block, masked later.
-        const int vb = min((v0 >> 4) + u, ((p.V + 15) >> 4) - 1);
-        src[j] = Wp + (size_t)vb * (p.Hd >> 5) * 512 + (lane >> 2) * 32 + 8 * c;
+    for (int j = 0; j < PW; ++j) {
+      const int u = w + NW * j;
+      const int r = (u < kVT / 16 ? 16 * u : 16 * (u - kVT / 16)) + (lane >> 2);
+      const int c = (lane & 3) ^ ((r >> 2) & 3);
+      if (u < kVT / 16) {
+        if (p.w_tiled) {
+          // the stage's 16 rows x 32 channels are one 1 KB block; the lane takes
+          // the same row and (swizzled) chunk as in the row-major case, so the
+          // LDS image is identical.  Blocks past V: any valid block, masked later.
+          const int vb = min((v0 >> 4) + u, ((p.V + 15) >> 4) - 1);
+          src[j] = Wp + (size_t)vb * (p.Hd >> 5) * 512 + (lane >> 2) * 32 + 8 * c;
+        } else {
+          const int v = min(v0 + r, p.V - 1);     // rows past V: any valid row, masked later
+          src[j] = Wp + (size_t)v * p.Hd + 8 * c;
+        }
       } else {
-        const int v = min(v0 + r, p.V - 1);     // rows past V: any valid row, masked later
-        src[j] = Wp + (size_t)v * p.Hd + 8 * c;
+        // hidden rows come from the per-call copy in the same 16-row x 32-channel
+        // block layout (rows past M there are zero and never stored)
+        const int mb = min((m0 >> 4) + (u - kVT / 16), ((p.M + 15) >> 4) - 1);
+        src[j] = Hp + (size_t)mb * (p.Hd >> 5) * 512 + (lane >> 2) * 32 + 8 * c;
       }
-    } else {
-      // hidden rows come from the per-call copy in the same 16-row x 32-channel
-      // block layout (rows past M there are zero and never stored)
-      const int mb = min((m0 >> 4) + (u - kVT / 16), ((p.M + 15) >> 4) - 1);
-      src[j] = Hp + (size_t)mb * (p.Hd >> 5) * 512 + (lane >> 2) * 32 + 8 * c;
     }
-  }
+  };
+  set_src(vt, rt);
   // Stage st goes to buffer st % NBUF.  Stages past the end reload the last
   // one into a free buffer, so that every wave has the same number of loads
   // in flight at every boundary.  dma(st, j0, j1): this wave's load blocks
@@ -494,12 +501,6 @@ __global__ __launch_bounds__(64 * NW) void lmhead_gemm_dlds_kernel(LmParams p) {
   };
 
   floatx16 acc[4][RB];
-#pragma unroll
-  for (int vb = 0; vb < 4; ++vb)
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) acc[vb][rb][e] = 0.f;
   // MFMAs of operand set `set` over vocabulary block vb.
   auto mma = [&](int set, int vb) {
 #pragma unroll
@@ -522,60 +523,94 @@ __global__ __launch_bounds__(64 * NW) void lmhead_gemm_dlds_kernel(LmParams p) {
   // MFMA of the k-step needs them.  The refill's loads are spread over the
   // MFMAs (a burst of them stalls the issuing wave, and that idles its share
   // of the matrix pipe).  sched_barrier pins the order.
+  //
+  // The workgroup is persistent: after a tile's last MFMAs it waits for the
+  // reloads past the end, and once every wave is done with the ring it
+  // issues the first NBUF - 1 stages of its next tile, whose loads land while
+  // the finished tile's epilogue runs.  The next tile's first wait is then a
+  // full one: the epilogue's record stores are in flight too, and loads and
+  // stores are not promised to complete in issue order.
   constexpr int Q1 = PW / 4, Q2 = PW / 2, Q3 = 3 * PW / 4;   // refill split points
 #pragma unroll
   for (int s0 = 0; s0 < NBUF - 1; ++s0) dma(s0, 0, PW);
-  asm volatile("s_waitcnt vmcnt(%0)" ::"n"((NBUF - 2) * PW) : "memory");
-  __builtin_amdgcn_s_barrier();
-  asm volatile("" ::: "memory");
-  load(0, s_ring, 0);
-  for (int st = 0; st + 1 < nst; ++st) {
-    const char* cur = s_ring + (st % NBUF) * SB;
-    const int pend = st + NBUF - 2;            // refill started at the last boundary
-    load(1, cur, 1);
-    IPDV_SB;
-    mma(0, 0);
-    IPDV_SB;
-    if (st > 0) dma(pend, Q1, Q2);
-    IPDV_SB;
-    mma(0, 1);
-    IPDV_SB;
-    if (st > 0) dma(pend, Q2, Q3);
-    IPDV_SB;
-    mma(0, 2);
-    IPDV_SB;
-    if (st > 0) dma(pend, Q3, PW);
-    IPDV_SB;
-    mma(0, 3);
-    IPDV_SB;
-    asm volatile("s_waitcnt vmcnt(%0)" ::"n"((NBUF - 3) * PW) : "memory");
+  bool first = true;
+  for (;;) {
+    if (first)
+      asm volatile("s_waitcnt vmcnt(%0)" ::"n"((NBUF - 2) * PW) : "memory");
+    else
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
-    dma(pend + 1, 0, Q1);
-    load(0, s_ring + ((st + 1) % NBUF) * SB, 0);
-    IPDV_SB;
-    mma(1, 0);
-    mma(1, 1);
-    mma(1, 2);
-    mma(1, 3);
-    IPDV_SB;
-  }
-  {
-    const char* cur = s_ring + ((nst - 1) % NBUF) * SB;
-    load(1, cur, 1);
-    mma(0, 0);
-    mma(0, 1);
-    mma(0, 2);
-    mma(0, 3);
-    mma(1, 0);
-    mma(1, 1);
-    mma(1, 2);
-    mma(1, 3);
+    load(0, s_ring, 0);
+#pragma unroll
+    for (int vb = 0; vb < 4; ++vb)
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) acc[vb][rb][e] = 0.f;
+    for (int st = 0; st + 1 < nst; ++st) {
+      const char* cur = s_ring + (st % NBUF) * SB;
+      const int pend = st + NBUF - 2;            // refill started at the last boundary
+      load(1, cur, 1);
+      IPDV_SB;
+      mma(0, 0);
+      IPDV_SB;
+      if (st > 0) dma(pend, Q1, Q2);
+      IPDV_SB;
+      mma(0, 1);
+      IPDV_SB;
+      if (st > 0) dma(pend, Q2, Q3);
+      IPDV_SB;
+      mma(0, 2);
+      IPDV_SB;
+      if (st > 0) dma(pend, Q3, PW);
+      IPDV_SB;
+      mma(0, 3);
+      IPDV_SB;
+      asm volatile("s_waitcnt vmcnt(%0)" ::"n"((NBUF - 3) * PW) : "memory");
+      __builtin_amdgcn_s_barrier();
+      asm volatile("" ::: "memory");
+      dma(pend + 1, 0, Q1);
+      load(0, s_ring + ((st + 1) % NBUF) * SB, 0);
+      IPDV_SB;
+      mma(1, 0);
+      mma(1, 1);
+      mma(1, 2);
+      mma(1, 3);
+      IPDV_SB;
+    }
+    {
+      const char* cur = s_ring + ((nst - 1) % NBUF) * SB;
+      load(1, cur, 1);
+      mma(0, 0);
+      mma(0, 1);
+      mma(0, 2);
+      mma(0, 3);
+      mma(1, 0);
+      mma(1, 1);
+      mma(1, 2);
+      mma(1, 3);
+    }
+    // the reloads past the end, and this wave's last operand reads
+    asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
+
+    const int vt_done = vt, m0_done = rt * NM;
+    id += gridDim.x;
+    const bool more = gemm_tile(p, id, vt, rt);
+    if (more) {
+      __builtin_amdgcn_s_barrier();   // every wave is done with the ring
+      asm volatile("" ::: "memory");
+      set_src(vt, rt);
+#pragma unroll
+      for (int s0 = 0; s0 < NBUF - 1; ++s0) dma(s0, 0, PW);
+    }
+    lm_epilogue_any<RB>(p, acc, vt_done, m0_done, wv, wr);
+    if (!more) break;
+    // the load addresses again, rather than held in registers across the epilogue
+    set_src(vt, rt);
+    first = false;
   }
 #undef IPDV_SB
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // reloads past the end still in flight
-
-  lm_epilogue_any<RB>(p, acc, vt, m0, wv, wr);
 }
 
 // ---------------------------------------------------------------------------
@@ -1292,6 +1327,29 @@ int device_cus() {
 
 dim3 gemm_grid(const LmParams& p) { return dim3((p.n_vt_run + 7) / 8 * 8 * p.n_rt); }
 
+// Launch of the persistent direct-to-LDS GEMM: as many workgroups as the
+// device holds at once (cached per device; a multiple of 8, so that each
+// stays on its XCD), but no more than there are tile numbers.
+template <int RB, int NBUF, int NW>
+void launch_dlds(const LmParams& q, hipStream_t st) {
+  static int slots[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) dev = -1;
+  int n = dev >= 0 ? slots[dev] : 0;
+  if (n == 0) {
+    int per_cu = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
+            &per_cu, reinterpret_cast<const void*>(&lmhead_gemm_dlds_kernel<RB, NBUF, NW>), 64 * NW, 0) !=
+            hipSuccess ||
+        per_cu < 1)
+      per_cu = 1;
+    n = max(8, device_cus() * per_cu / 8 * 8);
+    if (dev >= 0) slots[dev] = n;
+  }
+  const dim3 grid((unsigned)min((int)gemm_grid(q).x, n));
+  hipLaunchKernelGGL((lmhead_gemm_dlds_kernel<RB, NBUF, NW>), grid, dim3(64 * NW), 0, st, q);
+}
+
 template <int RB>
 void launch_gemm(const LmParams& p, dim3 grid, hipStream_t st, bf16) {
   // 64 * RB hidden rows per workgroup.  256 and 128 rows take eight waves
@@ -1323,18 +1381,18 @@ void launch_gemm(const LmParams& p, dim3 grid, hipStream_t st, bf16) {
     if (n_main > 0) {
       q.vt_base = 0;
       q.n_vt_run = n_main;
-      hipLaunchKernelGGL((lmhead_gemm_dlds_kernel<2, 4, 8>), gemm_grid(q), dim3(512), 0, st, q);
+      launch_dlds<2, 4, 8>(q, st);
     }
     if (n_main < p.n_vt) {
       q.vt_base = n_main;
       q.n_vt_run = p.n_vt - n_main;
       q.n_rt = (p.M + 127) / 128;
-      hipLaunchKernelGGL((lmhead_gemm_dlds_kernel<1, 4, 8>), gemm_grid(q), dim3(512), 0, st, q);
+      launch_dlds<1, 4, 8>(q, st);
     }
   } else if constexpr (RB == 2)
-    hipLaunchKernelGGL((lmhead_gemm_dlds_kernel<1, 4, 8>), grid, dim3(512), 0, st, p);
+    launch_dlds<1, 4, 8>(p, st);
   else
-    hipLaunchKernelGGL((lmhead_gemm_dlds_kernel<RB, 4, 4>), grid, dim3(256), 0, st, p);
+    launch_dlds<RB, 4, 4>(p, st);
 }
 
 template <int RB>
