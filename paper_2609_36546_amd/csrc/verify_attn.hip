@@ -657,62 +657,72 @@ __global__ __launch_bounds__(256, 2) void verify_attn_sk_kernel(AttnParams a) {
   __syncthreads();
   const int per = (n_it + 255) / 256;
   const int i_lo = min(n_it, tid * per), i_hi = min(n_it, (tid + 1) * per);
+  const int w = blockIdx.x;
+  int B_tot = 0, W = 0, lo = 0, hi = 0;
   {
+    // The thread's items' block counts (kept in s_start until their offsets
+    // are known), then exclusive scans over the threads, whose order is item
+    // order: within each wave with DPP moves, across the four waves' totals.
     int run = 0, cnt = 0;
     for (int i = i_lo; i < i_hi; ++i) {
       const int nb = sk_item(a, s_seq, i, maxblk).nb;
+      s_start[i] = nb;
       run += nb;
       cnt += nb > 0;
     }
-    s_part[0][tid] = run;
-    s_part[1][tid] = cnt;
-  }
-  __syncthreads();
-  if (t < 2) {
-    // 256 partial sums, 4 per lane: exclusive scan across the wave
-    int v[4], tot = 0;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) { v[e] = s_part[t][4 * lane + e]; tot += v[e]; }
-    int inc = tot;
-#pragma unroll
-    for (int o = 1; o < kWave; o <<= 1) {
-      const int y = __shfl_up(inc, o, kWave);
-      if (lane >= o) inc += y;
+    const int inc_r = wave_incl_scan_i(run), inc_c = wave_incl_scan_i(cnt);
+    if (lane == kWave - 1) {
+      s_part[0][t] = inc_r;
+      s_part[1][t] = inc_c;
     }
-    int ex = inc - tot;
+    __syncthreads();
+    int bs = inc_r - run, ns = inc_c - cnt;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) { s_part[t][4 * lane + e] = ex; ex += v[e]; }
-  }
-  __syncthreads();
-  {
-    int bs = s_part[0][tid], ns = s_part[1][tid];
+    for (int k = 0; k < 4; ++k) {
+      B_tot += s_part[0][k];
+      if (k < t) {
+        bs += s_part[0][k];
+        ns += s_part[1][k];
+      }
+    }
+    // Share [lo, hi) of the blocks; 32-bit arithmetic while B_tot * W fits.
+    W = min((int)gridDim.x, B_tot);
+    if (w < W) {
+      if (B_tot < (1 << 22) && W <= 1024) {
+        lo = (int)((unsigned)B_tot * (unsigned)w / (unsigned)W);
+        hi = (int)((unsigned)B_tot * (unsigned)(w + 1) / (unsigned)W);
+      } else {
+        lo = (int)((long)B_tot * w / W);
+        hi = (int)((long)B_tot * (w + 1) / W);
+      }
+    }
+    // Item offsets, and the items that hold the share's first and last
+    // blocks (each found by the one thread that owns it).
     for (int i = i_lo; i < i_hi; ++i) {
+      const int nb = s_start[i];
       s_start[i] = bs;
       s_ne[i] = ns;
-      const int nb = sk_item(a, s_seq, i, maxblk).nb;
+      if (bs <= lo && lo < bs + nb) s_part[0][4] = i;
+      if (bs < hi && hi <= bs + nb) s_part[1][4] = i;
       bs += nb;
       ns += nb > 0;
     }
     if (tid == 255) { s_start[n_it] = bs; s_ne[n_it] = ns; }   // thread 255 ends at n_it or owns no items
   }
   __syncthreads();
-  const int B_tot = s_start[n_it];
   if (blockIdx.x == 0)
     for (int i = tid; i <= n_it; i += 256) a.sk_start[i] = s_start[i];
-  const int W = min((int)gridDim.x, B_tot);
-  const int w = blockIdx.x;
   if (w >= W) return;
-  const int lo = (int)((long)B_tot * w / W), hi = (int)((long)B_tot * (w + 1) / W);
-  // Item of block x: s_start[i] <= x < s_start[i + 1] (empty items never qualify).
-  auto item_of = [&](int x) {
-    int l0 = 0, l1 = n_it - 1;
+  const int i_first = uni(s_part[0][4]), i_last = uni(s_part[1][4]);
+  // Item of block x among items l0 .. l1: s_start[i] <= x < s_start[i + 1]
+  // (empty items never qualify).
+  auto item_of = [&](int x, int l0, int l1) {
     while (l0 < l1) {
       const int mid = (l0 + l1 + 1) >> 1;
       if (s_start[mid] <= x) l0 = mid; else l1 = mid - 1;
     }
     return l0;
   };
-  const int i_first = uni(item_of(lo)), i_last = uni(item_of(hi - 1));
   const int n_units = (hi - lo) + QT * (s_ne[i_last + 1] - s_ne[i_first]);
   if (2 * (n_it + 1) + 4 * a.n_seq + 2 * (hi - lo) + n_units > kSkMeta) return;
   int* s_uq = s_pg + 2 * (hi - lo);          // [n_units] the workgroup's units, in order
@@ -768,13 +778,41 @@ __global__ __launch_bounds__(256, 2) void verify_attn_sk_kernel(AttnParams a) {
   // overlaps the page-table reads and the window append below.
   dma_issue(0);
 
+  // Unit records: query unit h (rows 64 h .. 64 h + 63 of the item) holds
+  // 4 item + 2 h + 1; a key/value unit holds 4 x + 2 (last block of the
+  // item's piece) with x the block's offset in the share.  Block x of item i is
+  // unit (x - lo) + QT (non-empty items from i_first through i); the QT units
+  // before an item's first block are its queries.  The page ids of a
+  // thread's first block stay in registers until the window append below has
+  // issued its own loads, so that both sets of loads are in flight together;
+  // those of further blocks (shares above 256 blocks) are written at once.
+  int pg_x = -1, pg_a = 0, pg_b = 0;
+  for (int x = lo + tid; x < hi; x += 256) {
+    const int i = item_of(x, i_first, i_last);
+    const int u = (x - lo) + QT * (s_ne[i + 1] - s_ne[i_first]);
+    const int last = (x + 1 == s_start[i + 1] || x + 1 == hi) ? 2 : 0;
+    s_uq[u] = 4 * (x - lo) + last;
+    if (x == max(lo, s_start[i]))
+      for (int h = 0; h < QT; ++h) s_uq[u - QT + h] = 4 * i + 2 * h + 1;
+    const SkItem m = sk_item(a, s_seq, i, maxblk);
+    const int* pt_row = a.page_table + (size_t)m.b * a.max_pages;
+    const int pl = 2 * (x - s_start[i]);
+    const int ga = pt_row[min(pl, a.max_pages - 1)], gb = pt_row[min(pl + 1, a.max_pages - 1)];
+    if (pg_x < 0) {
+      pg_x = x;
+      pg_a = ga;
+      pg_b = gb;
+    } else {
+      s_pg[2 * (x - lo)] = clampi(ga, 0, a.num_pages - 1);
+      s_pg[2 * (x - lo) + 1] = clampi(gb, 0, a.num_pages - 1);
+    }
+  }
 
   // Window append: the window's keys and values at positions L .. L+k-1 go
   // to the pages, for the positions inside this share's blocks (every window
   // position lies in some item's blocks; positions in two shares are written
   // twice, with the same values).  Each workgroup writes the positions it
-  // reads, and waits for the writes before it loads any key/value unit; the
-  // stores are issued first, so that the page-table reads below overlap them.
+  // reads, and waits for the writes before it loads any key/value unit.
   {
     bf16* kw = reinterpret_cast<bf16*>(a.k_cache);
     bf16* vw = reinterpret_cast<bf16*>(a.v_cache);
@@ -801,23 +839,9 @@ __global__ __launch_bounds__(256, 2) void verify_attn_sk_kernel(AttnParams a) {
       }
     }
   }
-  // Unit records: query unit h (rows 64 h .. 64 h + 63 of the item) holds
-  // 4 item + 2 h + 1; a key/value unit holds 4 x + 2 (last block of the
-  // item's piece) with x the block's offset in the share.  Block x of item i is
-  // unit (x - lo) + QT (non-empty items from i_first through i); the QT units
-  // before an item's first block are its queries.
-  for (int x = lo + tid; x < hi; x += 256) {
-    const int i = item_of(x);
-    const int u = (x - lo) + QT * (s_ne[i + 1] - s_ne[i_first]);
-    const int last = (x + 1 == s_start[i + 1] || x + 1 == hi) ? 2 : 0;
-    s_uq[u] = 4 * (x - lo) + last;
-    if (x == max(lo, s_start[i]))
-      for (int h = 0; h < QT; ++h) s_uq[u - QT + h] = 4 * i + 2 * h + 1;
-    const SkItem m = sk_item(a, s_seq, i, maxblk);
-    const int* pt_row = a.page_table + (size_t)m.b * a.max_pages;
-    const int pl = 2 * (x - s_start[i]);
-    s_pg[2 * (x - lo)] = clampi(pt_row[min(pl, a.max_pages - 1)], 0, a.num_pages - 1);
-    s_pg[2 * (x - lo) + 1] = clampi(pt_row[min(pl + 1, a.max_pages - 1)], 0, a.num_pages - 1);
+  if (pg_x >= 0) {
+    s_pg[2 * (pg_x - lo)] = clampi(pg_a, 0, a.num_pages - 1);
+    s_pg[2 * (pg_x - lo) + 1] = clampi(pg_b, 0, a.num_pages - 1);
   }
 
   // The window's stores and the page-table reads are done and the tables are
