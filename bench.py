@@ -250,8 +250,10 @@ def time_propose_step(dev, reps, seed=0):
 
 def time_attention_calls(steps, reps):
     """Median seconds of one step's verify_attn_paged calls (all models),
-    each call bracketed by its own event pair, with no events inside it."""
-    per = []
+    each call bracketed by its own event pair, with no events inside it.
+    The calls run back to back (one synchronisation after all of them), as
+    in a stream of steps."""
+    all_evs = []
     for r in range(reps):
         st = steps[r % len(steps)]
         evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
@@ -263,8 +265,9 @@ def time_attention_calls(steps, reps):
                                   st.ctx, st.cu, st.max_q, seq_ids=m.seq_ids,
                                   out=pm["out"], workspace=pm["ws_a"])
             e1.record()
-        torch.cuda.synchronize()
-        per.append(sum(e0.elapsed_time(e1) for e0, e1 in evs) * 1e-3)
+        all_evs.append(evs)
+    torch.cuda.synchronize()
+    per = [sum(e0.elapsed_time(e1) for e0, e1 in evs) * 1e-3 for evs in all_evs]
     return float(np.median(per))
 
 
