@@ -76,11 +76,11 @@ __global__ __launch_bounds__(256) void accept_scan_kernel(ScanParams p) {
     if (mask == 0) continue;
     const int first = __builtin_ctzll(mask);
     const int fi = i0 + first;
-    const bool f_allowed = __shfl(allowed ? 1 : 0, first, kWave);
-    const bool f_take = __shfl(take ? 1 : 0, first, kWave);
-    const bool f_hand = __shfl(hand ? 1 : 0, first, kWave);
-    const bool f_eos = __shfl(is_eos ? 1 : 0, first, kWave);
-    const bool f_cap = __shfl(cap_after ? 1 : 0, first, kWave);
+    // the first stopping lane's flags, read with one readlane (first is wave-uniform)
+    const int flags = (allowed ? 1 : 0) | (take ? 2 : 0) | (hand ? 4 : 0) | (is_eos ? 8 : 0) |
+                      (cap_after ? 16 : 0);
+    const int f = __builtin_amdgcn_readlane(flags, first);
+    const bool f_allowed = f & 1, f_take = f & 2, f_hand = f & 4, f_eos = f & 8, f_cap = f & 16;
     if (!f_allowed) {
       n_acc = fi;
       fin = 1;
