@@ -233,3 +233,23 @@ def test_many_sequences_beyond_stream_k_tables():
     cfg = inputs.scaled(inputs.WORKLOADS["teacher-bf16"], B=1000, ctx_lo=0, ctx_hi=40, pool_tokens=None,
                         models=(inputs.scaled_shape(inputs.TEACHER, vocab=512, hidden=64),))
     _check_all(_case(cfg, seed=11))
+
+
+def test_stream_k_shares_above_256_blocks():
+    """Eight student-head sequences with contexts near 70K tokens: about
+    140K key blocks, so each of the stream-K kernel's 512 workgroups streams
+    more than 256 blocks and its threads record the page ids of two blocks
+    each (the second written at once, the first after the window append's
+    loads); the oracle checks the longest and the shortest sequence."""
+    base = inputs.WORKLOADS["student-bf16"]
+    cfg = inputs.scaled(base, B=8, ctx_lo=68000, ctx_hi=72000,
+                        models=(inputs.scaled_shape(base.models[0], vocab=512, hidden=64),))
+    b = _case(cfg, seed=13, poison=False)
+    mdl = b.models[0]
+    blocks = int(sum(-(-(int(L) + int(k)) // 32) for L, k in zip(b.ctx_lens, b.k))) * mdl.shape.Hkv
+    assert blocks > 256 * 512, blocks
+    out, _, _ = parity.run_gpu_attention(mdl, b)
+    seqs = [int(np.argmax(b.ctx_lens)), int(np.argmin(b.ctx_lens))]
+    ref, rows = parity.oracle_attention_subset(mdl, b, seqs, mdl.shape.D)
+    worst = parity.check_attention_rows(out, ref, rows, mdl.q.dtype)
+    _say(f"  {blocks} key blocks: worst rel err {worst:.2e}")
