@@ -51,13 +51,15 @@ struct LmParams {
   int vt_base, n_vt_run;   // this launch's vocabulary tiles: vt_base .. vt_base + n_vt_run - 1
   // Group records, [M][rec_stride] each: the three largest logits of the group
   // with their indices, the fourth largest value, sum exp(l - v1) over each
-  // 32-entry quarter of the group (rec_sq[q]: entries 32 q .. 32 q + 31) and
-  // sum exp(l - v1) * l over the group.
+  // 32-entry quarter of the group (rec_sq[q]: entries 32 q .. 32 q + 31), over
+  // the group (rec_s, the quarters added in pairs) and sum exp(l - v1) * l
+  // over the group.
   float* rec_v1;
   float* rec_v2;
   float* rec_v3;
   float* rec_v4;
   float* rec_sq[4];
+  float* rec_s;
   float* rec_e;
   int32_t* rec_i1;
   int32_t* rec_i2;
@@ -271,6 +273,7 @@ __device__ __forceinline__ void lm_epilogue(const LmParams& p, floatx16 (&acc)[4
       p.rec_v4[r] = v4;
 #pragma unroll
       for (int q = 0; q < 4; ++q) p.rec_sq[q][r] = (v1 == -INFINITY) ? 0.f : sq[q];
+      p.rec_s[r] = (v1 == -INFINITY) ? 0.f : (sq[0] + sq[1]) + (sq[2] + sq[3]);
       p.rec_e[r] = (v1 == -INFINITY) ? 0.f : ee;
       p.rec_i1[r] = i1;
       p.rec_i2[r] = i2;
@@ -891,10 +894,7 @@ __global__ __launch_bounds__(kMT) void lmhead_merge_kernel(LmParams p) {
     const i32x4 i1 = ld16<i32x4>(p.rec_i1 + o);
     const i32x4 i2 = ld16<i32x4>(p.rec_i2 + o);
     const i32x4 i3 = ld16<i32x4>(p.rec_i3 + o);
-    const floatx4 q0 = ld16<floatx4>(p.rec_sq[0] + o);
-    const floatx4 q1 = ld16<floatx4>(p.rec_sq[1] + o);
-    const floatx4 q2 = ld16<floatx4>(p.rec_sq[2] + o);
-    const floatx4 q3 = ld16<floatx4>(p.rec_sq[3] + o);
+    const floatx4 sg = ld16<floatx4>(p.rec_s + o);
     const floatx4 ee = ld16<floatx4>(p.rec_e + o);
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
@@ -906,7 +906,7 @@ __global__ __launch_bounds__(kMT) void lmhead_merge_kernel(LmParams p) {
       ci[kCPG * u] = ok ? i1[e] : 0x7fffffff;
       ci[kCPG * u + 1] = ok ? i2[e] : 0x7fffffff;
       ci[kCPG * u + 2] = ok ? i3[e] : 0x7fffffff;
-      rs[u] = ok ? (q0[e] + q1[e]) + (q2[e] + q3[e]) : 0.f;
+      rs[u] = ok ? sg[e] : 0.f;
       re[u] = ok ? ee[e] : 0.f;
       mx = fmaxf(mx, cv[kCPG * u]);
     }
@@ -1431,7 +1431,7 @@ LmPlan lm_plan(int M, int Hd, int V, int K, bool bf16) {
   pl.rec_stride = (pl.n_groups + 3) / 4 * 4;
   const size_t recs = (size_t)M * pl.rec_stride;
   pl.rec_bytes = recs * sizeof(float);
-  pl.hid_off = 12 * ((pl.rec_bytes + 255) / 256 * 256);
+  pl.hid_off = 13 * ((pl.rec_bytes + 255) / 256 * 256);   // the 13 record arrays, then the hidden copy
   pl.workspace_bytes = pl.hid_off + (bf16 ? (size_t)((M + 15) / 16) * 16 * Hd * 2 : 0) + 256;
   (void)K;
   return pl;
@@ -1468,6 +1468,7 @@ LmParams lm_params(const void* hidden, const void* W, int M, int Hd, int V, int 
   p.rec_i1 = reinterpret_cast<int32_t*>(ws + 9 * stride);
   p.rec_i2 = reinterpret_cast<int32_t*>(ws + 10 * stride);
   p.rec_i3 = reinterpret_cast<int32_t*>(ws + 11 * stride);
+  p.rec_s = reinterpret_cast<float*>(ws + 12 * stride);
   return p;
 }
 
