@@ -6,25 +6,34 @@
 // of the coverage rule (Eq. (5)) and the entropy.
 //
 // Kernel 1 (GEMM + epilogue).  logits^T = W . hidden^T with
-// v_mfma_f32_32x32x16_bf16 (A = 32 vocabulary rows of W, B = 32 hidden rows).
-// A workgroup owns 256 vocabulary entries x 64*RB hidden rows; both tiles are
-// staged through LDS 64 channels at a time (double buffered, 8 lanes per
-// 128-byte line on the global side, padded rows so that the MFMA operand
-// reads are bank-conflict free).  Its 2x2 waves each own 128 vocabulary
-// entries x 32*RB rows: 4 x RB MFMA blocks for 4 + RB operand reads per
-// k-step.  In the accumulator layout a lane holds one hidden row and 16
-// vocabulary entries per 32x32 block, so every per-row reduction over the
-// vocabulary is in-lane plus one exchange with lane l^32.  For each (row,
-// 128-entry group) the epilogue emits a record: the largest logit v1 and its
-// index, the second largest v2 and its index, the third largest value v3,
-// s = sum exp(l - v1) and e = sum exp(l - v1) * l.
+// v_mfma_f32_32x32x16_bf16 (fp32: 32x32x2; A = 32 vocabulary rows of W, B =
+// 32 hidden rows).  A workgroup owns 256 vocabulary entries x a tile of
+// hidden rows, and wave (wv, wr) owns 128 of the entries (one record group)
+// x a slice of the rows.  For bf16, lmhead_gemm_dlds_kernel streams both
+// operands straight into a 4-deep LDS ring of 32-channel stages, with eight
+// waves (two per SIMD; four for 64- and 192-row tiles), and keeps its
+// workgroups resident, each walking tiles; lmhead_gemm_kernel (fp32) stages
+// 32 channels through registers, double buffered, with four waves.  In the
+// accumulator layout a lane holds one hidden row and 16 vocabulary entries
+// per 32x32 block, so every per-row reduction over the vocabulary is in-lane
+// plus one exchange with lane l^32.  For each (row, 128-entry group) the
+// epilogue emits a record: the three largest logits with their indices, the
+// fourth largest value, sum exp(l - v1) over each 32-entry quarter and over
+// the group, and sum exp(l - v1) * l.
 //
 // Kernel 2 (merge, one workgroup per row).  LSE = M + log sum_g s_g e^(v1_g-M),
 // entropy = LSE - (sum_g e_g e^(v1_g-M)) / (sum_g s_g e^(v1_g-M)).  Top-K: the
-// K best of the recorded (v1, v2) candidates; a group with two picks whose
-// recorded third value reaches the K-th pick may hide further members, so
+// K best of the recorded top-3 candidates; a group with three picks whose
+// recorded fourth value reaches the K-th pick may hide further members, so
 // such a group's logits are recomputed exactly and the selection is redone --
-// the result is the exact top-K of all V logits (ties: lower index first).  The proposal's logit is one dot product.
+// the result is the exact top-K of all V logits (ties: lower index first).
+// The proposal's logit is one dot product.
+//
+// Kernel 3 (draws, sample_kernel): a categorical draw from a row's
+// distribution by inverse CDF over the group records, then the selected
+// group's quarter sums, then 32 recomputed logits -- the takeover replacement
+// of Eq. (9) and the proposer's per-row draw.  logp_gather_kernel gives the
+// log-probs of a row at listed indices (the other model's top-K support).
 #include "common.h"
 #include "kernels.h"
 
@@ -98,20 +107,11 @@ __global__ __launch_bounds__(256) void pack_w_kernel(const bf16* W, int V, int H
   *reinterpret_cast<i32x4*>(Wt + (size_t)t * 8) = x;
 }
 
-// MFMA flavour per input type.  STAGE = hidden channels per pipeline stage;
+// MFMA flavour of the register-staged kernel (fp32; bf16 always takes the
+// direct-to-LDS kernel).  STAGE = hidden channels per pipeline stage;
 // a lane supplies its k-step operand from channels koff(ks, h) of the stage
 // (h = lane / 32).  Any bijection works as long as A and B agree.
 template <typename DT> struct Mm;
-
-template <> struct Mm<bf16> {
-  static constexpr int STAGE = 64;
-  static constexpr int KSTEPS = STAGE / 16;
-  typedef bf16x8 frag;
-  __device__ static floatx16 mma(frag a, frag b, floatx16 c) {
-    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
-  }
-  __device__ static int koff(int ks, int h) { return 16 * ks + 8 * h; }
-};
 
 template <> struct Mm<float> {
   static constexpr int STAGE = 32;
@@ -406,9 +406,9 @@ __global__ __launch_bounds__(256) void lmhead_gemm_kernel(LmParams p) {
 // bf16 GEMM with direct-to-LDS operand loads (global_load_lds_dwordx4).
 //
 // Each 16-byte load lands straight in LDS (lane i of an instruction fills
-// bytes 16 i .. 16 i + 15 of a 1 KB block), so no registers stage the tiles
-// and a 4-deep LDS ring keeps three 32-channel stages in flight while the
-// fourth is multiplied.  Rows are 64 bytes; the 16-byte chunk c of row r sits
+// bytes 16 i .. 16 i + 15 of a 1 KB block), so no registers stage the tiles.
+// In a 4-deep LDS ring of 32-channel stages, two stages are in flight while
+// one is multiplied and the one before it is still being read.  Rows are 64 bytes; the 16-byte chunk c of row r sits
 // at position c ^ ((r / 4) % 4), which puts the 16 rows an MFMA operand read
 // touches in distinct bank groups; the loading lane fetches the global chunk
 // that belongs at its position.
@@ -1357,11 +1357,7 @@ void launch_gemm(const LmParams& p, dim3 grid, hipStream_t st, bf16) {
   // 192 rows four.  The direct-to-LDS kernels read the hidden rows from a
   // copy in W's tiled block layout, written first into the workspace, so
   // that every operand load reads whole cache lines.
-  if (p.Hd % kDStage != 0) {
-    trace_mark(st);   // no hidden copy on this path: an empty interval
-    hipLaunchKernelGGL((lmhead_gemm_kernel<bf16, RB>), grid, dim3(256), 0, st, p);
-    return;
-  }
+  // Hd is a multiple of 64 (the host checks), so of the 32-channel stage.
   const size_t n_chunks = (size_t)((p.M + 15) / 16) * 16 * p.Hd / 8;
   hipLaunchKernelGGL(pack_w_kernel, dim3((unsigned)((n_chunks + 255) / 256)), dim3(256), 0, st,
                      reinterpret_cast<const bf16*>(p.hidden), p.M, p.Hd,

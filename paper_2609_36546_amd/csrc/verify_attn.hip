@@ -7,8 +7,11 @@
 // proposer's tokens are appended to it): for sequence b with L cached tokens
 // and a k-row window, row i attends to keys 0 .. L+i of its KV head.
 //
-// The window's keys and values are first appended to the pages by a small
-// kernel, so the attention kernel streams every key the same way.
+// The window's keys and values are appended to the pages first, so the
+// attention streams every key, window or cached, the same way: by the
+// stream-K kernel itself (each workgroup writes the window positions inside
+// its own key blocks before it reads any), or by a small kernel ahead of the
+// register kernel.
 //
 // Work decomposition.  The query rows of one (sequence, KV head) -- k window
 // positions x G = Hq/Hkv heads -- are packed position-major into groups of up
@@ -37,11 +40,13 @@
 // log-sum-exp form, unless the sequence fits in one chunk (then the
 // workgroup writes the output itself).
 //
-// Full 64-row groups of bf16 D = 128 heads in 16-token pages (the teacher
-// shapes) take a second kernel, verify_attn_sk_kernel below: persistent
-// workgroups, one 16-row tile per wave, keys streamed through an LDS ring
-// with direct-to-LDS loads, and the key blocks of all groups split evenly
-// between workgroups (stream-K).  Both kernels share the block arithmetic
+// bf16 D = 128 heads in 16-token pages (every bf16 workload), when the
+// kernel's LDS tables fit, take a second kernel, verify_attn_sk_kernel below:
+// persistent workgroups whose waves own one or two 16-row tiles (items of 64
+// or 128 rows of one (sequence, KV head)), keys and values streamed through
+// an LDS ring with direct-to-LDS loads, and the key blocks of all items split
+// evenly between workgroups (stream-K); items split between workgroups are
+// merged by attn_combine_sk_kernel.  Both kernels share the block arithmetic
 // (attend_block) and the pool layouts.
 #include <algorithm>
 #include <mutex>
