@@ -288,9 +288,9 @@ def work_per_launch(batch):
         # each row i attends to L + i + 1 keys: QK^T and PV
         res["attention"][1] += (4.0 * sh.Hq * sh.D * (k * (L + 1) + k * (k - 1) / 2)).sum()
         M = float(m.hidden.shape[0])
-        # W and the hidden rows once, plus the group records (twelve 4-byte
+        # W and the hidden rows once, plus the group records (eleven 4-byte
         # values per row and 128-entry group)
-        res["lmhead_gemm"][0] += (sh.vocab + M) * sh.hidden * s + M * -(-sh.vocab // 128) * 48
+        res["lmhead_gemm"][0] += (sh.vocab + M) * sh.hidden * s + M * -(-sh.vocab // 128) * 44
         res["lmhead_gemm"][1] += 2.0 * M * sh.vocab * sh.hidden
     return res
 

@@ -58,8 +58,9 @@ struct LmParams {
   int n_groups, n_rt, n_vt;
   int rec_stride;          // record entries per row: n_groups rounded up to a multiple of 4
   int vt_base, n_vt_run;   // this launch's vocabulary tiles: vt_base .. vt_base + n_vt_run - 1
-  // Group records, [M][rec_stride] each: the three largest logits of the group
-  // with their indices, the fourth largest value, sum exp(l - v1) over each
+  // Group records, [M][rec_stride] each: the three largest logits of the group,
+  // their positions in it (rec_i: 7 bits each, i1 | i2 << 7 | i3 << 14; any
+  // value where the logit is -inf), the fourth largest value, sum exp(l - v1) over each
   // 32-entry quarter of the group (rec_sq[q]: entries 32 q .. 32 q + 31), over
   // the group (rec_s, the quarters added in pairs) and sum exp(l - v1) * l
   // over the group.
@@ -70,9 +71,7 @@ struct LmParams {
   float* rec_sq[4];
   float* rec_s;
   float* rec_e;
-  int32_t* rec_i1;
-  int32_t* rec_i2;
-  int32_t* rec_i3;
+  int32_t* rec_i;
   float* lse;
   float* logp_prop;
   int32_t* argmax;
@@ -275,9 +274,8 @@ __device__ __forceinline__ void lm_epilogue(const LmParams& p, floatx16 (&acc)[4
       for (int q = 0; q < 4; ++q) p.rec_sq[q][r] = (v1 == -INFINITY) ? 0.f : sq[q];
       p.rec_s[r] = (v1 == -INFINITY) ? 0.f : (sq[0] + sq[1]) + (sq[2] + sq[3]);
       p.rec_e[r] = (v1 == -INFINITY) ? 0.f : ee;
-      p.rec_i1[r] = i1;
-      p.rec_i2[r] = i2;
-      p.rec_i3[r] = i3;
+      const int gb = kGroup * g;   // the group's first entry
+      p.rec_i[r] = ((i1 - gb) & 127) | (((i2 - gb) & 127) << 7) | (((i3 - gb) & 127) << 14);
     }
   }
 }
@@ -891,9 +889,7 @@ __global__ __launch_bounds__(kMT) void lmhead_merge_kernel(LmParams p) {
     const floatx4 v1 = ld16<floatx4>(p.rec_v1 + o);
     const floatx4 v2 = ld16<floatx4>(p.rec_v2 + o);
     const floatx4 v3 = ld16<floatx4>(p.rec_v3 + o);
-    const i32x4 i1 = ld16<i32x4>(p.rec_i1 + o);
-    const i32x4 i2 = ld16<i32x4>(p.rec_i2 + o);
-    const i32x4 i3 = ld16<i32x4>(p.rec_i3 + o);
+    const i32x4 ix = ld16<i32x4>(p.rec_i + o);
     const floatx4 sg = ld16<floatx4>(p.rec_s + o);
     const floatx4 ee = ld16<floatx4>(p.rec_e + o);
 #pragma unroll
@@ -903,9 +899,12 @@ __global__ __launch_bounds__(kMT) void lmhead_merge_kernel(LmParams p) {
       cv[kCPG * u] = ok ? v1[e] : -INFINITY;
       cv[kCPG * u + 1] = ok ? v2[e] : -INFINITY;
       cv[kCPG * u + 2] = ok ? v3[e] : -INFINITY;
-      ci[kCPG * u] = ok ? i1[e] : 0x7fffffff;
-      ci[kCPG * u + 1] = ok ? i2[e] : 0x7fffffff;
-      ci[kCPG * u + 2] = ok ? i3[e] : 0x7fffffff;
+      // indices from the group's first entry and the packed positions; an
+      // entry holding -inf has none
+      const int gb = kGroup * (g4 + e);
+      ci[kCPG * u] = (ok & (v1[e] != -INFINITY)) ? gb + (ix[e] & 127) : 0x7fffffff;
+      ci[kCPG * u + 1] = (ok & (v2[e] != -INFINITY)) ? gb + ((ix[e] >> 7) & 127) : 0x7fffffff;
+      ci[kCPG * u + 2] = (ok & (v3[e] != -INFINITY)) ? gb + ((ix[e] >> 14) & 127) : 0x7fffffff;
       rs[u] = ok ? sg[e] : 0.f;
       re[u] = ok ? ee[e] : 0.f;
       mx = fmaxf(mx, cv[kCPG * u]);
@@ -1427,7 +1426,7 @@ LmPlan lm_plan(int M, int Hd, int V, int K, bool bf16) {
   pl.rec_stride = (pl.n_groups + 3) / 4 * 4;
   const size_t recs = (size_t)M * pl.rec_stride;
   pl.rec_bytes = recs * sizeof(float);
-  pl.hid_off = 13 * ((pl.rec_bytes + 255) / 256 * 256);   // the 13 record arrays, then the hidden copy
+  pl.hid_off = 11 * ((pl.rec_bytes + 255) / 256 * 256);   // the 11 record arrays, then the hidden copy
   pl.workspace_bytes = pl.hid_off + (bf16 ? (size_t)((M + 15) / 16) * 16 * Hd * 2 : 0) + 256;
   (void)K;
   return pl;
@@ -1461,10 +1460,8 @@ LmParams lm_params(const void* hidden, const void* W, int M, int Hd, int V, int 
   p.rec_v4 = reinterpret_cast<float*>(ws + 3 * stride);
   for (int q = 0; q < 4; ++q) p.rec_sq[q] = reinterpret_cast<float*>(ws + (4 + q) * stride);
   p.rec_e = reinterpret_cast<float*>(ws + 8 * stride);
-  p.rec_i1 = reinterpret_cast<int32_t*>(ws + 9 * stride);
-  p.rec_i2 = reinterpret_cast<int32_t*>(ws + 10 * stride);
-  p.rec_i3 = reinterpret_cast<int32_t*>(ws + 11 * stride);
-  p.rec_s = reinterpret_cast<float*>(ws + 12 * stride);
+  p.rec_i = reinterpret_cast<int32_t*>(ws + 9 * stride);
+  p.rec_s = reinterpret_cast<float*>(ws + 10 * stride);
   return p;
 }
 
