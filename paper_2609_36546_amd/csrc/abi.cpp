@@ -6,8 +6,6 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
-#include <cstdlib>
-#include <cstring>
 #include <unordered_map>
 #include <vector>
 

@@ -25,10 +25,6 @@ __device__ __forceinline__ V ld16(const void* p) {
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 __device__ __forceinline__ float fast_log2(float x) { return __builtin_amdgcn_logf(x); }
 
-__device__ __forceinline__ float wave_max_xor(float v, int mask) {
-  return fmaxf(v, __shfl_xor(v, mask, kWave));
-}
-
 // ---- wave reductions and scans with DPP moves (VALU, no LDS round trip) ----
 // DPP controls (GFX9): quad_perm p0 | p1 << 2 | p2 << 4 | p3 << 6, row_shr:n
 // 0x110 + n, row_mirror 0x140, row_half_mirror 0x141.  Rows are 16 lanes.

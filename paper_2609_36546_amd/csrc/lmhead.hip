@@ -37,8 +37,6 @@
 #include "common.h"
 #include "kernels.h"
 
-#include <cstdlib>
-
 namespace ipdv {
 namespace {
 
@@ -619,18 +617,6 @@ __global__ __launch_bounds__(64 * NW) void lmhead_gemm_dlds_kernel(LmParams p) {
 // ---------------------------------------------------------------------------
 
 constexpr int kMT = 256;
-
-
-__device__ float block_sum(float x, float* s) {
-  x = wave_sum(x);
-  const int w = threadIdx.x >> 6;
-  __syncthreads();
-  if (lane_id() == 0) s[w] = x;
-  __syncthreads();
-  float t = 0.f;
-  for (int ww = 0; ww < kMT / kWave; ++ww) t += s[ww];
-  return t;
-}
 
 // Block sums of three values at once (s holds 3 * waves floats).
 __device__ void block_sum3(float& a, float& b, float& c, float* s) {
