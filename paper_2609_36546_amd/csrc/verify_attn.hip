@@ -1172,8 +1172,8 @@ AttnPlan attn_plan(int n_seq, int Hq, int Hkv, int D, int max_q, int max_pages, 
   pl.part_o_bytes = slots * kRows * D * sizeof(float);
   pl.part_lse_bytes = slots * kRows * sizeof(float);
   pl.workspace_bytes = pl.part_o_bytes + pl.part_lse_bytes + 256;
-  // Full 64-row groups of 16-slot D = 128 pages take the persistent stream-K
-  // kernel (bf16; the launch checks the type) when its LDS tables fit: item
+  // D = 128 heads in 16-slot pages take the persistent stream-K kernel (bf16;
+  // the launch checks the type) when its LDS tables fit: item
   // starts and non-empty counts, sequence data, and per workgroup two page
   // ids per block and one record per unit (a share is at most every item at
   // its largest block count over the grid; its units add sk_qt per item).

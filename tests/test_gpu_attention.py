@@ -69,6 +69,19 @@ def test_empty_windows_and_row_groups(B, ks, lo, hi, seed):
     _check_all(_case(cfg, seed=seed))
 
 
+@pytest.mark.parametrize("Hq,Hkv,ks,seed", [(32, 2, (16, 5, 0), 21), (32, 4, (24, 17, 3), 22)])
+def test_stream_k_several_row_groups(Hq, Hkv, ks, seed):
+    """More than 128 query rows per (sequence, KV head) -- 16 query heads per
+    KV head with 16-token windows (256 rows), or 8 with 24-token windows (192
+    rows) -- so the stream-K kernel has two 128-row items over the same keys,
+    the second partly filled or without rows, and both items' workgroups
+    append the same window positions."""
+    shape = inputs.ModelShape("wide-groups", Hq=Hq, Hkv=Hkv, D=128, hidden=64, vocab=512)
+    cfg = inputs.scaled(inputs.WORKLOADS["teacher-bf16"], B=5, ctx_lo=0, ctx_hi=2500, k_choices=ks,
+                        models=(shape,))
+    _check_all(_case(cfg, seed=seed))
+
+
 @pytest.mark.parametrize("ps", [32, 64])
 def test_other_page_sizes(ps):
     cfg = inputs.scaled(inputs.WORKLOADS["teacher-bf16"], B=3, ctx_lo=10, ctx_hi=900, page_size=ps,

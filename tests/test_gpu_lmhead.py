@@ -51,12 +51,15 @@ def test_tiny_fp32_config():
 @pytest.mark.parametrize("M,Hd,V,K", [(40, 2048, 151936, 16), (300, 256, 5003, 32),
                                       (1, 64, 64, 1), (129, 512, 2048, 4), (33, 128, 100, 32),
                                       (7, 4096, 262144, 16), (3, 4096, 262143, 32),
-                                      (100, 256, 151936, 16), (160, 256, 151936, 8)])
+                                      (100, 256, 151936, 16), (160, 256, 151936, 8),
+                                      (700, 256, 50000, 16), (1024, 128, 30000, 8)])
 def test_bf16_shapes(M, Hd, V, K):
     """Includes the largest supported shape (V = 262144, Hd = 4096) and a
     ragged last group at that size.  M = 100 and 160 take the 128-row and the
     192-row tiles with 594 vocabulary tiles, so every persistent workgroup
-    runs two or three tiles (M = 40, 7 and 3 do so with 64-row tiles)."""
+    runs two or three tiles (M = 40, 7 and 3 do so with 64-row tiles).  M =
+    700 and 1024 have three and four 256-row tiles (the last one ragged at
+    700), 588 and 472 tile numbers, so a workgroup's walk crosses row tiles."""
     _say(f"[lmhead] bf16 M={M} Hd={Hd} V={V} K={K}")
     h, W, prop = _rand(M, Hd, V, torch.bfloat16, M + V)
     _check(h, W, prop, K)
