@@ -83,6 +83,7 @@ struct AttnParams {
   int max_chunks, n_qg, n_seq;
   float scale_log2;   // softmax scale * log2(e)
   int32_t* sk_start;  // stream-K: first block of every item (written by the attention kernel)
+  int32_t* sk_ne;     // stream-K: non-empty items before every item (written with sk_start)
   int sk_grid;        // stream-K: persistent workgroups
   int item_rows;      // stream-K: packed query rows per item (64, or 128 with two tiles per wave)
 };
@@ -602,6 +603,16 @@ template <bool TAIL> struct LdsFrags {
   }
 };
 
+// The stream-K split charges each non-empty item's start this many quarter
+// blocks on top of its blocks: a piece of an item costs its workgroup the
+// item's QT query units and a partial (or output) write besides its key
+// blocks (per-workgroup timelines: a share that spans two items ended 4 us
+// later at 64-row items and 8 us later at 128-row items).  Four blocks per 64
+// rows timed best of 1.5, 2.5, 4 and 6.  Share w is the blocks whose cost
+// start lies in [C w / W, C (w + 1) / W), C the total cost, so shares that
+// start items take fewer blocks.
+__host__ __device__ constexpr int sk_item_cost(int qt) { return 16 * qt; }
+
 // Item `it` = (sequence slot, KV head g, row group qg), it = (slot Hkv + g) n_qg + qg:
 // the row groups of one (sequence, head) are neighbours, so the shares that
 // read the same keys for them run at the same time and the second read is a
@@ -680,35 +691,56 @@ __global__ __launch_bounds__(256, 2) void verify_attn_sk_kernel(AttnParams a) {
       s_part[0][t] = inc_r;
       s_part[1][t] = inc_c;
     }
+    if (tid == 0) {   // no claim yet: the share's bound is then the last block's end
+      s_part[0][4] = s_part[0][5] = -1;
+      s_part[1][4] = s_part[1][5] = -1;
+    }
     __syncthreads();
-    int bs = inc_r - run, ns = inc_c - cnt;
+    int bs = inc_r - run, ns = inc_c - cnt, NE = 0;
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
       B_tot += s_part[0][k];
+      NE += s_part[1][k];
       if (k < t) {
         bs += s_part[0][k];
         ns += s_part[1][k];
       }
     }
-    // Share [lo, hi) of the blocks; 32-bit arithmetic while B_tot * W fits.
+    // Share w: the blocks whose cost start lies in [y_lo, y_hi), in quarter
+    // blocks (sk_item_cost); 32-bit arithmetic while C * W fits.
+    constexpr int c4 = sk_item_cost(QT);
     W = min((int)gridDim.x, B_tot);
+    const int C = 4 * B_tot + c4 * NE;
+    int y_lo = 0, y_hi = 0;
     if (w < W) {
-      if (B_tot < (1 << 22) && W <= 1024) {
-        lo = (int)((unsigned)B_tot * (unsigned)w / (unsigned)W);
-        hi = (int)((unsigned)B_tot * (unsigned)(w + 1) / (unsigned)W);
+      if (C < (1 << 22) && W <= 1024) {
+        y_lo = (int)((unsigned)C * (unsigned)w / (unsigned)W);
+        y_hi = (int)((unsigned)C * (unsigned)(w + 1) / (unsigned)W);
       } else {
-        lo = (int)((long)B_tot * w / W);
-        hi = (int)((long)B_tot * (w + 1) / W);
+        y_lo = (int)((long)C * w / W);
+        y_hi = (int)((long)C * (w + 1) / W);
       }
     }
-    // Item offsets, and the items that hold the share's first and last
-    // blocks (each found by the one thread that owns it).
+    // Item offsets, and the share's bounds: the first block whose cost start
+    // reaches y_lo (y_hi), claimed by the one thread that owns its item.
+    // Block x of non-empty item i costs from 4 x + c4 (ne_i + 1); the block
+    // before the item's first (the previous non-empty item's last) from
+    // 4 bs_i - 4 + c4 ne_i.
     for (int i = i_lo; i < i_hi; ++i) {
       const int nb = s_start[i];
       s_start[i] = bs;
       s_ne[i] = ns;
-      if (bs <= lo && lo < bs + nb) s_part[0][4] = i;
-      if (bs < hi && hi <= bs + nb) s_part[1][4] = i;
+      if (nb > 0 && w < W) {
+        const int cs = 4 * bs + c4 * (ns + 1), ce = cs + 4 * (nb - 1);
+        if (y_lo <= ce && (bs == 0 || cs - 4 - c4 < y_lo)) {
+          s_part[0][4] = i;
+          s_part[0][5] = bs + max(0, (y_lo - cs + 3) >> 2);
+        }
+        if (y_hi <= ce && (bs == 0 || cs - 4 - c4 < y_hi)) {
+          s_part[1][4] = i;
+          s_part[1][5] = bs + max(0, (y_hi - cs + 3) >> 2);
+        }
+      }
       bs += nb;
       ns += nb > 0;
     }
@@ -716,9 +748,14 @@ __global__ __launch_bounds__(256, 2) void verify_attn_sk_kernel(AttnParams a) {
   }
   __syncthreads();
   if (blockIdx.x == 0)
-    for (int i = tid; i <= n_it; i += 256) a.sk_start[i] = s_start[i];
+    for (int i = tid; i <= n_it; i += 256) {
+      a.sk_start[i] = s_start[i];
+      a.sk_ne[i] = s_ne[i];
+    }
   if (w >= W) return;
-  const int i_first = uni(s_part[0][4]), i_last = uni(s_part[1][4]);
+  lo = uni(s_part[0][5] < 0 ? B_tot : s_part[0][5]);
+  hi = uni(s_part[1][5] < 0 ? B_tot : s_part[1][5]);
+  if (lo >= hi) return;   // a share of no blocks: its cost span lies in item starts
   // Item of block x among items l0 .. l1: s_start[i] <= x < s_start[i + 1]
   // (empty items never qualify).
   auto item_of = [&](int x, int l0, int l1) {
@@ -728,6 +765,10 @@ __global__ __launch_bounds__(256, 2) void verify_attn_sk_kernel(AttnParams a) {
     }
     return l0;
   };
+  // The share's first block lies in the item that claimed it; its last block
+  // in that of the block after it or an earlier one.
+  const int i_first = uni(s_part[0][4]);
+  const int i_last = uni(item_of(hi - 1, i_first, s_part[1][4] >= 0 ? s_part[1][4] : n_it - 1));
   const int n_units = (hi - lo) + QT * (s_ne[i_last + 1] - s_ne[i_first]);
   if (2 * (n_it + 1) + 4 * a.n_seq + 2 * (hi - lo) + n_units > kSkMeta) return;
   int* s_uq = s_pg + 2 * (hi - lo);          // [n_units] the workgroup's units, in order
@@ -1009,9 +1050,16 @@ __global__ __launch_bounds__(256) void attn_combine_sk_kernel(AttnParams a) {
   const int r0 = a.cu_q[b];
   const int kb = a.cu_q[b + 1] - r0;
   if (s1 <= s0) return;
+  const int NE = a.sk_ne[n_it], ne = a.sk_ne[it];
   const int W = min(a.sk_grid, B_tot);
-  // Workgroup whose share [B w / W, B (w+1) / W) holds block x.
-  auto wg_of = [&](int x) { return min(W - 1, (int)(((long)(x + 1) * W - 1) / B_tot)); };
+  // Workgroup whose share holds block x: the last w with C w / W at or below
+  // the block's cost start 4 x + c4 (ne + 1) (the attention kernel's split).
+  const int c4 = sk_item_cost(R / 64);
+  const long C = 4L * B_tot + (long)c4 * NE;
+  auto wg_of = [&](int x) {
+    const long cx = 4L * x + (long)c4 * (ne + 1);
+    return min(W - 1, (int)(((cx + 1) * W - 1) / C));
+  };
   const int w0 = wg_of(s0), w1 = wg_of(s1 - 1);
   if (w0 == w1) return;   // written whole by one workgroup
   const int G = a.G;
@@ -1173,25 +1221,28 @@ AttnPlan attn_plan(int n_seq, int Hq, int Hkv, int D, int max_q, int max_pages, 
   pl.part_lse_bytes = slots * kRows * sizeof(float);
   pl.workspace_bytes = pl.part_o_bytes + pl.part_lse_bytes + 256;
   // D = 128 heads in 16-slot pages take the persistent stream-K kernel (bf16;
-  // the launch checks the type) when its LDS tables fit: item
-  // starts and non-empty counts, sequence data, and per workgroup two page
-  // ids per block and one record per unit (a share is at most every item at
-  // its largest block count over the grid; its units add sk_qt per item).
+  // the launch checks the type) when its LDS tables fit: item starts and
+  // non-empty counts, sequence data, and per workgroup two page ids per
+  // block and one record per unit (its units add sk_qt per item).
   // More than 64 rows per (sequence, KV head) take 128-row items, two 16-row
   // tiles per wave, so that each key is read once per 128 rows.
   pl.sk_qt = rows > kRows ? 2 : 1;
   pl.sk_n_qg = (int)((rows + 64L * pl.sk_qt - 1) / (64L * pl.sk_qt));
   const long n_it = (long)n_seq * Hkv * pl.sk_n_qg;
   const long maxblk = (max_keys + kBlk - 1) / kBlk;
-  const long share = (n_it * maxblk + kSkGrid - 1) / kSkGrid;
-  pl.sk = D == 128 && page_size == 16 &&
+  // A share spans at most C / W quarter blocks of cost (C = 4 blocks + c4
+  // per non-empty item, W = min(grid, blocks)), so it holds at most that / 4
+  // + 1 blocks; costs stay below 2^31.
+  const long c4 = sk_item_cost(pl.sk_qt);
+  const long share = std::max((n_it * (4 * maxblk + c4) + 4L * kSkGrid - 1) / (4L * kSkGrid), (c4 + 3) / 4 + 1) + 1;
+  pl.sk = D == 128 && page_size == 16 && n_it * (4 * maxblk + c4) < (1L << 31) &&
           2 * (n_it + 1) + 4L * n_seq + 3 * share + pl.sk_qt * n_it <= kSkMeta;
   if (pl.sk) {
     const size_t sk_slots = (size_t)n_it + kSkGrid;
     const size_t sk_rows = 64 * (size_t)pl.sk_qt;
     pl.sk_o_bytes = std::max(pl.part_o_bytes, sk_slots * sk_rows * D * sizeof(float));
     pl.sk_lse_bytes = std::max(pl.part_lse_bytes, sk_slots * sk_rows * sizeof(float));
-    pl.workspace_bytes = pl.sk_o_bytes + pl.sk_lse_bytes + (n_it + 1) * sizeof(int32_t) + 256;
+    pl.workspace_bytes = pl.sk_o_bytes + pl.sk_lse_bytes + 2 * (n_it + 1) * sizeof(int32_t) + 256;
   }
   return pl;
 }
@@ -1272,6 +1323,7 @@ hipError_t launch_verify_attn(const AttnLaunch& L, const AttnPlan& pl, hipStream
   if (pl.sk && L.dtype_bf16 && L.D == 128 && L.page_size == 16) {
     p.part_lse = reinterpret_cast<float*>(reinterpret_cast<char*>(L.workspace) + pl.sk_o_bytes);
     p.sk_start = reinterpret_cast<int32_t*>(reinterpret_cast<char*>(L.workspace) + pl.sk_o_bytes + pl.sk_lse_bytes);
+    p.sk_ne = p.sk_start + ((size_t)L.n_seq * L.Hkv * pl.sk_n_qg + 1);
     p.sk_grid = kSkGrid;
     p.n_qg = pl.sk_n_qg;
     p.item_rows = 64 * pl.sk_qt;
