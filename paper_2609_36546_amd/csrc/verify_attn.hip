@@ -613,6 +613,19 @@ template <bool TAIL> struct LdsFrags {
 // start items take fewer blocks.
 __host__ __device__ constexpr int sk_item_cost(int qt) { return 16 * qt; }
 
+// Relative cost spans of the stream-K shares by XCD.  The hardware deals
+// workgroup ids to the eight XCDs round-robin, so workgroup w runs on XCD
+// w % 8; with equal shares, the odd-numbered XCDs streamed this access
+// pattern 6-10% slower than the even ones on every box and shape measured
+// (per-workgroup timelines), so an odd workgroup's span is kSkWO / kSkWE of
+// an even one's.  Only while the shares average at least 8 blocks: then no
+// span is shorter than one block's cost, so every workgroup between the
+// first and the last piece of an item holds a block of it.
+constexpr int kSkWE = 12, kSkWO = 11;
+__host__ __device__ constexpr bool sk_xcd_weighted(long blocks, long W) { return blocks >= 8 * W; }
+// Cost-span prefix of workgroups 0 .. v-1.
+__host__ __device__ inline long sk_span_prefix(long v, int we, int wo) { return we * ((v + 1) >> 1) + wo * (v >> 1); }
+
 // Item `it` = (sequence slot, KV head g, row group qg), it = (slot Hkv + g) n_qg + qg:
 // the row groups of one (sequence, head) are neighbours, so the shares that
 // read the same keys for them run at the same time and the second read is a
@@ -707,19 +720,17 @@ __global__ __launch_bounds__(256, 2) void verify_attn_sk_kernel(AttnParams a) {
       }
     }
     // Share w: the blocks whose cost start lies in [y_lo, y_hi), in quarter
-    // blocks (sk_item_cost); 32-bit arithmetic while C * W fits.
+    // blocks (sk_item_cost), the cost spans weighted by XCD (kSkWE, kSkWO).
     constexpr int c4 = sk_item_cost(QT);
     W = min((int)gridDim.x, B_tot);
     const int C = 4 * B_tot + c4 * NE;
+    const bool xw = sk_xcd_weighted(B_tot, W);
+    const int we = xw ? kSkWE : 1, wo = xw ? kSkWO : 1;
+    const long SW = sk_span_prefix(W, we, wo);
     int y_lo = 0, y_hi = 0;
     if (w < W) {
-      if (C < (1 << 22) && W <= 1024) {
-        y_lo = (int)((unsigned)C * (unsigned)w / (unsigned)W);
-        y_hi = (int)((unsigned)C * (unsigned)(w + 1) / (unsigned)W);
-      } else {
-        y_lo = (int)((long)C * w / W);
-        y_hi = (int)((long)C * (w + 1) / W);
-      }
+      y_lo = (int)((long)C * sk_span_prefix(w, we, wo) / SW);
+      y_hi = (int)((long)C * sk_span_prefix(w + 1, we, wo) / SW);
     }
     // Item offsets, and the share's bounds: the first block whose cost start
     // reaches y_lo (y_hi), claimed by the one thread that owns its item.
@@ -1052,13 +1063,19 @@ __global__ __launch_bounds__(256) void attn_combine_sk_kernel(AttnParams a) {
   if (s1 <= s0) return;
   const int NE = a.sk_ne[n_it], ne = a.sk_ne[it];
   const int W = min(a.sk_grid, B_tot);
-  // Workgroup whose share holds block x: the last w with C w / W at or below
-  // the block's cost start 4 x + c4 (ne + 1) (the attention kernel's split).
+  // Workgroup whose share holds block x: the last w whose span starts, at
+  // C S(w) / S(W), at or below the block's cost start 4 x + c4 (ne + 1) (the
+  // attention kernel's split; S the XCD-weighted span prefix).
   const int c4 = sk_item_cost(R / 64);
   const long C = 4L * B_tot + (long)c4 * NE;
+  const bool xw = sk_xcd_weighted(B_tot, W);
+  const int we = xw ? kSkWE : 1, wo = xw ? kSkWO : 1;
+  const long SW = sk_span_prefix(W, we, wo);
   auto wg_of = [&](int x) {
     const long cx = 4L * x + (long)c4 * (ne + 1);
-    return min(W - 1, (int)(((cx + 1) * W - 1) / C));
+    const long v = ((cx + 1) * SW + C - 1) / C - 1;   // the largest S(w) allowed
+    const long k = v / (we + wo), rem = v % (we + wo);
+    return min(W - 1, (int)(2 * k + (rem >= we ? 1 : 0)));
   };
   const int w0 = wg_of(s0), w1 = wg_of(s1 - 1);
   if (w0 == w1) return;   // written whole by one workgroup
@@ -1230,11 +1247,13 @@ AttnPlan attn_plan(int n_seq, int Hq, int Hkv, int D, int max_q, int max_pages, 
   pl.sk_n_qg = (int)((rows + 64L * pl.sk_qt - 1) / (64L * pl.sk_qt));
   const long n_it = (long)n_seq * Hkv * pl.sk_n_qg;
   const long maxblk = (max_keys + kBlk - 1) / kBlk;
-  // A share spans at most C / W quarter blocks of cost (C = 4 blocks + c4
-  // per non-empty item, W = min(grid, blocks)), so it holds at most that / 4
-  // + 1 blocks; costs stay below 2^31.
+  // A share spans at most C max(kSkWE, kSkWO) / S(W) + 1 quarter blocks of
+  // cost (C = 4 blocks + c4 per non-empty item; with the XCD weights W is
+  // the full grid, and S(W) >= (W (kSkWE + kSkWO) - max) / 2), so it holds at
+  // most that / 4 + 1 blocks; costs stay below 2^31.
   const long c4 = sk_item_cost(pl.sk_qt);
-  const long share = std::max((n_it * (4 * maxblk + c4) + 4L * kSkGrid - 1) / (4L * kSkGrid), (c4 + 3) / 4 + 1) + 1;
+  const long wmax = std::max(kSkWE, kSkWO), wden = 4L * (kSkGrid * (long)(kSkWE + kSkWO) - wmax);
+  const long share = std::max((n_it * (4 * maxblk + c4) * 2 * wmax + wden - 1) / wden, (c4 + 3) / 4 + 1) + 2;
   pl.sk = D == 128 && page_size == 16 && n_it * (4 * maxblk + c4) < (1L << 31) &&
           2 * (n_it + 1) + 4L * n_seq + 3 * share + pl.sk_qt * n_it <= kSkMeta;
   if (pl.sk) {
