@@ -65,6 +65,9 @@ struct AttnLaunch {
   void* workspace;
 };
 
+// Compute units of the current device (cached per device; 256 if unknown).
+int device_cus();
+
 AttnPlan attn_plan(int n_seq, int Hq, int Hkv, int D, int max_q, int max_pages, int page_size);
 hipError_t launch_verify_attn(const AttnLaunch& L, const AttnPlan& pl, hipStream_t st);
 // The same launches with the split-KV partials in the library's per-device

@@ -1296,20 +1296,6 @@ __global__ __launch_bounds__(kMT) void sample_kernel(LmParams p, SampleParams s)
 
 // GEMM launch per input type: bf16 takes the direct-to-LDS kernel when the
 // hidden size is a multiple of four stages, fp32 the register-staged one.
-// Compute units of the current device (cached per device).
-int device_cus() {
-  static int cus[64] = {};
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-  if (cus[dev] == 0) {
-    int n = 0;
-    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
-      n = 256;
-    cus[dev] = n;
-  }
-  return cus[dev];
-}
-
 dim3 gemm_grid(const LmParams& p) { return dim3((p.n_vt_run + 7) / 8 * 8 * p.n_rt); }
 
 // Launch of the persistent direct-to-LDS GEMM: as many workgroups as the
@@ -1398,6 +1384,20 @@ hipError_t launch_rb(const LmParams& p, hipStream_t st) {
 }
 
 }  // namespace
+
+// Compute units of the current device (cached per device; 256 if unknown).
+int device_cus() {
+  static int cus[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cus[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+      n = 256;
+    cus[dev] = n;
+  }
+  return cus[dev];
+}
 
 LmPlan lm_plan(int M, int Hd, int V, int K, bool bf16) {
   LmPlan pl{};

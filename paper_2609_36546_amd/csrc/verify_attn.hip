@@ -86,6 +86,7 @@ struct AttnParams {
   int32_t* sk_ne;     // stream-K: non-empty items before every item (written with sk_start)
   int sk_grid;        // stream-K: persistent workgroups
   int item_rows;      // stream-K: packed query rows per item (64, or 128 with two tiles per wave)
+  int sk_first;       // stream-K: workgroups dispatched first on their CU (the CU count)
 };
 
 template <typename DT, int D> struct Frags;
@@ -613,18 +614,43 @@ template <bool TAIL> struct LdsFrags {
 // start items take fewer blocks.
 __host__ __device__ constexpr int sk_item_cost(int qt) { return 16 * qt; }
 
-// Relative cost spans of the stream-K shares by XCD.  The hardware deals
-// workgroup ids to the eight XCDs round-robin, so workgroup w runs on XCD
-// w % 8; with equal shares, the odd-numbered XCDs streamed this access
-// pattern 6-10% slower than the even ones on every box and shape measured
-// (per-workgroup timelines), so an odd workgroup's span is kSkWO / kSkWE of
-// an even one's.  Only while the shares average at least 8 blocks: then no
-// span is shorter than one block's cost, so every workgroup between the
-// first and the last piece of an item holds a block of it.
-constexpr int kSkWE = 12, kSkWO = 11;
-__host__ __device__ constexpr bool sk_xcd_weighted(long blocks, long W) { return blocks >= 8 * W; }
-// Cost-span prefix of workgroups 0 .. v-1.
-__host__ __device__ inline long sk_span_prefix(long v, int we, int wo) { return we * ((v + 1) >> 1) + wo * (v >> 1); }
+// Relative cost spans of the stream-K shares.  The hardware deals workgroup
+// ids to the eight XCDs round-robin and gives each CU one workgroup before it
+// gives any a second, so workgroup w runs on XCD w % 8, first on its CU when
+// w < F (F = the CU count).  With equal shares (per-workgroup timelines, every
+// box and shape measured) the odd-numbered XCDs streamed 6-10% slower than the
+// even ones, and a CU's second workgroup 5-10% slower than its first, which
+// ended first on almost every CU (its waves are the older ones).  Spans:
+// kSkSpan = {first even, first odd, second even, second odd}.  Only while the
+// shares average at least 8 blocks (and F is even): then no span is shorter
+// than one block's cost, so every workgroup between the first and the last
+// piece of an item holds a block of it.
+struct SkSpan {
+  int e1, o1, e2, o2, F;
+};
+constexpr int kSkSpan[4] = {24, 22, 21, 19};
+__host__ __device__ inline SkSpan sk_spans(long blocks, int W, int first) {
+  if (blocks >= 8L * W && first > 0 && first % 2 == 0) return {kSkSpan[0], kSkSpan[1], kSkSpan[2], kSkSpan[3], first};
+  return {1, 1, 1, 1, 0};
+}
+__host__ __device__ inline long sk_pre(long v, int e, int o) { return e * ((v + 1) >> 1) + o * (v >> 1); }
+// Total span of workgroups 0 .. v-1.
+__host__ __device__ inline long sk_span_prefix(long v, const SkSpan& p) {
+  return v <= p.F ? sk_pre(v, p.e1, p.o1) : sk_pre(p.F, p.e1, p.o1) + sk_pre(v - p.F, p.e2, p.o2);
+}
+// The last workgroup (below W) whose span prefix is at most V.
+__host__ __device__ inline int sk_span_owner(long V, int W, const SkSpan& p) {
+  const long SF = sk_pre(p.F, p.e1, p.o1);
+  long w;
+  if (p.F >= W || V < SF) {
+    const long k = V / (p.e1 + p.o1), r = V % (p.e1 + p.o1);
+    w = 2 * k + (r >= p.e1 ? 1 : 0);
+  } else {
+    const long k = (V - SF) / (p.e2 + p.o2), r = (V - SF) % (p.e2 + p.o2);
+    w = p.F + 2 * k + (r >= p.e2 ? 1 : 0);
+  }
+  return (int)(w < W - 1 ? w : W - 1);
+}
 
 // Item `it` = (sequence slot, KV head g, row group qg), it = (slot Hkv + g) n_qg + qg:
 // the row groups of one (sequence, head) are neighbours, so the shares that
@@ -720,17 +746,16 @@ __global__ __launch_bounds__(256, 2) void verify_attn_sk_kernel(AttnParams a) {
       }
     }
     // Share w: the blocks whose cost start lies in [y_lo, y_hi), in quarter
-    // blocks (sk_item_cost), the cost spans weighted by XCD (kSkWE, kSkWO).
+    // blocks (sk_item_cost), the spans weighted by XCD and CU slot (kSkSpan).
     constexpr int c4 = sk_item_cost(QT);
     W = min((int)gridDim.x, B_tot);
     const int C = 4 * B_tot + c4 * NE;
-    const bool xw = sk_xcd_weighted(B_tot, W);
-    const int we = xw ? kSkWE : 1, wo = xw ? kSkWO : 1;
-    const long SW = sk_span_prefix(W, we, wo);
+    const SkSpan sp = sk_spans(B_tot, W, a.sk_first);
+    const long SW = sk_span_prefix(W, sp);
     int y_lo = 0, y_hi = 0;
     if (w < W) {
-      y_lo = (int)((long)C * sk_span_prefix(w, we, wo) / SW);
-      y_hi = (int)((long)C * sk_span_prefix(w + 1, we, wo) / SW);
+      y_lo = (int)((long)C * sk_span_prefix(w, sp) / SW);
+      y_hi = (int)((long)C * sk_span_prefix(w + 1, sp) / SW);
     }
     // Item offsets, and the share's bounds: the first block whose cost start
     // reaches y_lo (y_hi), claimed by the one thread that owns its item.
@@ -1065,17 +1090,14 @@ __global__ __launch_bounds__(256) void attn_combine_sk_kernel(AttnParams a) {
   const int W = min(a.sk_grid, B_tot);
   // Workgroup whose share holds block x: the last w whose span starts, at
   // C S(w) / S(W), at or below the block's cost start 4 x + c4 (ne + 1) (the
-  // attention kernel's split; S the XCD-weighted span prefix).
+  // attention kernel's split; S the weighted span prefix).
   const int c4 = sk_item_cost(R / 64);
   const long C = 4L * B_tot + (long)c4 * NE;
-  const bool xw = sk_xcd_weighted(B_tot, W);
-  const int we = xw ? kSkWE : 1, wo = xw ? kSkWO : 1;
-  const long SW = sk_span_prefix(W, we, wo);
+  const SkSpan sp = sk_spans(B_tot, W, a.sk_first);
+  const long SW = sk_span_prefix(W, sp);
   auto wg_of = [&](int x) {
     const long cx = 4L * x + (long)c4 * (ne + 1);
-    const long v = ((cx + 1) * SW + C - 1) / C - 1;   // the largest S(w) allowed
-    const long k = v / (we + wo), rem = v % (we + wo);
-    return min(W - 1, (int)(2 * k + (rem >= we ? 1 : 0)));
+    return sk_span_owner(((cx + 1) * SW + C - 1) / C - 1, W, sp);   // the largest S(w) allowed
   };
   const int w0 = wg_of(s0), w1 = wg_of(s1 - 1);
   if (w0 == w1) return;   // written whole by one workgroup
@@ -1247,13 +1269,15 @@ AttnPlan attn_plan(int n_seq, int Hq, int Hkv, int D, int max_q, int max_pages, 
   pl.sk_n_qg = (int)((rows + 64L * pl.sk_qt - 1) / (64L * pl.sk_qt));
   const long n_it = (long)n_seq * Hkv * pl.sk_n_qg;
   const long maxblk = (max_keys + kBlk - 1) / kBlk;
-  // A share spans at most C max(kSkWE, kSkWO) / S(W) + 1 quarter blocks of
-  // cost (C = 4 blocks + c4 per non-empty item; with the XCD weights W is
-  // the full grid, and S(W) >= (W (kSkWE + kSkWO) - max) / 2), so it holds at
-  // most that / 4 + 1 blocks; costs stay below 2^31.
+  // A share spans at most C wmax / S(W) + 1 quarter blocks of cost (C = 4
+  // blocks + c4 per non-empty item; with the span weights W is the full grid
+  // and S(W) >= W wmin), so it holds at most that / 4 + 1 blocks; costs stay
+  // below 2^31.
   const long c4 = sk_item_cost(pl.sk_qt);
-  const long wmax = std::max(kSkWE, kSkWO), wden = 4L * (kSkGrid * (long)(kSkWE + kSkWO) - wmax);
-  const long share = std::max((n_it * (4 * maxblk + c4) * 2 * wmax + wden - 1) / wden, (c4 + 3) / 4 + 1) + 2;
+  const long wmax = std::max(std::max(kSkSpan[0], kSkSpan[1]), std::max(kSkSpan[2], kSkSpan[3]));
+  const long wmin = std::min(std::min(kSkSpan[0], kSkSpan[1]), std::min(kSkSpan[2], kSkSpan[3]));
+  const long wden = 4L * kSkGrid * wmin;
+  const long share = std::max((n_it * (4 * maxblk + c4) * wmax + wden - 1) / wden, (c4 + 3) / 4 + 1) + 2;
   pl.sk = D == 128 && page_size == 16 && n_it * (4 * maxblk + c4) < (1L << 31) &&
           2 * (n_it + 1) + 4L * n_seq + 3 * share + pl.sk_qt * n_it <= kSkMeta;
   if (pl.sk) {
@@ -1344,6 +1368,7 @@ hipError_t launch_verify_attn(const AttnLaunch& L, const AttnPlan& pl, hipStream
     p.sk_start = reinterpret_cast<int32_t*>(reinterpret_cast<char*>(L.workspace) + pl.sk_o_bytes + pl.sk_lse_bytes);
     p.sk_ne = p.sk_start + ((size_t)L.n_seq * L.Hkv * pl.sk_n_qg + 1);
     p.sk_grid = kSkGrid;
+    p.sk_first = device_cus();
     p.n_qg = pl.sk_n_qg;
     p.item_rows = 64 * pl.sk_qt;
     return launch_sk(p, dim3(pl.sk_n_qg, L.n_seq * L.Hkv), st);
