@@ -82,6 +82,21 @@ def test_stream_k_several_row_groups(Hq, Hkv, ks, seed):
     _check_all(_case(cfg, seed=seed))
 
 
+@pytest.mark.parametrize("lo,hi,seed,weighted", [(480, 540, 31, True), (400, 470, 32, False)])
+def test_stream_k_split_near_the_weight_threshold(lo, hi, seed, weighted):
+    """64 teacher-head sequences whose key blocks average just above (4256)
+    or just below (3660) eight per workgroup: the stream-K split weights its
+    spans by XCD and CU slot only from eight blocks per share on, where its
+    shortest spans still hold a block, so every workgroup between an item's
+    first and last piece has written a partial for the combine."""
+    cfg = inputs.scaled(inputs.WORKLOADS["teacher-bf16"], B=64, ctx_lo=lo, ctx_hi=hi,
+                        models=(inputs.scaled_shape(inputs.TEACHER, vocab=512, hidden=64),))
+    b = _case(cfg, seed=seed)
+    blocks = int(sum(-(-(int(L) + int(k)) // 32) for L, k in zip(b.ctx_lens, b.k))) * b.models[0].shape.Hkv
+    assert (blocks >= 8 * 512) == weighted, blocks
+    _check_all(b)
+
+
 @pytest.mark.parametrize("ps", [32, 64])
 def test_other_page_sizes(ps):
     cfg = inputs.scaled(inputs.WORKLOADS["teacher-bf16"], B=3, ctx_lo=10, ctx_hi=900, page_size=ps,
